@@ -1,0 +1,279 @@
+/*
+ * m2c.h -- C ABI of the MI355X (gfx950) dynamic sparse mixed-precision FFN
+ * with a neuron-level HBM slot cache (M2Cache, arXiv 2410.14740).
+ *
+ * One decode step of one FFN layer is four calls, in this order:
+ *
+ *   m2c_predict_rank  score every FFN neuron with the layer's low-rank
+ *                     predictor, take the top-k, split them into FP16 / INT8 /
+ *                     INT4 tiers by score rank            (Sec. 1 "Active Neuron
+ *                     Identification" and "Active Score-based Quantization";
+ *                     Sec. 5.2, Fig. 3)
+ *   m2c_cache_plan    resolve the active neurons against the layer's HBM slot
+ *                     cache: hit / refill / new / bypass, LRU victims, slot
+ *                     table update                        (Sec. 5.3 "Overall
+ *                     architecture" and "Cache Policy"; Sec. 1 LRU cache)
+ *   m2c_cache_fill    copy every missing neuron record, at its tier, from the
+ *                     pinned host-DRAM neuron store into its slot (Sec. 1
+ *                     "Selective Loading into GPU"; Sec. 6.1 dedicated streams)
+ *   m2c_sparse_ffn    gated FFN over only the active neurons, each read from
+ *                     its slot and dequantized at its tier (Sec. 1, Sec. 5.2)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - All functions return an m2c_status. On an error detected on the host
+ *   nothing is enqueued, the layer is unchanged and m2c_last_error() returns
+ *   a message (thread-local). Nothing throws across the ABI.
+ * - "dev" pointers are device memory of the layer's device; "host" pointers
+ *   are ordinary host memory. The caller owns every pointer it passes.
+ * - Streams are hipStream_t values passed as void*; NULL is the null stream.
+ *   Asynchronous calls only enqueue work on the given stream and return.
+ *   Ordering between streams (for example the fill stream and the FFN
+ *   stream) is the caller's job, with events.
+ * - fp16 values are passed as their IEEE binary16 bit patterns (uint16_t).
+ *
+ * Neuron and tiers (Sec. 1 footnote, Sec. 5.2)
+ * --------------------------------------------
+ * Neuron i of a SwiGLU FFN with W_gate, W_up [d_ff][d_model] and
+ * W_down [d_model][d_ff] is row i of W_gate, row i of W_up and column i of
+ * W_down. Tier codes: 0 inactive, 1 INT4, 2 INT8, 3 FP16 (higher score ->
+ * higher precision, Sec. 5.2).
+ *
+ * Neuron records (the unit that is stored, copied and cached)
+ * ----------------------------------------------------------
+ * d = d_model, G = d / 128 (quantization group of 128 consecutive elements).
+ *   FP16 record (tier 3), 6d bytes:
+ *     gate[d] fp16 | up[d] fp16 | down[d] fp16
+ *   INT8 record (tier 2), 3d + 6G bytes:
+ *     gate[d] int8 | up[d] int8 | down[d] int8 |
+ *     gate_scale[G] fp16 | up_scale[G] fp16 | down_scale[G] fp16
+ *   INT4 record (tier 1), 1.5d + 6G bytes:
+ *     gate[d/2] | up[d/2] | down[d/2] | gate_scale[G] | up_scale[G] | down_scale[G]
+ *     byte m of a vector holds element 2m in bits 0-3 and element 2m+1 in
+ *     bits 4-7, each a two's-complement nibble.
+ * Quantization (symmetric, per group g of one vector, qmax = 127 or 7):
+ *     amax = max |w| over the group (w are the fp16 weights),
+ *     s    = fp16_rne( fp32(amax) / qmax )        (IEEE fp32 division),
+ *     q    = clamp( rne( fp32(w) / fp32(s) ), -qmax, qmax ), q = 0 if s == 0,
+ *     dequantized weight = q * s (exact in fp32).
+ * Records of tier t are stored back to back with a stride of
+ * record_stride[t] = record_bytes[t] rounded up to 16 bytes.
+ *
+ * Predictor scores (Sec. 5.2; low-rank predictor of Sec. 1)
+ * ---------------------------------------------------------
+ *   z = A x  (A [r][d] fp16),   s = B z + bias  (B [d_ff][r] fp16, bias fp32).
+ * Every dot product is evaluated in fp32 in one fixed order, so that scores
+ * (and therefore the selected ids) are reproducible bit for bit:
+ *   n-element dot product, n % 8 == 0: split into chunks of 8 consecutive
+ *   elements; L = min(64, largest power of two <= n/8) partial sums; chunk c
+ *   belongs to partial c % L; each partial starts at +0.0f and takes
+ *   acc = fmaf(a_j, b_j, acc) over its chunks in ascending order, elements in
+ *   ascending order inside a chunk; then for off = L/2, L/4, ..., 1 every
+ *   partial p becomes p[l] + p[l ^ off]; the result is p[0]. z stays fp32;
+ *   the bias, when present, is one fp32 addition after the dot product.
+ *
+ * Selection and tiers (Sec. 5.2)
+ * ------------------------------
+ * Neurons are ranked by score descending, ties by id ascending; scores are
+ * compared as order-preserving unsigned keys of their fp32 bit patterns
+ * (so -0.0 ranks below +0.0). Rank rho < n_fp16 -> tier 3;
+ * rho < n_fp16 + n_int8 -> tier 2; rho < k -> tier 1; else tier 0.
+ *
+ * Cache policy (Sec. 5.3; LRU of Sec. 1 and Sec. 6.4)
+ * ---------------------------------------------------
+ * One cache unit per layer: C resident slots plus S staging slots, each
+ * slot_bytes = 6d bytes (an FP16 record). The required set R of a step is
+ * every neuron with tier > 0 in some batch row, taken at the highest tier any
+ * row asks for. The step is atomic: for i in R (ascending id)
+ *   HIT     i is resident at the requested tier;
+ *   REFILL  i is resident at another tier: it is refilled in its own slot;
+ *   NEW     i is not resident.
+ * Victims are the slots holding no neuron of R, ordered by (last use
+ * ascending, slot ascending); never-used slots count as last use -1. The j-th
+ * NEW neuron in ascending id takes the j-th victim and evicts its previous
+ * neuron. NEW neurons beyond the number of victims are BYPASS: they are
+ * filled into staging slot C + j' (j' counts bypasses in ascending id) and
+ * are not retained. Every slot of R gets last use = step. With C = k and a
+ * single tier this reduces to the paper's Adjacent Token Update policy.
+ */
+#ifndef M2C_H
+#define M2C_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  M2C_OK = 0,
+  M2C_ERR_INVALID_ARG = 1,  /* bad pointer, size, count or descriptor        */
+  M2C_ERR_OUT_OF_MEMORY = 2,/* device or pinned host allocation failed       */
+  M2C_ERR_HIP = 3,          /* a HIP runtime call failed (message has detail)*/
+  M2C_ERR_CAPACITY = 4,     /* a size beyond what the layer was created for  */
+  M2C_ERR_STATE = 5         /* call out of order (e.g. step not increasing)  */
+} m2c_status;
+
+typedef struct m2c_layer m2c_layer; /* opaque; one per FFN layer */
+
+enum { M2C_TIER_NONE = 0, M2C_TIER_INT4 = 1, M2C_TIER_INT8 = 2, M2C_TIER_FP16 = 3 };
+
+/* Layer descriptor. All fields are required. */
+typedef struct {
+  int32_t d_model;       /* d: multiple of 128, 128..65536                      */
+  int32_t d_ff;          /* neurons: 1..262144                                  */
+  int32_t pred_rank;     /* r: multiple of 8, 8..4096                           */
+  int32_t group;         /* quantization group; must be 128                     */
+  int32_t k_max;         /* largest k any call will use: 0..d_ff                */
+  int32_t max_batch;     /* largest batch any call will use: 1..32              */
+  int32_t cache_slots;   /* C: resident slots, 0..d_ff                          */
+  int32_t staging_slots; /* S: bypass slots; -1 = the minimum that can never
+                            overflow, max(0, min(d_ff, max_batch*k_max) - C);
+                            smaller explicit values are rejected               */
+  int32_t device;        /* HIP device ordinal                                  */
+} m2c_layer_desc;
+
+/* Sizes that follow from a descriptor. */
+typedef struct {
+  int32_t record_bytes[4];  /* by tier; [0] = 0                               */
+  int32_t record_stride[4]; /* host store stride by tier; [0] = 0             */
+  int32_t slot_bytes;       /* 6 * d_model                                    */
+  int32_t cache_slots;      /* C                                              */
+  int32_t staging_slots;    /* S (resolved)                                   */
+  int32_t plan_capacity;    /* entries of every plan list: min(d_ff, max_batch*k_max) */
+  int64_t plan_bytes;       /* size of one plan buffer                        */
+  int64_t host_store_bytes; /* pinned host neuron store (all three tiers)     */
+  int64_t device_bytes;     /* device memory the layer owns                   */
+} m2c_layer_info;
+
+/* A plan is one caller-allocated device buffer of info.plan_bytes bytes,
+ * 256-byte aligned. These are the byte offsets of its arrays; every list has
+ * plan_capacity entries of which counts[...] are valid. */
+enum {
+  M2C_CNT_REQ = 0,     /* |R|                                                 */
+  M2C_CNT_HIT = 1,
+  M2C_CNT_REFILL = 2,
+  M2C_CNT_NEW = 3,     /* NEW that got a resident victim slot                 */
+  M2C_CNT_BYPASS = 4,  /* NEW that went to a staging slot                     */
+  M2C_CNT_EVICT = 5,   /* victims that held a neuron                          */
+  M2C_CNT_FILL = 6,    /* REFILL + NEW + BYPASS                               */
+  M2C_CNT_REQ_FP16 = 7,/* |R| by tier                                         */
+  M2C_CNT_REQ_INT8 = 8,
+  M2C_CNT_REQ_INT4 = 9,
+  M2C_CNT_FILL_FP16 = 10, /* fills by tier                                    */
+  M2C_CNT_FILL_INT8 = 11,
+  M2C_CNT_FILL_INT4 = 12,
+  M2C_NCOUNTS = 16
+};
+typedef struct {
+  int64_t counts;      /* int32 [M2C_NCOUNTS]                                 */
+  int64_t req_ids;     /* int32 [cap] R in ascending neuron id                */
+  int64_t req_tier;    /* uint8 [cap] tier taken for the step (max over rows) */
+  int64_t req_hit;     /* uint8 [cap] 0 NEW, 1 HIT, 2 REFILL, 3 BYPASS        */
+  int64_t req_slot;    /* int32 [cap] slot read by the FFN                    */
+  int64_t req_mask;    /* uint32[cap] bit b set if batch row b selected it    */
+  int64_t fill_ids;    /* int32 [cap] misses in ascending neuron id           */
+  int64_t fill_tier;   /* uint8 [cap]                                         */
+  int64_t fill_slot;   /* int32 [cap]                                         */
+  int64_t evicted_ids; /* int32 [cap] evicted neurons in victim order         */
+  int64_t work_slot;   /* int32 [cap] R regrouped tier-major (FP16, INT8,
+                          INT4), ascending id inside a tier: FFN work order    */
+  int64_t work_mask;   /* uint32[cap] row masks in work order                 */
+  int64_t total_bytes;
+} m2c_plan_layout;
+
+/* Cumulative per-layer counters since creation or the last cache reset. */
+typedef struct {
+  int64_t plans;
+  int64_t req, hit, refill, new_, bypass, evict;
+  int64_t fill[4];        /* fills by tier                                    */
+  int64_t fill_bytes;     /* sum of record_bytes over fills                   */
+} m2c_stats;
+
+/* Bytes of one neuron record of `tier` (1..3) for d_model d, or -1. */
+int64_t m2c_record_bytes(int32_t d_model, int32_t tier);
+
+/* Create a layer (Sec. 5.3 isolated cache unit + the layer's share of the
+ * host-DRAM neuron store). Host inputs, copied; may be freed on return:
+ *   w_gate, w_up  [d_ff][d_model] fp16; w_down [d_model][d_ff] fp16;
+ *   pred_a [pred_rank][d_model] fp16;  pred_b [d_ff][pred_rank] fp16;
+ *   score_bias [d_ff] fp32 or NULL (no addition).
+ * Quantizes every neuron to the INT8 and INT4 records on the device and keeps
+ * all three records in pinned host memory; the cache starts cold.
+ * Synchronous. */
+m2c_status m2c_layer_create(const m2c_layer_desc* desc, const uint16_t* w_gate,
+                            const uint16_t* w_up, const uint16_t* w_down,
+                            const uint16_t* pred_a, const uint16_t* pred_b,
+                            const float* score_bias, m2c_layer** out);
+
+/* Create a layer that reads its neuron records from the host store of
+ * `weights_of` (same d_model, d_ff and device) instead of owning a copy; it
+ * has its own predictor, slot cache and tables. The store lives until every
+ * layer using it is destroyed. Synchronous. */
+m2c_status m2c_layer_create_shared(const m2c_layer_desc* desc, const m2c_layer* weights_of,
+                                   const uint16_t* pred_a, const uint16_t* pred_b,
+                                   const float* score_bias, m2c_layer** out);
+
+/* Wait for the device, then free everything the layer owns. NULL is a no-op. */
+m2c_status m2c_layer_destroy(m2c_layer* layer);
+
+m2c_status m2c_layer_get_info(const m2c_layer* layer, m2c_layer_info* out);
+m2c_status m2c_plan_get_layout(const m2c_layer* layer, m2c_plan_layout* out);
+
+/* Scores and tiers for `batch` tokens.
+ *   x        dev fp16 [batch][d_model]
+ *   scores   dev fp32 [batch][d_ff] output, or NULL (kept internally)
+ *   tier_map dev uint8 [batch][d_ff] output, tier of every neuron
+ * 0 <= n_fp16, 0 <= n_int8, n_fp16 + n_int8 <= k <= k_max, 1 <= batch <= max_batch. */
+m2c_status m2c_predict_rank(m2c_layer* layer, const uint16_t* x, int32_t batch, int32_t k,
+                            int32_t n_fp16, int32_t n_int8, float* scores, uint8_t* tier_map,
+                            void* stream);
+
+/* Resolve tier_map (dev uint8 [batch][d_ff]) against the slot cache for
+ * decode step `step`, write the plan into `plan` (dev, plan_bytes) and update
+ * the slot tables. `step` must be >= 0, < 2^31 and strictly greater than the
+ * previous step given to this layer (M2C_ERR_STATE otherwise). The plan must
+ * not be reused until every fill and FFN that reads it has completed. */
+m2c_status m2c_cache_plan(m2c_layer* layer, const uint8_t* tier_map, int32_t batch, int64_t step,
+                          void* plan, void* stream);
+
+/* Copy every fill of `plan` from the pinned host store into its slot, on
+ * `stream`, by a device gather kernel that reads host memory over the host
+ * link. Must run after the plan on the same stream or behind an event, and
+ * before the FFN that reads the plan. No host synchronization. */
+m2c_status m2c_cache_fill(m2c_layer* layer, const void* plan, void* stream);
+
+/* y = sum over i in R of silu(<g_i, x>) * <u_i, x> * d_i, per batch row b over
+ * the neurons whose req_mask has bit b, every vector dequantized at the
+ * neuron's step tier; fp32 accumulation.
+ *   x dev fp16 [batch][d_model];  y dev fp32 [batch][d_model] output.
+ * `batch` must equal the batch given to the plan. */
+m2c_status m2c_sparse_ffn(m2c_layer* layer, const uint16_t* x, int32_t batch, const void* plan,
+                          float* y, void* stream);
+
+/* Make the cache cold again (all slots empty, stats zeroed, step history
+ * cleared), on `stream`. */
+m2c_status m2c_layer_reset_cache(m2c_layer* layer, void* stream);
+
+/* Synchronizes the device, then reads the cumulative counters. */
+m2c_status m2c_layer_stats(const m2c_layer* layer, m2c_stats* out);
+
+/* Test support. Copies one record of the host store (no device work). */
+m2c_status m2c_debug_read_record(const m2c_layer* layer, int32_t tier, int32_t neuron, void* out,
+                                 size_t bytes);
+/* Test support. Synchronizes the device, then copies slot `slot` (0..C+S-1). */
+m2c_status m2c_debug_read_slot(const m2c_layer* layer, int32_t slot, void* out, size_t bytes);
+/* Test support. Synchronizes the device, then copies the slot tables; any
+ * pointer may be NULL. slot_of int32 [d_ff] (-1 = not resident);
+ * slot_key int32 [C] (-1 = empty); slot_tier uint8 [C]; slot_last int32 [C]. */
+m2c_status m2c_debug_read_tables(const m2c_layer* layer, int32_t* slot_of, int32_t* slot_key,
+                                 uint8_t* slot_tier, int32_t* slot_last);
+
+/* Message of the last error on this thread ("" if none). */
+const char* m2c_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* M2C_H */
