@@ -1,0 +1,543 @@
+// Host side of the m2c C ABI: argument checking, the layer object, the
+// pinned host neuron store, create-time quantization and the entry points.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <new>
+
+#include "m2c_internal.h"
+
+using m2c::Store;
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+m2c_status fail(m2c_status code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+m2c_status hip_fail(hipError_t e, const char* what) {
+  if (e == hipErrorOutOfMemory)
+    return fail(M2C_ERR_OUT_OF_MEMORY, "%s: %s", what, hipGetErrorString(e));
+  return fail(M2C_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIPOK(call, what)                   \
+  do {                                      \
+    hipError_t e_ = (call);                 \
+    if (e_ != hipSuccess) {                 \
+      (void)hipGetLastError();              \
+      return hip_fail(e_, what);            \
+    }                                       \
+  } while (0)
+
+// Makes `dev` current for the scope and restores the caller's device.
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = false;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+int64_t rec_bytes(int d, int tier) {
+  const int64_t G = d / 128;
+  if (tier == 3) return 6LL * d;
+  if (tier == 2) return 3LL * d + 6 * G;
+  if (tier == 1) return 3LL * d / 2 + 6 * G;
+  return -1;
+}
+
+m2c_status check_desc(const m2c_layer_desc* D, int* S_out, int* cap_out) {
+  if (!D) return fail(M2C_ERR_INVALID_ARG, "desc is NULL");
+  if (D->d_model < 128 || D->d_model > 16384 || D->d_model % 128)
+    return fail(M2C_ERR_INVALID_ARG, "d_model %d: need a multiple of 128 in [128, 16384]",
+                D->d_model);
+  if (D->d_ff < 1 || D->d_ff > 262144)
+    return fail(M2C_ERR_INVALID_ARG, "d_ff %d: need [1, 262144]", D->d_ff);
+  if (D->pred_rank < 8 || D->pred_rank > 1024 || D->pred_rank % 8)
+    return fail(M2C_ERR_INVALID_ARG, "pred_rank %d: need a multiple of 8 in [8, 1024]",
+                D->pred_rank);
+  if (D->group != 128) return fail(M2C_ERR_INVALID_ARG, "group %d: only 128 is supported", D->group);
+  if (D->k_max < 0 || D->k_max > D->d_ff)
+    return fail(M2C_ERR_INVALID_ARG, "k_max %d: need [0, d_ff]", D->k_max);
+  if (D->max_batch < 1 || D->max_batch > 32)
+    return fail(M2C_ERR_INVALID_ARG, "max_batch %d: need [1, 32]", D->max_batch);
+  if (D->cache_slots < 0 || D->cache_slots > D->d_ff)
+    return fail(M2C_ERR_INVALID_ARG, "cache_slots %d: need [0, d_ff]", D->cache_slots);
+  const int64_t cap64 = (int64_t)D->max_batch * D->k_max;
+  const int cap = (int)(cap64 < D->d_ff ? cap64 : D->d_ff);
+  const int need = cap - D->cache_slots > 0 ? cap - D->cache_slots : 0;
+  int S = D->staging_slots;
+  if (S == -1) S = need;
+  if (S < need)
+    return fail(M2C_ERR_INVALID_ARG, "staging_slots %d: at least %d are needed (or -1)",
+                D->staging_slots, need);
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || D->device < 0 || D->device >= ndev)
+    return fail(M2C_ERR_INVALID_ARG, "device %d: %d HIP devices visible", D->device, ndev);
+  *S_out = S;
+  *cap_out = cap;
+  return M2C_OK;
+}
+
+void fill_info_layout(m2c_layer* L) {
+  const m2c_layer_desc& D = L->desc;
+  m2c_layer_info& I = L->info;
+  memset(&I, 0, sizeof(I));
+  for (int t = 1; t <= 3; ++t) {
+    I.record_bytes[t] = (int32_t)rec_bytes(D.d_model, t);
+    I.record_stride[t] = (int32_t)round_up(rec_bytes(D.d_model, t), 16);
+  }
+  I.slot_bytes = 6 * D.d_model;
+  I.cache_slots = D.cache_slots;
+  I.staging_slots = L->S;
+  I.plan_capacity = L->cap;
+  m2c_plan_layout& P = L->layout;
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    int64_t o = off;
+    off = round_up(off + (bytes > 0 ? bytes : 1), 256);
+    return o;
+  };
+  const int64_t c = L->cap;
+  P.counts = take(4 * M2C_NCOUNTS);
+  P.req_ids = take(4 * c);
+  P.req_tier = take(c);
+  P.req_hit = take(c);
+  P.req_slot = take(4 * c);
+  P.req_mask = take(4 * c);
+  P.fill_ids = take(4 * c);
+  P.fill_tier = take(c);
+  P.fill_slot = take(4 * c);
+  P.evicted_ids = take(4 * c);
+  P.work_slot = take(4 * c);
+  P.work_mask = take(4 * c);
+  P.total_bytes = off;
+  I.plan_bytes = off;
+}
+
+void release_store(Store* s) {
+  if (!s) return;
+  if (--s->refs > 0) return;
+  for (int t = 1; t <= 3; ++t)
+    if (s->host[t]) (void)hipHostFree(s->host[t]);
+  delete s;
+}
+
+void free_layer(m2c_layer* L) {
+  if (!L) return;
+  {
+    DeviceGuard g(L->desc.device);
+    if (L->dev_base) {
+      (void)hipDeviceSynchronize();
+      (void)hipFree(L->dev_base);
+    }
+    release_store(L->store);
+  }
+  delete L;
+}
+
+// Device memory of a layer: one allocation, carved in 256-byte pieces.
+m2c_status alloc_device(m2c_layer* L, bool with_bias) {
+  const m2c_layer_desc& D = L->desc;
+  const int64_t d = D.d_model, dff = D.d_ff, r = D.pred_rank, C = D.cache_slots;
+  const int64_t cap = L->cap, mb = D.max_batch;
+  const int n_slices = (int)((d + 511) / 512);
+  int ng = 512 / n_slices;
+  if (ng < 1) ng = 1;
+  if (ng > 32) ng = 32;
+  const int ng_cap = (int)(cap / 16 > 1 ? cap / 16 : 1);
+  if (ng > ng_cap) ng = ng_cap;
+  L->ffn_groups = ng;
+  struct Piece { void** dst; int64_t bytes; };
+  void* p_pred_a; void* p_pred_b; void* p_bias; void* p_z; void* p_scores; void* p_slots;
+  void* p_h; void* p_ypart; void* p_ctr; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
+  void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
+  void* p_vslot; void* p_vold; void* p_stats;
+  Piece pieces[] = {
+      {&p_slots, (C + L->S) * (int64_t)L->info.slot_bytes},
+      {&p_pred_a, r * d * 2},
+      {&p_pred_b, dff * r * 2},
+      {&p_bias, with_bias ? dff * 4 : 0},
+      {&p_z, mb * r * 4},
+      {&p_scores, mb * dff * 4},
+      {&p_h, cap * mb * 4},
+      {&p_ypart, (int64_t)ng * mb * d * 4},
+      {&p_ctr, 64},
+      {&p_slot_of, dff * 4},
+      {&p_slot_key, C * 4},
+      {&p_slot_tier, C},
+      {&p_slot_last, C * 4},
+      {&p_lru, 2 * C * 4},
+      {&p_lru_cur, 4},
+      {&p_new_pos, cap * 4},
+      {&p_work_pos, cap * 4},
+      {&p_vslot, cap * 4},
+      {&p_vold, cap * 4},
+      {&p_stats, 16 * 8},
+  };
+  int64_t total = 0;
+  int64_t offs[sizeof(pieces) / sizeof(pieces[0])];
+  for (size_t q = 0; q < sizeof(pieces) / sizeof(pieces[0]); ++q) {
+    offs[q] = total;
+    total = round_up(total + (pieces[q].bytes > 0 ? pieces[q].bytes : 1), 256);
+  }
+  void* base = nullptr;
+  HIPOK(hipMalloc(&base, total), "hipMalloc(layer device memory)");
+  L->dev_base = (uint8_t*)base;
+  L->dev_bytes = total;
+  for (size_t q = 0; q < sizeof(pieces) / sizeof(pieces[0]); ++q)
+    *pieces[q].dst = L->dev_base + offs[q];
+  L->slots = (uint8_t*)p_slots;
+  L->pred_a = (uint16_t*)p_pred_a;
+  L->pred_b = (uint16_t*)p_pred_b;
+  L->bias = with_bias ? (float*)p_bias : nullptr;
+  L->z = (float*)p_z;
+  L->scores = (float*)p_scores;
+  L->h = (float*)p_h;
+  L->y_part = (float*)p_ypart;
+  L->ffn_ctr = (int32_t*)p_ctr;
+  L->st.slot_of = (int32_t*)p_slot_of;
+  L->st.slot_key = (int32_t*)p_slot_key;
+  L->st.slot_tier = (uint8_t*)p_slot_tier;
+  L->st.slot_last = (int32_t*)p_slot_last;
+  L->st.lru = (int32_t*)p_lru;
+  L->st.lru_cur = (int32_t*)p_lru_cur;
+  L->st.new_pos = (int32_t*)p_new_pos;
+  L->st.work_pos = (int32_t*)p_work_pos;
+  L->st.vict_slot = (int32_t*)p_vslot;
+  L->st.vict_old = (int32_t*)p_vold;
+  L->st.stats = (unsigned long long*)p_stats;
+  L->info.device_bytes = total;
+  HIPOK(hipMemset(p_ctr, 0, 64), "hipMemset(work counters)");
+  return M2C_OK;
+}
+
+m2c_status upload_predictor(m2c_layer* L, const uint16_t* pred_a, const uint16_t* pred_b,
+                            const float* bias) {
+  const m2c_layer_desc& D = L->desc;
+  HIPOK(hipMemcpy(L->pred_a, pred_a, (size_t)D.pred_rank * D.d_model * 2, hipMemcpyHostToDevice),
+        "upload pred_a");
+  HIPOK(hipMemcpy(L->pred_b, pred_b, (size_t)D.d_ff * D.pred_rank * 2, hipMemcpyHostToDevice),
+        "upload pred_b");
+  if (bias)
+    HIPOK(hipMemcpy(L->bias, bias, (size_t)D.d_ff * 4, hipMemcpyHostToDevice), "upload bias");
+  HIPOK(m2c::launch_reset(L, 0), "reset kernel");
+  HIPOK(hipDeviceSynchronize(), "layer init");
+  return M2C_OK;
+}
+
+// Builds the three records of every neuron on the device and copies them
+// into the pinned store.
+m2c_status build_store(m2c_layer* L, const uint16_t* w_gate, const uint16_t* w_up,
+                       const uint16_t* w_down) {
+  const int d = L->desc.d_model, dff = L->desc.d_ff;
+  Store* S = L->store;
+  for (int t = 1; t <= 3; ++t) {
+    void* p = nullptr;
+    HIPOK(hipHostMalloc(&p, (size_t)dff * S->stride[t], hipHostMallocDefault),
+          "hipHostMalloc(neuron store)");
+    S->host[t] = (uint8_t*)p;
+    S->bytes += (int64_t)dff * S->stride[t];
+  }
+  const size_t wbytes = (size_t)dff * d * 2;
+  const int chunk = dff < 4096 ? dff : 4096;
+  const size_t rbytes = (size_t)chunk * (S->stride[1] + S->stride[2] + S->stride[3]);
+  void *wg = nullptr, *wu = nullptr, *wd = nullptr, *wdT = nullptr, *rec = nullptr;
+  m2c_status rc = M2C_OK;
+  hipError_t e = hipMalloc(&wg, wbytes);
+  if (e == hipSuccess) e = hipMalloc(&wu, wbytes);
+  if (e == hipSuccess) e = hipMalloc(&wd, wbytes);
+  if (e == hipSuccess) e = hipMalloc(&wdT, wbytes);
+  if (e == hipSuccess) e = hipMalloc(&rec, rbytes);
+  if (e == hipSuccess) e = hipMemcpy(wg, w_gate, wbytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(wu, w_up, wbytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(wd, w_down, wbytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = m2c::launch_transpose_u16((const uint16_t*)wd, (uint16_t*)wdT, d, dff, 0);
+  uint8_t* r16 = (uint8_t*)rec;
+  uint8_t* r8 = r16 + (size_t)chunk * S->stride[3];
+  uint8_t* r4 = r8 + (size_t)chunk * S->stride[2];
+  for (int i0 = 0; e == hipSuccess && i0 < dff; i0 += chunk) {
+    const int n = dff - i0 < chunk ? dff - i0 : chunk;
+    e = hipMemset(rec, 0, rbytes);
+    if (e == hipSuccess)
+      e = m2c::launch_quantize_records((const uint16_t*)wg, (const uint16_t*)wu,
+                                       (const uint16_t*)wdT, d, i0, n, r16, S->stride[3], r8,
+                                       S->stride[2], r4, S->stride[1], 0);
+    if (e == hipSuccess)
+      e = hipMemcpy(S->host[3] + (size_t)i0 * S->stride[3], r16, (size_t)n * S->stride[3],
+                    hipMemcpyDeviceToHost);
+    if (e == hipSuccess)
+      e = hipMemcpy(S->host[2] + (size_t)i0 * S->stride[2], r8, (size_t)n * S->stride[2],
+                    hipMemcpyDeviceToHost);
+    if (e == hipSuccess)
+      e = hipMemcpy(S->host[1] + (size_t)i0 * S->stride[1], r4, (size_t)n * S->stride[1],
+                    hipMemcpyDeviceToHost);
+  }
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    rc = hip_fail(e, "building the neuron store");
+  }
+  for (void* p : {wg, wu, wd, wdT, rec})
+    if (p) (void)hipFree(p);
+  return rc;
+}
+
+m2c_status new_layer(const m2c_layer_desc* desc, m2c_layer** out, m2c_layer** made) {
+  if (!out) return fail(M2C_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  int S = 0, cap = 0;
+  m2c_status rc = check_desc(desc, &S, &cap);
+  if (rc != M2C_OK) return rc;
+  m2c_layer* L = new (std::nothrow) m2c_layer();
+  if (!L) return fail(M2C_ERR_OUT_OF_MEMORY, "host allocation failed");
+  L->desc = *desc;
+  L->S = S;
+  L->cap = cap;
+  fill_info_layout(L);
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, desc->device) != hipSuccess) {
+    delete L;
+    return fail(M2C_ERR_HIP, "hipGetDeviceProperties failed");
+  }
+  L->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 1;
+  *made = L;
+  return M2C_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t m2c_record_bytes(int32_t d_model, int32_t tier) {
+  if (d_model <= 0 || d_model % 128) return -1;
+  return rec_bytes(d_model, tier);
+}
+
+const char* m2c_last_error(void) { return g_err; }
+
+m2c_status m2c_layer_create(const m2c_layer_desc* desc, const uint16_t* w_gate,
+                            const uint16_t* w_up, const uint16_t* w_down, const uint16_t* pred_a,
+                            const uint16_t* pred_b, const float* score_bias, m2c_layer** out) {
+  if (!w_gate || !w_up || !w_down || !pred_a || !pred_b)
+    return fail(M2C_ERR_INVALID_ARG, "a weight or predictor pointer is NULL");
+  m2c_layer* L = nullptr;
+  m2c_status rc = new_layer(desc, out, &L);
+  if (rc != M2C_OK) return rc;
+  DeviceGuard g(desc->device);
+  if (!g.ok) {
+    delete L;
+    return fail(M2C_ERR_HIP, "hipSetDevice(%d) failed", desc->device);
+  }
+  L->store = new (std::nothrow) Store();
+  if (!L->store) {
+    delete L;
+    return fail(M2C_ERR_OUT_OF_MEMORY, "host allocation failed");
+  }
+  L->store->device = desc->device;
+  L->store->d_model = desc->d_model;
+  L->store->d_ff = desc->d_ff;
+  for (int t = 1; t <= 3; ++t) L->store->stride[t] = L->info.record_stride[t];
+  rc = build_store(L, w_gate, w_up, w_down);
+  if (rc == M2C_OK) rc = alloc_device(L, score_bias != nullptr);
+  if (rc == M2C_OK) rc = upload_predictor(L, pred_a, pred_b, score_bias);
+  if (rc != M2C_OK) {
+    char keep[sizeof(g_err)];
+    memcpy(keep, g_err, sizeof(keep));
+    free_layer(L);
+    memcpy(g_err, keep, sizeof(keep));
+    return rc;
+  }
+  L->info.host_store_bytes = L->store->bytes;
+  *out = L;
+  return M2C_OK;
+}
+
+m2c_status m2c_layer_create_shared(const m2c_layer_desc* desc, const m2c_layer* weights_of,
+                                   const uint16_t* pred_a, const uint16_t* pred_b,
+                                   const float* score_bias, m2c_layer** out) {
+  if (!weights_of || !pred_a || !pred_b)
+    return fail(M2C_ERR_INVALID_ARG, "weights_of or a predictor pointer is NULL");
+  if (!desc || desc->d_model != weights_of->desc.d_model || desc->d_ff != weights_of->desc.d_ff ||
+      desc->device != weights_of->desc.device)
+    return fail(M2C_ERR_INVALID_ARG, "d_model, d_ff and device must match weights_of");
+  m2c_layer* L = nullptr;
+  m2c_status rc = new_layer(desc, out, &L);
+  if (rc != M2C_OK) return rc;
+  DeviceGuard g(desc->device);
+  if (!g.ok) {
+    delete L;
+    return fail(M2C_ERR_HIP, "hipSetDevice(%d) failed", desc->device);
+  }
+  L->store = weights_of->store;
+  L->store->refs++;
+  rc = alloc_device(L, score_bias != nullptr);
+  if (rc == M2C_OK) rc = upload_predictor(L, pred_a, pred_b, score_bias);
+  if (rc != M2C_OK) {
+    char keep[sizeof(g_err)];
+    memcpy(keep, g_err, sizeof(keep));
+    free_layer(L);
+    memcpy(g_err, keep, sizeof(keep));
+    return rc;
+  }
+  L->info.host_store_bytes = L->store->bytes;
+  *out = L;
+  return M2C_OK;
+}
+
+m2c_status m2c_layer_destroy(m2c_layer* layer) {
+  free_layer(layer);
+  return M2C_OK;
+}
+
+m2c_status m2c_layer_get_info(const m2c_layer* layer, m2c_layer_info* out) {
+  if (!layer || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  *out = layer->info;
+  return M2C_OK;
+}
+
+m2c_status m2c_plan_get_layout(const m2c_layer* layer, m2c_plan_layout* out) {
+  if (!layer || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  *out = layer->layout;
+  return M2C_OK;
+}
+
+m2c_status m2c_predict_rank(m2c_layer* L, const uint16_t* x, int32_t batch, int32_t k,
+                            int32_t n_fp16, int32_t n_int8, float* scores, uint8_t* tier_map,
+                            void* stream) {
+  if (!L || !x || !tier_map) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (batch < 1 || batch > L->desc.max_batch)
+    return fail(M2C_ERR_CAPACITY, "batch %d outside [1, max_batch=%d]", batch, L->desc.max_batch);
+  if (k < 0 || k > L->desc.k_max)
+    return fail(M2C_ERR_CAPACITY, "k %d outside [0, k_max=%d]", k, L->desc.k_max);
+  if (n_fp16 < 0 || n_int8 < 0 || (int64_t)n_fp16 + n_int8 > k)
+    return fail(M2C_ERR_INVALID_ARG, "tier counts %d + %d exceed k %d", n_fp16, n_int8, k);
+  DeviceGuard g(L->desc.device);
+  hipStream_t s = (hipStream_t)stream;
+  float* sc = scores ? scores : L->scores;
+  HIPOK(m2c::launch_predict(L, x, batch, sc, s), "predictor launch");
+  HIPOK(m2c::launch_select(sc, batch, L->desc.d_ff, k, n_fp16, n_int8, tier_map, s),
+        "select launch");
+  return M2C_OK;
+}
+
+m2c_status m2c_cache_plan(m2c_layer* L, const uint8_t* tier_map, int32_t batch, int64_t step,
+                          void* plan, void* stream) {
+  if (!L || !tier_map || !plan) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (((uintptr_t)plan) % 256) return fail(M2C_ERR_INVALID_ARG, "plan must be 256-byte aligned");
+  if (batch < 1 || batch > L->desc.max_batch)
+    return fail(M2C_ERR_CAPACITY, "batch %d outside [1, max_batch=%d]", batch, L->desc.max_batch);
+  if (step < 0 || step >= 0x7fffffffLL) return fail(M2C_ERR_INVALID_ARG, "step %lld out of range",
+                                                    (long long)step);
+  if (step <= L->last_step)
+    return fail(M2C_ERR_STATE, "step %lld is not after the previous step %lld", (long long)step,
+                (long long)L->last_step);
+  DeviceGuard g(L->desc.device);
+  HIPOK(m2c::launch_plan(L, tier_map, batch, (int)step, (uint8_t*)plan, (hipStream_t)stream),
+        "plan launch");
+  L->last_step = step;
+  return M2C_OK;
+}
+
+m2c_status m2c_cache_fill(m2c_layer* L, const void* plan, void* stream) {
+  if (!L || !plan) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  DeviceGuard g(L->desc.device);
+  HIPOK(m2c::launch_fill(L, (const uint8_t*)plan, (hipStream_t)stream), "fill launch");
+  return M2C_OK;
+}
+
+m2c_status m2c_sparse_ffn(m2c_layer* L, const uint16_t* x, int32_t batch, const void* plan,
+                          float* y, void* stream) {
+  if (!L || !x || !plan || !y) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (batch != 1) return fail(M2C_ERR_CAPACITY, "sparse FFN: batch %d not supported yet", batch);
+  DeviceGuard g(L->desc.device);
+  HIPOK(m2c::launch_ffn(L, x, batch, (const uint8_t*)plan, y, (hipStream_t)stream), "ffn launch");
+  return M2C_OK;
+}
+
+m2c_status m2c_layer_reset_cache(m2c_layer* L, void* stream) {
+  if (!L) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  DeviceGuard g(L->desc.device);
+  HIPOK(m2c::launch_reset(L, (hipStream_t)stream), "reset launch");
+  L->last_step = -1;
+  return M2C_OK;
+}
+
+m2c_status m2c_layer_stats(const m2c_layer* L, m2c_stats* out) {
+  if (!L || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  DeviceGuard g(L->desc.device);
+  long long st[16];
+  HIPOK(hipDeviceSynchronize(), "synchronize");
+  HIPOK(hipMemcpy(st, L->st.stats, sizeof(st), hipMemcpyDeviceToHost), "read stats");
+  memset(out, 0, sizeof(*out));
+  out->plans = st[0];
+  out->req = st[1];
+  out->hit = st[2];
+  out->refill = st[3];
+  out->new_ = st[4];
+  out->bypass = st[5];
+  out->evict = st[6];
+  out->fill[1] = st[7];
+  out->fill[2] = st[8];
+  out->fill[3] = st[9];
+  for (int t = 1; t <= 3; ++t) out->fill_bytes += out->fill[t] * L->info.record_bytes[t];
+  return M2C_OK;
+}
+
+m2c_status m2c_debug_read_record(const m2c_layer* L, int32_t tier, int32_t neuron, void* out,
+                                 size_t bytes) {
+  if (!L || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (tier < 1 || tier > 3 || neuron < 0 || neuron >= L->desc.d_ff)
+    return fail(M2C_ERR_INVALID_ARG, "tier %d / neuron %d out of range", tier, neuron);
+  if ((int64_t)bytes > L->store->stride[tier])
+    return fail(M2C_ERR_INVALID_ARG, "%zu bytes exceed the record stride %lld", bytes,
+                (long long)L->store->stride[tier]);
+  memcpy(out, L->store->host[tier] + (int64_t)neuron * L->store->stride[tier], bytes);
+  return M2C_OK;
+}
+
+m2c_status m2c_debug_read_slot(const m2c_layer* L, int32_t slot, void* out, size_t bytes) {
+  if (!L || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (slot < 0 || slot >= L->desc.cache_slots + L->S || (int64_t)bytes > L->info.slot_bytes)
+    return fail(M2C_ERR_INVALID_ARG, "slot %d / %zu bytes out of range", slot, bytes);
+  DeviceGuard g(L->desc.device);
+  HIPOK(hipDeviceSynchronize(), "synchronize");
+  HIPOK(hipMemcpy(out, L->slots + (int64_t)slot * L->info.slot_bytes, bytes,
+                  hipMemcpyDeviceToHost),
+        "read slot");
+  return M2C_OK;
+}
+
+m2c_status m2c_debug_read_tables(const m2c_layer* L, int32_t* slot_of, int32_t* slot_key,
+                                 uint8_t* slot_tier, int32_t* slot_last) {
+  if (!L) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  DeviceGuard g(L->desc.device);
+  const size_t C = (size_t)L->desc.cache_slots;
+  HIPOK(hipDeviceSynchronize(), "synchronize");
+  if (slot_of)
+    HIPOK(hipMemcpy(slot_of, L->st.slot_of, (size_t)L->desc.d_ff * 4, hipMemcpyDeviceToHost),
+          "read slot_of");
+  if (slot_key && C)
+    HIPOK(hipMemcpy(slot_key, L->st.slot_key, C * 4, hipMemcpyDeviceToHost), "read slot_key");
+  if (slot_tier && C)
+    HIPOK(hipMemcpy(slot_tier, L->st.slot_tier, C, hipMemcpyDeviceToHost), "read slot_tier");
+  if (slot_last && C)
+    HIPOK(hipMemcpy(slot_last, L->st.slot_last, C * 4, hipMemcpyDeviceToHost), "read slot_last");
+  return M2C_OK;
+}
+
+}  // extern "C"

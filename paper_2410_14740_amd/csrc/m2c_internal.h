@@ -1,0 +1,135 @@
+// Internal definitions of the m2c HIP library (gfx950). Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+#include "../../include/m2c.h"
+
+namespace m2c {
+
+// ---------------------------------------------------------------------------
+// Host-side layer object
+
+// Pinned host-DRAM neuron store: every neuron at all three tiers, record
+// stores back to back per tier. Shared (refcounted) between layers created
+// with m2c_layer_create_shared.
+struct Store {
+  int refs = 1;
+  int device = 0;
+  int d_model = 0, d_ff = 0;
+  uint8_t* host[4] = {nullptr, nullptr, nullptr, nullptr};  // by tier, [1..3]
+  int64_t stride[4] = {0, 0, 0, 0};
+  int64_t bytes = 0;
+};
+
+// Offsets of the per-layer device scratch used by the plan kernel.
+struct DeviceState {
+  int32_t* slot_of = nullptr;    // [d_ff]
+  int32_t* slot_key = nullptr;   // [C]
+  uint8_t* slot_tier = nullptr;  // [C]
+  int32_t* slot_last = nullptr;  // [C]
+  int32_t* lru = nullptr;        // [2][C] ping-pong LRU order
+  int32_t* lru_cur = nullptr;    // [1]
+  int32_t* new_pos = nullptr;    // [cap] plan scratch: req position of the j-th NEW
+  int32_t* work_pos = nullptr;   // [cap] plan scratch: work position of req p
+  int32_t* vict_slot = nullptr;  // [cap] plan scratch
+  int32_t* vict_old = nullptr;   // [cap] plan scratch
+  unsigned long long* stats = nullptr;  // [16] cumulative counters
+};
+
+}  // namespace m2c
+
+struct m2c_layer {
+  m2c_layer_desc desc;
+  int S = 0;    // staging slots
+  int cap = 0;  // plan capacity
+  int num_cus = 0;
+  m2c::Store* store = nullptr;
+  m2c_layer_info info;
+  m2c_plan_layout layout;
+  // device memory (one allocation, carved)
+  uint8_t* dev_base = nullptr;
+  int64_t dev_bytes = 0;
+  uint16_t* pred_a = nullptr;  // [r][d]
+  uint16_t* pred_b = nullptr;  // [d_ff][r]
+  float* bias = nullptr;       // [d_ff] or null
+  float* z = nullptr;          // [max_batch][r]
+  float* scores = nullptr;     // [max_batch][d_ff]
+  uint8_t* slots = nullptr;    // [C+S][slot_bytes]
+  float* h = nullptr;          // [cap] FFN hidden activations in work order
+  float* y_part = nullptr;     // [ffn_groups][d] down-projection partials
+  int32_t* ffn_ctr = nullptr;  // [4] work-grab counters (self-resetting)
+  int ffn_groups = 1;
+  m2c::DeviceState st;
+  int64_t last_step = -1;
+};
+
+namespace m2c {
+
+// ---------------------------------------------------------------------------
+// Launchers (one per kernel file). All enqueue on `stream` and return the
+// hipError_t of the launch.
+
+hipError_t launch_transpose_u16(const uint16_t* in, uint16_t* out, int rows, int cols,
+                                hipStream_t stream);
+hipError_t launch_quantize_records(const uint16_t* wg, const uint16_t* wu, const uint16_t* wdT,
+                                   int d, int i0, int n, uint8_t* r16, int64_t st16, uint8_t* r8,
+                                   int64_t st8, uint8_t* r4, int64_t st4, hipStream_t stream);
+hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, float* scores,
+                          hipStream_t stream);
+hipError_t launch_select(const float* scores, int batch, int d_ff, int k, int n16, int n8,
+                         uint8_t* tier_map, hipStream_t stream);
+hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int step, uint8_t* plan,
+                       hipStream_t stream);
+hipError_t launch_reset(m2c_layer* L, hipStream_t stream);
+hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
+hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
+                      hipStream_t stream);
+
+// ---------------------------------------------------------------------------
+// Device helpers shared by the kernels
+
+__device__ __forceinline__ float h2f(uint16_t b) {
+  return (float)__builtin_bit_cast(_Float16, b);
+}
+
+__device__ __forceinline__ uint32_t score_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Block-wide exclusive prefix sum over one value per thread. `tmp` holds at
+// least blockDim.x / 64 + 1 entries of shared memory. Returns the exclusive
+// prefix; *total gets the block sum. Contains __syncthreads().
+template <typename T>
+__device__ T block_exclusive_scan(T v, T* tmp, T* total) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = (blockDim.x + 63) >> 6;
+  T incl = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    T o = __shfl_up(incl, off);
+    if (lane >= off) incl += o;
+  }
+  if (lane == 63) tmp[wave] = incl;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    T run = 0;
+    for (int w = 0; w < nwaves; ++w) {
+      T t = tmp[w];
+      tmp[w] = run;
+      run += t;
+    }
+    tmp[nwaves] = run;
+  }
+  __syncthreads();
+  T res = tmp[wave] + incl - v;
+  *total = tmp[nwaves];
+  __syncthreads();
+  return res;
+}
+
+}  // namespace m2c

@@ -21,6 +21,7 @@ tensor, so any layer can be drawn alone.
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
 from dataclasses import dataclass, field
 from fractions import Fraction as F
 
@@ -109,10 +110,12 @@ def _normal_f16(rng: np.random.Generator, shape, sigma: float) -> np.ndarray:
 
 
 def layer_weights(seed: int, layer: int, d: int, d_ff: int, sigma_w: float):
-    """(w_gate [d_ff][d], w_up [d_ff][d], w_down [d][d_ff]) fp16."""
-    return (_normal_f16(_rng(seed, layer, _T_GATE), (d_ff, d), sigma_w),
-            _normal_f16(_rng(seed, layer, _T_UP), (d_ff, d), sigma_w),
-            _normal_f16(_rng(seed, layer, _T_DOWN), (d, d_ff), sigma_w))
+    """(w_gate [d_ff][d], w_up [d_ff][d], w_down [d][d_ff]) fp16. The three
+    matrices come from independent streams and are drawn in parallel threads
+    (numpy releases the GIL while filling large arrays)."""
+    jobs = ((_T_GATE, (d_ff, d)), (_T_UP, (d_ff, d)), (_T_DOWN, (d, d_ff)))
+    with cf.ThreadPoolExecutor(3) as ex:
+        return tuple(ex.map(lambda j: _normal_f16(_rng(seed, layer, j[0]), j[1], sigma_w), jobs))
 
 
 def layer_predictor(seed: int, layer: int, d: int, d_ff: int, r: int, sigma_p: float,

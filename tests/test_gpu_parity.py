@@ -1,0 +1,256 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle.
+
+Integer outputs (records, scores bits, tiers, plans, slot tables) must match
+bit for bit; FFN outputs within 2e-3 of the oracle under the floored
+relative error of helpers.r8_errors.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_14740_amd import m2c
+from paper_2410_14740_amd import workloads as W
+
+from helpers import FFN_TOL, oracle_ffn, r8_errors, say
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+# (name, d_model, d_ff, pred_rank, seed): a ragged shape (d/8 = 48 chunks,
+# r/8 = 6 chunks, d_ff not a multiple of 64) and the tiny workload's shape.
+SHAPES = [("ragged", 384, 700, 48, 101), ("tiny", 1024, 2752, 128, W.WORKLOADS["tiny"].seed)]
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _x16(ld, t):
+    return _dev(ld.x[t].view(np.uint16)).view(torch.float16)
+
+
+def _layer(ld, k_max, C, max_batch=1, staging=-1):
+    desc = m2c.make_desc(ld.d_model, ld.d_ff, ld.pred_rank, k_max, C, max_batch, staging)
+    return m2c.Layer(desc, ld)
+
+
+def _counts(k, frac16=(1, 3), frac8=(1, 3)):
+    n16 = k * frac16[0] // frac16[1]
+    n8 = k * (frac16[0] * frac8[1] + frac8[0] * frac16[1]) // (frac16[1] * frac8[1]) - n16
+    return n16, n8
+
+
+@pytest.mark.parametrize("name,d,d_ff,r,seed", SHAPES)
+def test_records_bit_exact(name, d, d_ff, r, seed):
+    ld = W.make_layer(seed, 0, d, d_ff, r, 1)
+    say(f"records {name} d={d} d_ff={d_ff}")
+    L = _layer(ld, d_ff // 4, d_ff // 2)
+    for t in (1, 2, 3):
+        ref = oracle.build_records(ld.w_gate, ld.w_up, ld.w_down, t)
+        nb = L.info.record_stride[t]
+        assert ref.shape[1] == nb
+        got = np.stack([m2c.m2c_debug_read_record(L.handle, t, i, nb) for i in range(d_ff)])
+        assert np.array_equal(got, ref), f"tier {t}: {np.argwhere((got != ref).any(1))[:5].ravel()}"
+    L.close()
+
+
+@pytest.mark.parametrize("batch", [1, 3])
+@pytest.mark.parametrize("name,d,d_ff,r,seed", SHAPES)
+def test_predict_and_tiers_bit_exact(name, d, d_ff, r, seed, batch):
+    rhos = tuple([0.9, 0.5, 0.95][:batch])
+    ld = W.make_layer(seed, 1, d, d_ff, r, 4, rhos=rhos, zipf_bias=(batch == 3))
+    k = d_ff // 4
+    n16, n8 = _counts(k)
+    say(f"predict {name} batch={batch}")
+    L = _layer(ld, k, d_ff // 2, max_batch=batch)
+    scores = torch.empty((batch, d_ff), dtype=torch.float32, device="cuda")
+    tiers = torch.empty((batch, d_ff), dtype=torch.uint8, device="cuda")
+    for t in range(4):
+        L.predict_rank(_x16(ld, t), batch, k, n16, n8, scores, tiers)
+        torch.cuda.synchronize()
+        s_gpu, t_gpu = scores.cpu().numpy(), tiers.cpu().numpy()
+        for b in range(batch):
+            _, s_ref = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, b])
+            assert np.array_equal(s_gpu[b].view(np.uint32), s_ref.view(np.uint32)), \
+                f"step {t} row {b}: {np.count_nonzero(s_gpu[b] != s_ref)} scores differ"
+            t_ref, _ = oracle.select_tiers(s_ref, k, n16, n8)
+            assert np.array_equal(t_gpu[b], t_ref)
+    L.close()
+
+
+def _compare_plan(g, o, step):
+    for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "fill_ids",
+                "fill_tier", "fill_slot", "evicted_ids", "work_slot", "work_mask"):
+        assert np.array_equal(g[key], o[key]), f"step {step}: plan field {key} differs"
+    assert np.array_equal(g["counts"][:13], o["counts"][:13]), f"step {step}: counts differ"
+
+
+def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label=""):
+    """predict -> plan -> fill -> FFN on the GPU and in the oracle, step by
+    step, comparing every stage."""
+    d_ff = ld.d_ff
+    L = _layer(ld, k, C, max_batch=batch)
+    cache = oracle.LRUCache(d_ff, C, L.info.staging_slots)
+    tiers = torch.empty((batch, d_ff), dtype=torch.uint8, device="cuda")
+    y = torch.empty((batch, ld.d_model), dtype=torch.float32, device="cuda")
+    stats = np.zeros(16, np.int64)
+    worst = 0.0
+    for t in range(steps):
+        say(f"{label} step {t}")
+        x = _x16(ld, t)
+        L.predict_rank(x, batch, k, n16, n8, None, tiers)
+        L.cache_plan(tiers, batch, t)
+        L.cache_fill()
+        if check_ffn and batch == 1:
+            L.sparse_ffn(x, batch, y)
+        torch.cuda.synchronize()
+        tm_ref = np.stack([oracle.select_tiers(oracle.predict(ld.pred_a, ld.pred_b, ld.bias,
+                                                              ld.x[t, b])[1], k, n16, n8)[0]
+                           for b in range(batch)])
+        assert np.array_equal(tiers.cpu().numpy(), tm_ref), f"step {t}: tier maps differ"
+        o = cache.plan(tm_ref, t)
+        g = L.read_plan()
+        _compare_plan(g, o, t)
+        stats += o["counts"]
+        slot_of, key, stier, last = m2c.m2c_debug_read_tables(L.handle, d_ff, C)
+        assert np.array_equal(slot_of, cache.slot_of)
+        assert np.array_equal(key, cache.slot_key[:C])
+        assert np.array_equal(stier, cache.slot_tier[:C])
+        assert np.array_equal(last, cache.slot_last[:C])
+        if check_ffn and batch == 1:
+            y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"])
+            err = r8_errors(y.cpu().numpy(), y_ref).max()
+            worst = max(worst, err)
+            assert err <= FFN_TOL, f"step {t}: FFN error {err:.3e}"
+    st = L.stats()
+    assert (st.plans, st.req, st.hit, st.refill, st.new_, st.bypass, st.evict) == (
+        steps, stats[0], stats[1], stats[2], stats[3], stats[4], stats[5])
+    assert (st.fill[3], st.fill[2], st.fill[1]) == (stats[10], stats[11], stats[12])
+    L.close()
+    return worst
+
+
+@pytest.mark.parametrize("name,d,d_ff,r,seed", SHAPES)
+def test_end_to_end_steps(name, d, d_ff, r, seed):
+    ld = W.make_layer(seed, 2, d, d_ff, r, 10, rhos=(0.8,))
+    k = d_ff // 4
+    n16, n8 = _counts(k)
+    # C < k forces evictions and bypasses every step
+    _run_steps(ld, 10, k, n16, n8, C=(2 * k) // 3, label=f"e2e {name}")
+
+
+def test_tiny_workload_all_steps():
+    wl = W.WORKLOADS["tiny"]
+    ld = W.workload_layer(wl, 0)
+    k, n16, n8 = wl.counts()
+    worst = _run_steps(ld, wl.steps, k, n16, n8, wl.cache_slots(), label="tiny workload")
+    say(f"tiny workload worst FFN error {worst:.2e}")
+
+
+def test_batched_plan_union_and_bypass():
+    ld = W.make_layer(77, 0, 384, 700, 48, 6, rhos=(0.5, 0.95, 0.9, 0.7), zipf_bias=True)
+    k = 120
+    n16, n8 = _counts(k, (1, 10), (2, 5))
+    _run_steps(ld, 6, k, n16, n8, C=200, batch=4, check_ffn=False, label="batched plan")
+
+
+def test_dense_equivalence_all_fp16():
+    """k = d_ff, every neuron FP16, every neuron cached: the sparse FFN is the
+    dense SwiGLU FFN."""
+    d, d_ff = 512, 640
+    ld = W.make_layer(55, 0, d, d_ff, 32, 2)
+    L = _layer(ld, d_ff, d_ff)
+    tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
+    y = torch.empty((1, d), dtype=torch.float32, device="cuda")
+    for t in range(2):
+        x = _x16(ld, t)
+        L.predict_rank(x, 1, d_ff, d_ff, 0, None, tiers)
+        L.cache_plan(tiers, 1, t)
+        L.cache_fill()
+        L.sparse_ffn(x, 1, y)
+        torch.cuda.synchronize()
+        assert (tiers.cpu().numpy() == 3).all()
+        y_ref = oracle.dense_ffn(ld.w_gate, ld.w_up, ld.w_down, ld.x[t, 0])
+        assert r8_errors(y.cpu().numpy()[0], y_ref).max() <= FFN_TOL
+    g = L.read_plan()
+    assert g["counts"][m2c.CNT_HIT] == d_ff  # second step: everything hits
+    L.close()
+
+
+def test_k_zero_and_all_equal_scores():
+    d, d_ff, r = 256, 300, 16
+    ld = W.make_layer(9, 0, d, d_ff, r, 2)
+    ld.pred_a[:] = 0  # every score is exactly +0.0: ties resolve by id
+    L = _layer(ld, 40, 100)
+    tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
+    y = torch.empty((1, d), dtype=torch.float32, device="cuda")
+    x = _x16(ld, 0)
+    L.predict_rank(x, 1, 40, 10, 10, None, tiers)
+    torch.cuda.synchronize()
+    tm = tiers.cpu().numpy()[0]
+    assert list(tm[:40]) == [3] * 10 + [2] * 10 + [1] * 20 and not tm[40:].any()
+    L.predict_rank(x, 1, 0, 0, 0, None, tiers)
+    L.cache_plan(tiers, 1, 0)
+    L.cache_fill()
+    L.sparse_ffn(x, 1, y)
+    torch.cuda.synchronize()
+    assert not tiers.cpu().numpy().any()
+    assert L.read_plan()["counts"][m2c.CNT_REQ] == 0
+    assert not y.cpu().numpy().any()
+    L.close()
+
+
+def test_host_errors_leave_layer_usable():
+    ld = W.make_layer(3, 0, 256, 200, 16, 3)
+    L = _layer(ld, 50, 60)
+    tiers = torch.zeros((1, 200), dtype=torch.uint8, device="cuda")
+    L.cache_plan(tiers, 1, 5)
+    with pytest.raises(m2c.M2CError) as e:
+        L.cache_plan(tiers, 1, 5)
+    assert e.value.status == m2c.M2C_ERR_STATE
+    with pytest.raises(m2c.M2CError) as e:
+        L.predict_rank(_x16(ld, 0), 1, 51, 0, 0, None, tiers)
+    assert e.value.status == m2c.M2C_ERR_CAPACITY
+    with pytest.raises(m2c.M2CError) as e:
+        L.predict_rank(_x16(ld, 0), 2, 10, 0, 0, None, tiers)
+    assert e.value.status == m2c.M2C_ERR_CAPACITY
+    with pytest.raises(m2c.M2CError) as e:
+        L.predict_rank(_x16(ld, 0), 1, 10, 6, 6, None, tiers)
+    assert e.value.status == m2c.M2C_ERR_INVALID_ARG
+    L.predict_rank(_x16(ld, 0), 1, 10, 2, 3, None, tiers)
+    L.cache_plan(tiers, 1, 6)
+    torch.cuda.synchronize()
+    assert L.read_plan()["counts"][m2c.CNT_REQ] == 10
+    L.reset_cache()
+    L.cache_plan(tiers, 1, 0)  # history cleared by the reset
+    torch.cuda.synchronize()
+    assert L.read_plan()["counts"][m2c.CNT_NEW] == 10
+    L.close()
+
+
+def test_shared_store_layers():
+    ld0 = W.make_layer(13, 0, 256, 300, 16, 2)
+    ld1 = W.make_layer(13, 1, 256, 300, 16, 2, weight_layer=0)
+    L0 = _layer(ld0, 60, 60)
+    desc = m2c.make_desc(256, 300, 16, 60, 60)
+    L1 = m2c.Layer(desc, ld1, weights_of=L0)
+    nb = L0.info.record_stride[2]
+    assert np.array_equal(m2c.m2c_debug_read_record(L1.handle, 2, 7, nb),
+                          m2c.m2c_debug_read_record(L0.handle, 2, 7, nb))
+    L0.close()  # the store stays alive for L1
+    ref = oracle.build_records(ld0.w_gate, ld0.w_up, ld0.w_down, 2)
+    assert np.array_equal(m2c.m2c_debug_read_record(L1.handle, 2, 7, nb), ref[7])
+    L1.close()
+
+
+def test_llama70b_layer_shape():
+    """One layer at the 70B shape (d 8192, d_ff 28672, rank 512, k 2867,
+    tiers 286/860/1721, C = k): scores, tiers, plans and tables bit-exact,
+    every FFN output within tolerance, over three steps."""
+    wl = W.WORKLOADS["llama2-70b"]
+    say("70B layer: drawing weights")
+    ld = W.workload_layer(wl, 0, steps=3)
+    k, n16, n8 = wl.counts()
+    worst = _run_steps(ld, 3, k, n16, n8, wl.cache_slots(), label="70B layer")
+    say(f"70B layer worst FFN error {worst:.2e}")
