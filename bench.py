@@ -1,0 +1,351 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the dynamic sparse mixed-precision FFN stack.
+
+One step = one decode token through every FFN layer of the stack: for each
+layer, predictor scores -> top-k and tiers -> cache plan -> cache fill from
+the pinned host store -> gather-dequant sparse FFN, all through the C ABI.
+
+Streams: predict+plan run on an aux stream, fills on a copy stream, the FFN on
+the main stream. Layer l's predict may start once the FFN of layer l-2 is
+done (the one-layer look-ahead of the paper's preloader, Sec. 5.4), so the
+fill of layer l overlaps the FFN of layer l-1 (Sec. 1: asynchronous loading
+overlapped with computation).
+
+Prints one JSON line (the benchmark contract), including the HBM roofline of
+the sparse FFN and the oracle timed on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "sparse MP-FFN µs/layer-step + tokens/s; achieved HBM GB/s vs MI355X peak"
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, vendor figure
+
+
+def parse_args():
+    p = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=120, help="timed decode steps")
+    p.add_argument("--warmup", type=int, default=8, help="untimed decode steps first")
+    p.add_argument("--workload", default="llama2-7b")
+    p.add_argument("--weight-sets", type=int, default=0,
+                   help="draw only this many distinct weight sets and let layers share them "
+                        "(0 = every layer its own weights)")
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="target CPU time of the oracle baseline sample (0 = skip)")
+    p.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
+    p.add_argument("--gemv-workload", default="llama2-70b",
+                   help="layer shape of the isolated sparse-FFN measurement ('' = skip)")
+    p.add_argument("--gemv-layers", type=int, default=8,
+                   help="layers cycled by the isolated measurement (their slots exceed the "
+                        "256 MB Infinity Cache, so it measures HBM, not the cache)")
+    p.add_argument("--gemv-reps", type=int, default=20)
+    p.add_argument("--deterministic-ffn", action="store_true",
+                   help="use the three-kernel sparse FFN whose output repeats bit for bit")
+    p.add_argument("--only-gemv", action="store_true",
+                   help="run only the isolated sparse-FFN measurement (for profiling)")
+    p.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
+                   help="only copy a buffer of this many MB device to device, 5 times "
+                        "(a plain copy kernel of known size, to scale HBM counters)")
+    return p.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def build_stack(wl, n_layers, steps_total, weight_sets, torch, m2c, W, flags=0):
+    """Create every layer (weights drawn in a thread pool, layers created in
+    order) and stage every layer's decode inputs on the device."""
+    k, n16, n8 = wl.counts()
+    C = wl.cache_slots()
+    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, flags=flags)
+    x_dev = torch.empty((n_layers, steps_total, wl.d_model), dtype=torch.float16, device="cuda")
+    layers, first = [], None
+
+    def draw(l):
+        wsrc = None if weight_sets <= 0 else l % weight_sets
+        return W.workload_layer(wl, l, steps=steps_total, weight_layer=wsrc,
+                                draw_weights=weight_sets <= 0 or l < weight_sets)
+
+    keep = None
+    with cf.ThreadPoolExecutor(4) as ex:
+        futs = [ex.submit(draw, l) for l in range(n_layers)]
+        for l, fu in enumerate(futs):
+            ld = fu.result()
+            futs[l] = None
+            x_dev[l].copy_(torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16))
+            owner = None
+            if weight_sets > 0 and l >= weight_sets:
+                owner = layers[l % weight_sets]
+            layers.append(m2c.Layer(desc, ld, weights_of=owner))
+            if l == 0:
+                keep = ld
+            if l % 8 == 7 or l == n_layers - 1:
+                log(f"created {l + 1}/{n_layers} layers")
+    return layers, x_dev, keep
+
+
+def cpu_baseline(wl, ld, n_layers, budget_s, oracle):
+    """The oracle (plain C, one thread) on a bounded sample of the same work:
+    layer 0 of the stack, consecutive decode steps until about `budget_s`
+    seconds of predict + select + plan + FFN have run. Record building is
+    set-up, not timed. Returns the contract's cpu_baseline object."""
+    k, n16, n8 = wl.counts()
+    C = wl.cache_slots()
+    cap = min(wl.d_ff, k)
+    cache = oracle.LRUCache(wl.d_ff, C, max(0, cap - C))
+    # records for the neurons the sample will touch (found by a first pass)
+    steps_avail = ld.x.shape[0]
+    tiers_by_step = []
+    t0 = time.perf_counter()
+    for t in range(min(steps_avail, 64)):
+        _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
+        tiers_by_step.append(oracle.select_tiers(s, k, n16, n8)[0])
+        if time.perf_counter() - t0 > budget_s / 3:
+            break
+    used = np.nonzero(np.any(np.stack(tiers_by_step) > 0, axis=0))[0]
+    row = np.full(wl.d_ff, -1, np.int64)
+    row[used] = np.arange(used.size)
+    recs = {q: oracle.build_records(ld.w_gate[used], ld.w_up[used],
+                                    np.ascontiguousarray(ld.w_down[:, used]), q) for q in (1, 2, 3)}
+    n_steps = len(tiers_by_step)
+    t_start = time.perf_counter()
+    done = 0
+    for t in range(n_steps):
+        _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
+        tm, _ = oracle.select_tiers(s, k, n16, n8)
+        plan = cache.plan(tm, t)
+        ids = row[plan["req_ids"]].astype(np.int32)
+        oracle.sparse_ffn(ld.x[t], ids, plan["req_tier"], recs)
+        done += 1
+        if time.perf_counter() - t_start > budget_s:
+            break
+    el = time.perf_counter() - t_start
+    per = el / done
+    return {"value": 1.0 / (per * n_layers), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"layer 0 of {wl.name}, {done} consecutive decode steps of predict + "
+                      f"select + LRU plan + fp64 sparse FFN, single thread; "
+                      f"{per * 1e3:.1f} ms per layer-step, scaled to {n_layers} layers",
+            "ms_per_layer_step": per * 1e3}
+
+
+def gemv_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
+    """The sparse FFN alone on `n_layers` layers of workload `wl`'s shape that
+    share one weight store: a few warm-up decode steps fill every cache, then
+    the FFN of each layer is launched back to back, cycling through the
+    layers, on one stream. Returns the HBM roofline of the FFN call."""
+    k, n16, n8 = wl.counts()
+    n4 = k - n16 - n8
+    C = wl.cache_slots()
+    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, flags=flags)
+    steps = 4
+    layers = []
+    for l in range(n_layers):
+        ld = W.workload_layer(wl, l, steps=steps, draw_weights=(l == 0))
+        layers.append((m2c.Layer(desc, ld, weights_of=layers[0][0] if l else None),
+                       torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16).cuda()))
+    d, d_ff = wl.d_model, wl.d_ff
+    tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
+    y = torch.empty((1, d), dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    for t in range(steps):
+        for L, x in layers:
+            L.predict_rank(x[t], 1, k, n16, n8, None, tiers, stream=s)
+            L.cache_plan(tiers, 1, t, stream=s)
+            L.cache_fill(stream=s)
+            L.sparse_ffn(x[t], 1, y, stream=s)
+    torch.cuda.synchronize()
+    ev = []
+    for r in range(reps):
+        for L, x in layers:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            L.sparse_ffn(x[steps - 1], 1, y, stream=s)
+            b.record(s)
+            ev.append((a, b))
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    rb = layers[0][0].info.record_bytes
+    nbytes = n16 * rb[3] + n8 * rb[2] + n4 * rb[1] + 6 * d
+    avg = float(ms.mean()) * 1e-3
+    for L, _ in layers:
+        L.close()
+    return {"workload": wl.name, "layers_cycled": n_layers, "launches": len(ev),
+            "us_avg": avg * 1e6, "us_min": float(ms.min()) * 1e3,
+            "bytes_per_launch": nbytes, "achieved_GBps": nbytes / avg / 1e9,
+            "frac_of_peak": nbytes / avg / 1e9 / PEAK_HBM_GBPS}
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the hot path is "
+              "built and measured on a single MI355X.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2410_14740_amd import m2c
+    from paper_2410_14740_amd import workloads as W
+
+    if not os.path.exists(m2c.LIB_PATH):
+        from paper_2410_14740_amd import build as hip_build
+        hip_build.build()
+    m2c.load()
+    torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 20
+        a = torch.ones(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n, "launches": 5}), flush=True)
+        return
+    ffn_flags = m2c.FLAG_DETERMINISTIC_FFN if args.deterministic_ffn else 0
+    if args.only_gemv:
+        g = gemv_isolated(W.WORKLOADS[args.gemv_workload], args.gemv_layers, args.gemv_reps,
+                          torch, m2c, W, flags=ffn_flags)
+        print(json.dumps({"gemv_isolated": g}), flush=True)
+        return
+    wl = W.WORKLOADS[args.workload]
+    n_layers = args.layers or wl.n_layers
+    k, n16, n8 = wl.counts()
+    n4 = k - n16 - n8
+    steps_total = args.warmup + args.steps
+    t_setup = time.perf_counter()
+    layers, x_dev, ld0 = build_stack(wl, n_layers, steps_total, args.weight_sets, torch, m2c, W,
+                                     flags=ffn_flags)
+    log(f"setup {time.perf_counter() - t_setup:.1f} s")
+    d, d_ff = wl.d_model, wl.d_ff
+    info = layers[0].info
+    rb = info.record_bytes
+    ffn_bytes = n16 * rb[3] + n8 * rb[2] + n4 * rb[1] + 2 * d + 4 * d
+
+    main_s, aux_s, copy_s = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    ev_plan = [torch.cuda.Event() for _ in range(n_layers)]
+    ev_fill = [torch.cuda.Event() for _ in range(n_layers)]
+    ev_ffn = [torch.cuda.Event() for _ in range(n_layers)]
+    tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
+    # m2c_sparse_ffn adds into y (a residual stream): one zeroed row per
+    # layer-step, so every output is the plain FFN of its token
+    y = torch.zeros((steps_total, n_layers, d), dtype=torch.float32, device="cuda")
+    lag = min(2, n_layers)
+    timing = []  # (ffn_start, ffn_end, fill_start, fill_end) per timed layer-step
+
+    def step(t, timed):
+        for l in range(n_layers):
+            f = t * n_layers + l
+            L = layers[l]
+            if f - lag >= 0:
+                aux_s.wait_event(ev_ffn[(f - lag) % n_layers])
+            x = x_dev[l, t]
+            L.predict_rank(x, 1, k, n16, n8, None, tiers[l], stream=aux_s)
+            L.cache_plan(tiers[l], 1, t, stream=aux_s)
+            ev_plan[l].record(aux_s)
+            copy_s.wait_event(ev_plan[l])
+            if timed:
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                ev[2].record(copy_s)
+            L.cache_fill(stream=copy_s)
+            if timed:
+                ev[3].record(copy_s)
+            ev_fill[l].record(copy_s)
+            main_s.wait_event(ev_fill[l])
+            if timed:
+                ev[0].record(main_s)
+            L.sparse_ffn(x, 1, y[t, l], stream=main_s)
+            if timed:
+                ev[1].record(main_s)
+                timing.append(ev)
+            ev_ffn[l].record(main_s)
+
+    for t in range(args.warmup):
+        step(t, False)
+    torch.cuda.synchronize()
+    st0 = [L.stats() for L in layers]
+    t0 = time.perf_counter()
+    for t in range(args.warmup, steps_total):
+        step(t, True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st1 = [L.stats() for L in layers]
+
+    ffn_ms = np.array([e[0].elapsed_time(e[1]) for e in timing])
+    fill_ms = np.array([e[2].elapsed_time(e[3]) for e in timing])
+    reqs = sum(b.req - a.req for a, b in zip(st0, st1))
+    hits = sum(b.hit - a.hit for a, b in zip(st0, st1))
+    refills = sum(b.refill - a.refill for a, b in zip(st0, st1))
+    bypass = sum(b.bypass - a.bypass for a, b in zip(st0, st1))
+    fill_bytes = sum(b.fill_bytes - a.fill_bytes for a, b in zip(st0, st1))
+    n_ls = args.steps * n_layers
+    ffn_avg_s = float(ffn_ms.mean()) * 1e-3
+    achieved = ffn_bytes / ffn_avg_s / 1e9
+    tokens_per_s = args.steps / wall
+
+    for L in layers:
+        L.close()
+    layers = []
+    gemv = None
+    if args.gemv_workload:
+        log(f"isolated sparse FFN on {args.gemv_layers} {args.gemv_workload} layers")
+        gemv = gemv_isolated(W.WORKLOADS[args.gemv_workload], args.gemv_layers, args.gemv_reps,
+                             torch, m2c, W, flags=ffn_flags)
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        import oracle
+        log("timing the oracle on the host")
+        cpu = cpu_baseline(wl, ld0, n_layers, args.cpu_seconds, oracle)
+
+    out = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "layers": n_layers, "d_model": d, "d_ff": d_ff,
+            "pred_rank": wl.pred_rank, "k": k, "tiers_fp16_int8_int4": [n16, n8, n4],
+            "cache_slots": wl.cache_slots(), "batch": 1, "decode_steps": steps_total,
+            "weights": "fp16 records with int8/int4 copies (group 128, fp16 scales)",
+            "distinct_weight_sets": args.weight_sets or n_layers,
+            "ffn": "three kernels, deterministic" if args.deterministic_ffn else "fused kernel",
+        },
+        "us_per_layer_step": wall / n_ls * 1e6,
+        "ffn_us_avg": ffn_avg_s * 1e6,
+        "fill_us_avg": float(fill_ms.mean()) * 1e3,
+        "fill_MB_per_layer_step": fill_bytes / n_ls / 1e6,
+        "host_link_GBps_in_fill": fill_bytes / n_ls / (float(fill_ms.mean()) * 1e-3) / 1e9,
+        "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
+                  "bypass_rate": bypass / max(reqs, 1)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": None,
+                     "kernel": "m2c_sparse_ffn (ffn_up + ffn_down + ffn_reduce)",
+                     "bytes_per_launch": ffn_bytes},
+        "cpu_baseline": cpu,
+        "gemv_isolated": gemv,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -121,9 +121,9 @@ enum { M2C_TIER_NONE = 0, M2C_TIER_INT4 = 1, M2C_TIER_INT8 = 2, M2C_TIER_FP16 = 
 
 /* Layer descriptor. All fields are required. */
 typedef struct {
-  int32_t d_model;       /* d: multiple of 128, 128..65536                      */
+  int32_t d_model;       /* d: multiple of 128, 128..16384                      */
   int32_t d_ff;          /* neurons: 1..262144                                  */
-  int32_t pred_rank;     /* r: multiple of 8, 8..4096                           */
+  int32_t pred_rank;     /* r: multiple of 8, 8..1024                           */
   int32_t group;         /* quantization group; must be 128                     */
   int32_t k_max;         /* largest k any call will use: 0..d_ff                */
   int32_t max_batch;     /* largest batch any call will use: 1..32              */
@@ -132,7 +132,18 @@ typedef struct {
                             overflow, max(0, min(d_ff, max_batch*k_max) - C);
                             smaller explicit values are rejected               */
   int32_t device;        /* HIP device ordinal                                  */
+  int32_t flags;         /* M2C_FLAG_* bits, 0 for the defaults                 */
 } m2c_layer_desc;
+
+/* m2c_layer_desc.flags */
+enum {
+  /* Sparse FFN by three kernels (up, down by column slices, ordered reduce)
+     whose output is the same bit pattern on every run. The default is one
+     fused kernel that adds workgroup partial rows into y with fp32 atomics,
+     so the summation order, and the last bits of y, vary from run to run.
+     Layers with d_model > 8192 always take the three-kernel path. */
+  M2C_FLAG_DETERMINISTIC_FFN = 1
+};
 
 /* Sizes that follow from a descriptor. */
 typedef struct {
@@ -244,10 +255,11 @@ m2c_status m2c_cache_plan(m2c_layer* layer, const uint8_t* tier_map, int32_t bat
  * before the FFN that reads the plan. No host synchronization. */
 m2c_status m2c_cache_fill(m2c_layer* layer, const void* plan, void* stream);
 
-/* y = sum over i in R of silu(<g_i, x>) * <u_i, x> * d_i, per batch row b over
- * the neurons whose req_mask has bit b, every vector dequantized at the
- * neuron's step tier; fp32 accumulation.
- *   x dev fp16 [batch][d_model];  y dev fp32 [batch][d_model] output.
+/* y += sum over i in R of silu(<g_i, x>) * <u_i, x> * d_i, per batch row b
+ * over the neurons whose req_mask has bit b, every vector dequantized at the
+ * neuron's step tier; fp32 accumulation. The result is ADDED to y (a residual
+ * stream); zero y first for the plain FFN output.
+ *   x dev fp16 [batch][d_model];  y dev fp32 [batch][d_model], in/out.
  * `batch` must equal the batch given to the plan. */
 m2c_status m2c_sparse_ffn(m2c_layer* layer, const uint16_t* x, int32_t batch, const void* plan,
                           float* y, void* stream);

@@ -12,6 +12,9 @@
 namespace m2c {
 
 constexpr int kFillThreads = 256;
+constexpr int kFillBlocks = 64;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 struct FillSrc {
   const uint8_t* host[4];
@@ -33,19 +36,22 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
     // plans written by m2c_cache_plan always pass; anything else is skipped
     if (t < 1 || t > 3 || id < 0 || id >= d_ff || slot < 0 || slot >= n_slots) continue;
     const int64_t bytes = src.stride[t];  // multiple of 16, <= slot_bytes
-    const uint4* s = reinterpret_cast<const uint4*>(src.host[t] + (int64_t)id * bytes);
-    uint4* dst = reinterpret_cast<uint4*>(slots + (int64_t)slot * slot_bytes);
+    const u32x4* s = reinterpret_cast<const u32x4*>(src.host[t] + (int64_t)id * bytes);
+    u32x4* dst = reinterpret_cast<u32x4*>(slots + (int64_t)slot * slot_bytes);
     const int nvec = (int)(bytes >> 4);
     int v = threadIdx.x;
     for (; v + 3 * kFillThreads < nvec; v += 4 * kFillThreads) {
-      const uint4 a = s[v], b = s[v + kFillThreads], c = s[v + 2 * kFillThreads],
-                  d = s[v + 3 * kFillThreads];
+      // host records are read once: non-temporal loads keep them out of the caches
+      const u32x4 a = __builtin_nontemporal_load(s + v);
+      const u32x4 b = __builtin_nontemporal_load(s + v + kFillThreads);
+      const u32x4 c = __builtin_nontemporal_load(s + v + 2 * kFillThreads);
+      const u32x4 d = __builtin_nontemporal_load(s + v + 3 * kFillThreads);
       dst[v] = a;
       dst[v + kFillThreads] = b;
       dst[v + 2 * kFillThreads] = c;
       dst[v + 3 * kFillThreads] = d;
     }
-    for (; v < nvec; v += kFillThreads) dst[v] = s[v];
+    for (; v < nvec; v += kFillThreads) dst[v] = __builtin_nontemporal_load(s + v);
   }
 }
 
@@ -56,7 +62,10 @@ hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stre
     src.host[t] = L->store->host[t];
     src.stride[t] = L->store->stride[t];
   }
-  int blocks = 2 * L->num_cus;
+  // The host link, not the CUs, bounds a fill: 64 workgroups keep about
+  // 1 MB of reads in flight, enough to cover its latency, while leaving the
+  // CUs and the memory system's request queues to the kernels that overlap.
+  int blocks = kFillBlocks;
   if (blocks > L->cap) blocks = L->cap > 0 ? L->cap : 1;
   hipLaunchKernelGGL(fill_kernel, dim3(blocks), dim3(kFillThreads), 0, stream,
                      reinterpret_cast<const int32_t*>(plan + lay.counts),

@@ -85,6 +85,8 @@ m2c_status check_desc(const m2c_layer_desc* D, int* S_out, int* cap_out) {
   if (S < need)
     return fail(M2C_ERR_INVALID_ARG, "staging_slots %d: at least %d are needed (or -1)",
                 D->staging_slots, need);
+  if (D->flags & ~M2C_FLAG_DETERMINISTIC_FFN)
+    return fail(M2C_ERR_INVALID_ARG, "flags 0x%x: unknown bits", D->flags);
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || D->device < 0 || D->device >= ndev)
     return fail(M2C_ERR_INVALID_ARG, "device %d: %d HIP devices visible", D->device, ndev);
@@ -156,15 +158,17 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   const int64_t d = D.d_model, dff = D.d_ff, r = D.pred_rank, C = D.cache_slots;
   const int64_t cap = L->cap, mb = D.max_batch;
   const int n_slices = (int)((d + 511) / 512);
+  // (column slices) x (neuron groups) workgroups for the down projection:
+  // about 512, at most 64 partial rows, groups of at least 16 neurons.
   int ng = 512 / n_slices;
   if (ng < 1) ng = 1;
-  if (ng > 32) ng = 32;
+  if (ng > 64) ng = 64;
   const int ng_cap = (int)(cap / 16 > 1 ? cap / 16 : 1);
   if (ng > ng_cap) ng = ng_cap;
   L->ffn_groups = ng;
   struct Piece { void** dst; int64_t bytes; };
   void* p_pred_a; void* p_pred_b; void* p_bias; void* p_z; void* p_scores; void* p_slots;
-  void* p_h; void* p_ypart; void* p_ctr; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
+  void* p_h; void* p_ypart; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
   void* p_vslot; void* p_vold; void* p_stats;
   Piece pieces[] = {
@@ -174,9 +178,8 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_bias, with_bias ? dff * 4 : 0},
       {&p_z, mb * r * 4},
       {&p_scores, mb * dff * 4},
-      {&p_h, cap * mb * 4},
+      {&p_h, 4 * cap * mb * 8},
       {&p_ypart, (int64_t)ng * mb * d * 4},
-      {&p_ctr, 64},
       {&p_slot_of, dff * 4},
       {&p_slot_key, C * 4},
       {&p_slot_tier, C},
@@ -207,9 +210,8 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->bias = with_bias ? (float*)p_bias : nullptr;
   L->z = (float*)p_z;
   L->scores = (float*)p_scores;
-  L->h = (float*)p_h;
+  L->ab = (float2*)p_h;
   L->y_part = (float*)p_ypart;
-  L->ffn_ctr = (int32_t*)p_ctr;
   L->st.slot_of = (int32_t*)p_slot_of;
   L->st.slot_key = (int32_t*)p_slot_key;
   L->st.slot_tier = (uint8_t*)p_slot_tier;
@@ -222,7 +224,6 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.vict_old = (int32_t*)p_vold;
   L->st.stats = (unsigned long long*)p_stats;
   L->info.device_bytes = total;
-  HIPOK(hipMemset(p_ctr, 0, 64), "hipMemset(work counters)");
   return M2C_OK;
 }
 

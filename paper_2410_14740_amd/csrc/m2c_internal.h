@@ -5,7 +5,7 @@
 #include <hip/hip_fp16.h>
 #include <stdint.h>
 
-#include "../../include/m2c.h"
+#include "m2c.h"
 
 namespace m2c {
 
@@ -58,9 +58,8 @@ struct m2c_layer {
   float* z = nullptr;          // [max_batch][r]
   float* scores = nullptr;     // [max_batch][d_ff]
   uint8_t* slots = nullptr;    // [C+S][slot_bytes]
-  float* h = nullptr;          // [cap] FFN hidden activations in work order
-  float* y_part = nullptr;     // [ffn_groups][d] down-projection partials
-  int32_t* ffn_ctr = nullptr;  // [4] work-grab counters (self-resetting)
+  float2* ab = nullptr;        // [4 * cap] partial gate/up dot products per FFN unit
+  float* y_part = nullptr;     // [ffn_groups][d] down-projection partial rows
   int ffn_groups = 1;
   m2c::DeviceState st;
   int64_t last_step = -1;
@@ -87,6 +86,8 @@ hipError_t launch_reset(m2c_layer* L, hipStream_t stream);
 hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
 hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
                       hipStream_t stream);
+hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
+                            hipStream_t stream);
 
 // ---------------------------------------------------------------------------
 // Device helpers shared by the kernels

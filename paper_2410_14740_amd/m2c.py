@@ -34,10 +34,13 @@ class M2CError(RuntimeError):
         super().__init__(f"m2c {name}: {msg}")
 
 
+FLAG_DETERMINISTIC_FFN = 1
+
+
 class LayerDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "d_model", "d_ff", "pred_rank", "group", "k_max", "max_batch", "cache_slots",
-        "staging_slots", "device")]
+        "staging_slots", "device", "flags")]
 
 
 class LayerInfo(ctypes.Structure):
@@ -265,6 +268,7 @@ class Layer:
         m2c_cache_fill(self.handle, self.plan if plan is None else plan, stream)
 
     def sparse_ffn(self, x, batch, y, stream=None, plan=None):
+        """y += FFN(x) (zero y first for the plain output)."""
         m2c_sparse_ffn(self.handle, x, batch, self.plan if plan is None else plan, y, stream)
 
     def reset_cache(self, stream=None):
@@ -308,6 +312,6 @@ class Layer:
 
 
 def make_desc(d_model, d_ff, pred_rank, k_max, cache_slots, max_batch=1, staging_slots=-1,
-              device=0) -> LayerDesc:
+              device=0, flags=0) -> LayerDesc:
     return LayerDesc(d_model, d_ff, pred_rank, 128, k_max, max_batch, cache_slots, staging_slots,
-                     device)
+                     device, flags)

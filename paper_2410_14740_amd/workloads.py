@@ -169,18 +169,23 @@ class LayerData:
 
 def make_layer(seed: int, layer: int, d: int, d_ff: int, r: int, steps: int, rhos=(0.9,),
                sigma_w: float = 0.02, sigma_p: float = 0.05, zipf_bias: bool = False,
-               weight_layer: int | None = None) -> LayerData:
+               weight_layer: int | None = None, draw_weights: bool = True) -> LayerData:
     """Draw one layer. `weight_layer` selects whose weights to draw (to let
-    several layers of a stack share one weight set); default: this layer."""
+    several layers of a stack share one weight set); default: this layer.
+    With draw_weights=False the weight fields are None (a layer that will read
+    another layer's neuron store)."""
     wl = layer if weight_layer is None else weight_layer
-    wg, wu, wd = layer_weights(seed, wl, d, d_ff, sigma_w)
+    if draw_weights:
+        wg, wu, wd = layer_weights(seed, wl, d, d_ff, sigma_w)
+    else:
+        wg = wu = wd = None
     A, Bm, bias = layer_predictor(seed, layer, d, d_ff, r, sigma_p, zipf_bias)
     x = layer_inputs(seed, layer, d, steps, rhos)
     return LayerData(d, d_ff, r, wg, wu, wd, A, Bm, bias, x)
 
 
 def workload_layer(wl: Workload, layer: int, steps: int | None = None, batch: int | None = None,
-                   weight_layer: int | None = None) -> LayerData:
+                   weight_layer: int | None = None, draw_weights: bool = True) -> LayerData:
     return make_layer(wl.seed, layer, wl.d_model, wl.d_ff, wl.pred_rank,
                       wl.steps if steps is None else steps, batch_rhos(wl, batch),
-                      wl.sigma_w, wl.sigma_p, wl.zipf_bias, weight_layer)
+                      wl.sigma_w, wl.sigma_p, wl.zipf_bias, weight_layer, draw_weights)

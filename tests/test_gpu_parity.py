@@ -30,8 +30,9 @@ def _x16(ld, t):
     return _dev(ld.x[t].view(np.uint16)).view(torch.float16)
 
 
-def _layer(ld, k_max, C, max_batch=1, staging=-1):
-    desc = m2c.make_desc(ld.d_model, ld.d_ff, ld.pred_rank, k_max, C, max_batch, staging)
+def _layer(ld, k_max, C, max_batch=1, staging=-1, flags=0):
+    desc = m2c.make_desc(ld.d_model, ld.d_ff, ld.pred_rank, k_max, C, max_batch, staging,
+                         flags=flags)
     return m2c.Layer(desc, ld)
 
 
@@ -86,11 +87,11 @@ def _compare_plan(g, o, step):
     assert np.array_equal(g["counts"][:13], o["counts"][:13]), f"step {step}: counts differ"
 
 
-def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label=""):
+def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flags=0):
     """predict -> plan -> fill -> FFN on the GPU and in the oracle, step by
     step, comparing every stage."""
     d_ff = ld.d_ff
-    L = _layer(ld, k, C, max_batch=batch)
+    L = _layer(ld, k, C, max_batch=batch, flags=flags)
     cache = oracle.LRUCache(d_ff, C, L.info.staging_slots)
     tiers = torch.empty((batch, d_ff), dtype=torch.uint8, device="cuda")
     y = torch.empty((batch, ld.d_model), dtype=torch.float32, device="cuda")
@@ -103,6 +104,7 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label=""):
         L.cache_plan(tiers, batch, t)
         L.cache_fill()
         if check_ffn and batch == 1:
+            y.zero_()
             L.sparse_ffn(x, batch, y)
         torch.cuda.synchronize()
         tm_ref = np.stack([oracle.select_tiers(oracle.predict(ld.pred_a, ld.pred_b, ld.bias,
@@ -131,13 +133,14 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label=""):
     return worst
 
 
+@pytest.mark.parametrize("flags", [0, m2c.FLAG_DETERMINISTIC_FFN])
 @pytest.mark.parametrize("name,d,d_ff,r,seed", SHAPES)
-def test_end_to_end_steps(name, d, d_ff, r, seed):
+def test_end_to_end_steps(name, d, d_ff, r, seed, flags):
     ld = W.make_layer(seed, 2, d, d_ff, r, 10, rhos=(0.8,))
     k = d_ff // 4
     n16, n8 = _counts(k)
     # C < k forces evictions and bypasses every step
-    _run_steps(ld, 10, k, n16, n8, C=(2 * k) // 3, label=f"e2e {name}")
+    _run_steps(ld, 10, k, n16, n8, C=(2 * k) // 3, label=f"e2e {name} flags={flags}", flags=flags)
 
 
 def test_tiny_workload_all_steps():
@@ -168,6 +171,7 @@ def test_dense_equivalence_all_fp16():
         L.predict_rank(x, 1, d_ff, d_ff, 0, None, tiers)
         L.cache_plan(tiers, 1, t)
         L.cache_fill()
+        y.zero_()
         L.sparse_ffn(x, 1, y)
         torch.cuda.synchronize()
         assert (tiers.cpu().numpy() == 3).all()
@@ -193,6 +197,7 @@ def test_k_zero_and_all_equal_scores():
     L.predict_rank(x, 1, 0, 0, 0, None, tiers)
     L.cache_plan(tiers, 1, 0)
     L.cache_fill()
+    y.zero_()
     L.sparse_ffn(x, 1, y)
     torch.cuda.synchronize()
     assert not tiers.cpu().numpy().any()
@@ -254,3 +259,44 @@ def test_llama70b_layer_shape():
     k, n16, n8 = wl.counts()
     worst = _run_steps(ld, 3, k, n16, n8, wl.cache_slots(), label="70B layer")
     say(f"70B layer worst FFN error {worst:.2e}")
+
+
+@pytest.mark.parametrize("d,d_ff", [(1024, 2752), (4096, 3000), (8192, 3000)])
+def test_ffn_modes_accumulate_and_determinism(d, d_ff):
+    """Both FFN paths add into y; the deterministic path repeats bit for bit
+    and the fused path agrees with it to fp32 rounding. (Each of the fused
+    path's per-workgroup atomic adds rounds at the magnitude of what y already
+    holds, so the cross-mode check starts from y = 0.)"""
+    ld = W.make_layer(61, 0, d, d_ff, 64, 1)
+    k = d_ff // 5
+    n16, n8 = _counts(k, (1, 10), (2, 5))
+    outs = {}
+    for flags in (0, m2c.FLAG_DETERMINISTIC_FFN):
+        say(f"ffn modes d={d} flags={flags}")
+        L = _layer(ld, k, k, flags=flags)
+        tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
+        x = _x16(ld, 0)
+        L.predict_rank(x, 1, k, n16, n8, None, tiers)
+        L.cache_plan(tiers, 1, 0)
+        L.cache_fill()
+        ys = []
+        for _ in range(3):
+            y = torch.zeros((1, d), dtype=torch.float32, device="cuda")
+            L.sparse_ffn(x, 1, y)
+            ys.append(y)
+        base = torch.linspace(-1.0, 1.0, d, device="cuda").reshape(1, d)
+        yb = base.clone()
+        L.sparse_ffn(x, 1, yb)
+        torch.cuda.synchronize()
+        ys = [yy.cpu().numpy()[0] for yy in ys]
+        if flags:
+            assert all(np.array_equal(ys[0], yy) for yy in ys[1:])
+        plan = L.read_plan()
+        y_ref = oracle_ffn(ld, ld.x[0], plan["req_ids"], plan["req_tier"])[0]
+        for yy in ys:
+            assert r8_errors(yy, y_ref).max() <= FFN_TOL
+        acc = (yb - base).cpu().numpy()[0].astype(np.float64)
+        assert r8_errors(acc, y_ref).max() <= FFN_TOL  # accumulated into y
+        outs[flags] = ys[0]
+        L.close()
+    assert r8_errors(outs[0], outs[m2c.FLAG_DETERMINISTIC_FFN]).max() <= 1e-4
