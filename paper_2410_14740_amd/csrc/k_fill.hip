@@ -11,8 +11,11 @@
 
 namespace m2c {
 
+#ifndef M2C_FILL_BLOCKS
+#define M2C_FILL_BLOCKS 64
+#endif
 constexpr int kFillThreads = 256;
-constexpr int kFillBlocks = 64;
+constexpr int kFillBlocks = M2C_FILL_BLOCKS;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
