@@ -31,6 +31,7 @@ if ROOT not in sys.path:
 
 METRIC = "sparse MP-FFN µs/layer-step + tokens/s; achieved HBM GB/s vs MI355X peak"
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, vendor figure
+PEAK_HOST_LINK_GBPS = 64.0  # PCIe Gen5 x16, one direction, before protocol overhead
 
 
 def parse_args():
@@ -45,16 +46,18 @@ def parse_args():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle baseline sample (0 = skip)")
     p.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
-    p.add_argument("--gemv-workload", default="llama2-70b",
-                   help="layer shape of the isolated sparse-FFN measurement ('' = skip)")
-    p.add_argument("--gemv-layers", type=int, default=8,
-                   help="layers cycled by the isolated measurement (their slots exceed the "
-                        "256 MB Infinity Cache, so it measures HBM, not the cache)")
-    p.add_argument("--gemv-reps", type=int, default=20)
+    p.add_argument("--ffn-layers", type=int, default=16,
+                   help="layers cycled by the isolated sparse-FFN measurement on the workload's "
+                        "layer shape (their active records exceed the 256 MB Infinity Cache)")
+    p.add_argument("--ffn-reps", type=int, default=10, help="passes over those layers")
+    p.add_argument("--target-workload", default="llama2-70b",
+                   help="second isolated sparse-FFN measurement on this layer shape ('' = skip)")
+    p.add_argument("--target-layers", type=int, default=8)
     p.add_argument("--deterministic-ffn", action="store_true",
                    help="use the three-kernel sparse FFN whose output repeats bit for bit")
-    p.add_argument("--only-gemv", action="store_true",
-                   help="run only the isolated sparse-FFN measurement (for profiling)")
+    p.add_argument("--only-ffn", default="", metavar="WORKLOAD",
+                   help="run only the isolated sparse-FFN measurement on this layer shape "
+                        "(for profiling)")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                    help="only copy a buffer of this many MB device to device, 5 times "
                         "(a plain copy kernel of known size, to scale HBM counters)")
@@ -141,11 +144,53 @@ def cpu_baseline(wl, ld, n_layers, budget_s, oracle):
             "ms_per_layer_step": per * 1e3}
 
 
-def gemv_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
+def hold_stream(torch, s, host_seconds):
+    """Enqueue a spin kernel on `s` that lasts longer than `host_seconds` of
+    host work, so that everything the host enqueues behind it runs back to
+    back on the GPU (measured launches are then not spaced out by the host's
+    own enqueue time). Returns the event recorded before the spin."""
+    probe = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(s):
+        probe[0].record(s)
+        torch.cuda._sleep(1 << 20)
+        probe[1].record(s)
+        torch.cuda.synchronize()
+        ms_per_cycle = max(probe[0].elapsed_time(probe[1]), 1e-3) / float(1 << 20)
+        # twice the host time, at most two seconds
+        ms = min(2.0 * host_seconds * 1e3, 2000.0)
+        cycles = int(ms / ms_per_cycle) + (1 << 20)
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(s)
+        torch.cuda._sleep(cycles)
+    return start
+
+
+def timed_back_to_back(torch, s, calls, host_seconds):
+    """Run `calls` (zero-argument launchers) back to back on stream `s`
+    behind a spin kernel, between one pair of HIP events. Returns the average
+    time per call in ms and whether the spin outlasted the host's enqueue
+    (if not, the GPU waited on the host and the average is too high)."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start = hold_stream(torch, s, host_seconds)
+    t0 = time.perf_counter()
+    e0.record(s)
+    for fn in calls:
+        fn()
+    e1.record(s)
+    enq_ms = (time.perf_counter() - t0) * 1e3
+    torch.cuda.synchronize()
+    covered = start.elapsed_time(e0) > enq_ms
+    return e0.elapsed_time(e1) / len(calls), covered
+
+
+def ffn_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
     """The sparse FFN alone on `n_layers` layers of workload `wl`'s shape that
-    share one weight store: a few warm-up decode steps fill every cache, then
-    the FFN of each layer is launched back to back, cycling through the
-    layers, on one stream. Returns the HBM roofline of the FFN call."""
+    share one neuron store: a few decode steps fill every layer's cache, then
+    the FFN of each layer is launched `reps` times, cycling through the layers
+    (their active records exceed the 256 MB Infinity Cache for the 70B shape,
+    so the data comes from HBM), back to back on one stream. Returns the HBM
+    roofline of the FFN call (algorithmic bytes: every active record at its
+    tier, x and y)."""
     k, n16, n8 = wl.counts()
     n4 = k - n16 - n8
     C = wl.cache_slots()
@@ -158,7 +203,7 @@ def gemv_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
                        torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16).cuda()))
     d, d_ff = wl.d_model, wl.d_ff
     tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
-    y = torch.empty((1, d), dtype=torch.float32, device="cuda")
+    y = torch.zeros((1, d), dtype=torch.float32, device="cuda")
     s = torch.cuda.current_stream()
     for t in range(steps):
         for L, x in layers:
@@ -167,25 +212,24 @@ def gemv_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
             L.cache_fill(stream=s)
             L.sparse_ffn(x[t], 1, y, stream=s)
     torch.cuda.synchronize()
-    ev = []
-    for r in range(reps):
-        for L, x in layers:
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(s)
-            L.sparse_ffn(x[steps - 1], 1, y, stream=s)
-            b.record(s)
-            ev.append((a, b))
+    calls = [(lambda L=L, x=x: L.sparse_ffn(x[steps - 1], 1, y, stream=s))
+             for _ in range(reps) for L, x in layers]
+    t0 = time.perf_counter()
+    for fn in calls[:n_layers]:
+        fn()
     torch.cuda.synchronize()
-    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    per_call = (time.perf_counter() - t0) / n_layers
+    ms, covered = timed_back_to_back(torch, s, calls, per_call * len(calls) * 10 + 0.05)
     rb = layers[0][0].info.record_bytes
-    nbytes = n16 * rb[3] + n8 * rb[2] + n4 * rb[1] + 6 * d
-    avg = float(ms.mean()) * 1e-3
+    nbytes = n16 * rb[3] + n8 * rb[2] + n4 * rb[1] + 2 * d + 4 * d
+    avg = ms * 1e-3
     for L, _ in layers:
         L.close()
-    return {"workload": wl.name, "layers_cycled": n_layers, "launches": len(ev),
-            "us_avg": avg * 1e6, "us_min": float(ms.min()) * 1e3,
-            "bytes_per_launch": nbytes, "achieved_GBps": nbytes / avg / 1e9,
-            "frac_of_peak": nbytes / avg / 1e9 / PEAK_HBM_GBPS}
+    if not covered:
+        log("warning: the host enqueue outlasted the stream hold; FFN time is overstated")
+    return {"workload": wl.name, "layers_cycled": n_layers, "launches": len(calls),
+            "us_avg": avg * 1e6, "bytes_per_launch": nbytes, "achieved_GBps": nbytes / avg / 1e9,
+            "frac_of_peak": nbytes / avg / 1e9 / PEAK_HBM_GBPS, "host_hidden": bool(covered)}
 
 
 def main():
@@ -214,10 +258,11 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n, "launches": 5}), flush=True)
         return
     ffn_flags = m2c.FLAG_DETERMINISTIC_FFN if args.deterministic_ffn else 0
-    if args.only_gemv:
-        g = gemv_isolated(W.WORKLOADS[args.gemv_workload], args.gemv_layers, args.gemv_reps,
-                          torch, m2c, W, flags=ffn_flags)
-        print(json.dumps({"gemv_isolated": g}), flush=True)
+    if args.only_ffn:
+        wl_f = W.WORKLOADS[args.only_ffn]
+        g = ffn_isolated(wl_f, args.ffn_layers if args.only_ffn == args.workload else args.target_layers,
+                         args.ffn_reps, torch, m2c, W, flags=ffn_flags)
+        print(json.dumps({"ffn_isolated": g}), flush=True)
         return
     wl = W.WORKLOADS[args.workload]
     n_layers = args.layers or wl.n_layers
@@ -290,18 +335,20 @@ def main():
     bypass = sum(b.bypass - a.bypass for a, b in zip(st0, st1))
     fill_bytes = sum(b.fill_bytes - a.fill_bytes for a, b in zip(st0, st1))
     n_ls = args.steps * n_layers
-    ffn_avg_s = float(ffn_ms.mean()) * 1e-3
-    achieved = ffn_bytes / ffn_avg_s / 1e9
+    fill_avg_s = float(fill_ms.mean()) * 1e-3
+    fill_Bps = fill_bytes / n_ls / fill_avg_s
     tokens_per_s = args.steps / wall
 
     for L in layers:
         L.close()
     layers = []
-    gemv = None
-    if args.gemv_workload:
-        log(f"isolated sparse FFN on {args.gemv_layers} {args.gemv_workload} layers")
-        gemv = gemv_isolated(W.WORKLOADS[args.gemv_workload], args.gemv_layers, args.gemv_reps,
-                             torch, m2c, W, flags=ffn_flags)
+    log(f"isolated sparse FFN on {args.ffn_layers} {wl.name}-shaped layers")
+    iso = ffn_isolated(wl, args.ffn_layers, args.ffn_reps, torch, m2c, W, flags=ffn_flags)
+    target = None
+    if args.target_workload:
+        log(f"isolated sparse FFN on {args.target_layers} {args.target_workload}-shaped layers")
+        target = ffn_isolated(W.WORKLOADS[args.target_workload], args.target_layers,
+                              args.ffn_reps, torch, m2c, W, flags=ffn_flags)
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -309,6 +356,13 @@ def main():
         log("timing the oracle on the host")
         cpu = cpu_baseline(wl, ld0, n_layers, args.cpu_seconds, oracle)
 
+    # HBM bytes per call from the committed counter summary of this layer
+    # shape, or None when the FFN kernels have changed since it was taken
+    from paper_2410_14740_amd import rocprof_summary
+    ffn_traffic = None if args.deterministic_ffn else rocprof_summary.read_ffn_traffic(
+        os.path.join(ROOT, "profiles", f"sparse_ffn_{wl.name}_layer.md"))
+    ffn_kind = ("three kernels (up, down, ordered reduce), deterministic" if args.deterministic_ffn
+                else "two kernels (h, down by column slice)")
     out = {
         "metric": METRIC,
         "value": tokens_per_s,
@@ -326,23 +380,36 @@ def main():
             "workload": wl.name, "layers": n_layers, "d_model": d, "d_ff": d_ff,
             "pred_rank": wl.pred_rank, "k": k, "tiers_fp16_int8_int4": [n16, n8, n4],
             "cache_slots": wl.cache_slots(), "batch": 1, "decode_steps": steps_total,
-            "weights": "fp16 records with int8/int4 copies (group 128, fp16 scales)",
+            "weights": "fp16 records with int8/int4 copies (group 128, fp16 scales), "
+                       "pinned host store",
             "distinct_weight_sets": args.weight_sets or n_layers,
-            "ffn": "three kernels, deterministic" if args.deterministic_ffn else "fused kernel",
+            "ffn": ffn_kind,
         },
         "us_per_layer_step": wall / n_ls * 1e6,
-        "ffn_us_avg": ffn_avg_s * 1e6,
-        "fill_us_avg": float(fill_ms.mean()) * 1e3,
-        "fill_MB_per_layer_step": fill_bytes / n_ls / 1e6,
-        "host_link_GBps_in_fill": fill_bytes / n_ls / (float(fill_ms.mean()) * 1e-3) / 1e9,
-        "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
-                  "bypass_rate": bypass / max(reqs, 1)},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBPS, "traffic": None,
-                     "kernel": "m2c_sparse_ffn (ffn_up + ffn_down + ffn_reduce)",
-                     "bytes_per_launch": ffn_bytes},
+        "pipeline": {
+            "ffn_us_avg": float(ffn_ms.mean()) * 1e3,
+            "fill_us_avg": fill_avg_s * 1e6,
+            "fill_MB_per_layer_step": fill_bytes / n_ls / 1e6,
+            "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
+                      "bypass_rate": bypass / max(reqs, 1)},
+        },
+        # the step's gather-GEMV (m2c_sparse_ffn: ffn_h_kernel + ffn_dn_kernel),
+        # algorithmic bytes per call over the per-call time of back-to-back calls
+        "roofline": {"bound": "hbm", "achieved": iso["achieved_GBps"], "peak": PEAK_HBM_GBPS,
+                     "unit": "GB/s", "frac": iso["achieved_GBps"] / PEAK_HBM_GBPS,
+                     "traffic": ffn_traffic, "kernel": "m2c_sparse_ffn (ffn_h_kernel + ffn_dn_kernel)",
+                     "workload": f"{wl.name} layer shape, {args.ffn_layers} layers cycled",
+                     "bytes_per_launch": iso["bytes_per_launch"], "us_per_launch": iso["us_avg"]},
+        "roofline_target_layer": None if target is None else {
+            "bound": "hbm", "achieved": target["achieved_GBps"], "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s", "frac": target["achieved_GBps"] / PEAK_HBM_GBPS,
+            "workload": f"{target['workload']} layer shape, {args.target_layers} layers cycled",
+            "bytes_per_launch": target["bytes_per_launch"], "us_per_launch": target["us_avg"]},
+        # the fills are bound by the host link, not by HBM
+        "host_link": {"kernel": "fill_kernel (device gather from pinned host memory)",
+                      "achieved": fill_Bps / 1e9, "peak": PEAK_HOST_LINK_GBPS, "unit": "GB/s",
+                      "frac": fill_Bps / 1e9 / PEAK_HOST_LINK_GBPS},
         "cpu_baseline": cpu,
-        "gemv_isolated": gemv,
     }
     print(json.dumps(out), flush=True)
 

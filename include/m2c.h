@@ -138,10 +138,10 @@ typedef struct {
 /* m2c_layer_desc.flags */
 enum {
   /* Sparse FFN by three kernels (up, down by column slices, ordered reduce)
-     whose output is the same bit pattern on every run. The default is one
-     fused kernel that adds workgroup partial rows into y with fp32 atomics,
-     so the summation order, and the last bits of y, vary from run to run.
-     Layers with d_model > 8192 always take the three-kernel path. */
+     whose output is the same bit pattern on every run. The default is two
+     kernels (h of every neuron, then the down projection by column slice and
+     neuron group) whose neuron groups are added into y with fp32 atomics,
+     so the summation order, and the last bits of y, vary from run to run. */
   M2C_FLAG_DETERMINISTIC_FFN = 1
 };
 
@@ -268,7 +268,11 @@ m2c_status m2c_sparse_ffn(m2c_layer* layer, const uint16_t* x, int32_t batch, co
  * cleared), on `stream`. */
 m2c_status m2c_layer_reset_cache(m2c_layer* layer, void* stream);
 
-/* Synchronizes the device, then reads the cumulative counters. */
+/* Synchronizes the device, then reads the cumulative counters. Returns
+ * M2C_ERR_CAPACITY (and clears the condition) if a cache plan since the last
+ * call received a tier map with more active neurons than the layer's plan
+ * capacity, min(d_ff, max_batch * k_max): such a plan is left empty and the
+ * cache unchanged. */
 m2c_status m2c_layer_stats(const m2c_layer* layer, m2c_stats* out);
 
 /* Test support. Copies one record of the host store (no device work). */

@@ -91,6 +91,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
     if (tid == 0) {
       for (int q = 0; q < M2C_NCOUNTS; ++q) P.counts[q] = 0;
       P.counts[M2C_NCOUNTS - 1] = NREQ;
+      atomicOr(st.status, M2C_STATUS_PLAN_OVERFLOW);
     }
     return;
   }

@@ -170,9 +170,11 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_pred_a; void* p_pred_b; void* p_bias; void* p_z; void* p_scores; void* p_slots;
   void* p_h; void* p_ypart; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
-  void* p_vslot; void* p_vold; void* p_stats;
+  void* p_vslot; void* p_vold; void* p_stats; void* p_status;
   Piece pieces[] = {
-      {&p_slots, (C + L->S) * (int64_t)L->info.slot_bytes},
+      // C resident + S staging slots, then one slot that stays zero: padding
+      // lanes of the FFN kernels read it instead of branching around loads
+      {&p_slots, (C + L->S + 1) * (int64_t)L->info.slot_bytes},
       {&p_pred_a, r * d * 2},
       {&p_pred_b, dff * r * 2},
       {&p_bias, with_bias ? dff * 4 : 0},
@@ -191,6 +193,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_vslot, cap * 4},
       {&p_vold, cap * 4},
       {&p_stats, 16 * 8},
+      {&p_status, 4},
   };
   int64_t total = 0;
   int64_t offs[sizeof(pieces) / sizeof(pieces[0])];
@@ -223,7 +226,11 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.vict_slot = (int32_t*)p_vslot;
   L->st.vict_old = (int32_t*)p_vold;
   L->st.stats = (unsigned long long*)p_stats;
+  L->st.status = (int32_t*)p_status;
   L->info.device_bytes = total;
+  HIPOK(hipMemset(L->slots + (C + L->S) * (int64_t)L->info.slot_bytes, 0, L->info.slot_bytes),
+        "clear the zero slot");
+  HIPOK(hipMemset(L->st.status, 0, 4), "clear the status word");
   return M2C_OK;
 }
 
@@ -482,8 +489,16 @@ m2c_status m2c_layer_stats(const m2c_layer* L, m2c_stats* out) {
   if (!L || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
   DeviceGuard g(L->desc.device);
   long long st[16];
+  int32_t status = 0;
   HIPOK(hipDeviceSynchronize(), "synchronize");
   HIPOK(hipMemcpy(st, L->st.stats, sizeof(st), hipMemcpyDeviceToHost), "read stats");
+  HIPOK(hipMemcpy(&status, L->st.status, 4, hipMemcpyDeviceToHost), "read status");
+  if (status) {
+    HIPOK(hipMemset(L->st.status, 0, 4), "clear the status word");
+    return fail(M2C_ERR_CAPACITY, "a cache plan since the last check had more active neurons than "
+                "the layer was created for (k_max * max_batch); it was left empty (status 0x%x)",
+                status);
+  }
   memset(out, 0, sizeof(*out));
   out->plans = st[0];
   out->req = st[1];

@@ -9,6 +9,10 @@
 
 namespace m2c {
 
+// Bits of the per-layer device status word, reported (and cleared) by
+// m2c_layer_stats.
+constexpr int M2C_STATUS_PLAN_OVERFLOW = 2;  // a tier map had more active neurons than cap
+
 // ---------------------------------------------------------------------------
 // Host-side layer object
 
@@ -37,6 +41,7 @@ struct DeviceState {
   int32_t* vict_slot = nullptr;  // [cap] plan scratch
   int32_t* vict_old = nullptr;   // [cap] plan scratch
   unsigned long long* stats = nullptr;  // [16] cumulative counters
+  int32_t* status = nullptr;           // [1] M2C_STATUS_* bits set by kernels
 };
 
 }  // namespace m2c
@@ -86,7 +91,7 @@ hipError_t launch_reset(m2c_layer* L, hipStream_t stream);
 hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
 hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
                       hipStream_t stream);
-hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
+hipError_t launch_ffn_split(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
                             hipStream_t stream);
 
 // ---------------------------------------------------------------------------

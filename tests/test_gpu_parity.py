@@ -300,3 +300,23 @@ def test_ffn_modes_accumulate_and_determinism(d, d_ff):
         outs[flags] = ys[0]
         L.close()
     assert r8_errors(outs[0], outs[m2c.FLAG_DETERMINISTIC_FFN]).max() <= 1e-4
+
+
+def test_plan_overflow_is_reported():
+    """A tier map with more active neurons than the plan capacity leaves the
+    plan empty and the cache unchanged; m2c_layer_stats reports it once."""
+    ld = W.make_layer(17, 0, 256, 200, 16, 2)
+    L = _layer(ld, 20, 30)  # capacity min(d_ff, 1 * 20) = 20
+    tiers = torch.full((1, 200), 1, dtype=torch.uint8, device="cuda")  # 200 active
+    say("plan overflow")
+    L.cache_plan(tiers, 1, 0)
+    torch.cuda.synchronize()
+    assert L.read_plan()["counts"][m2c.CNT_REQ] == 0
+    with pytest.raises(m2c.M2CError) as e:
+        L.stats()
+    assert e.value.status == m2c.M2C_ERR_CAPACITY
+    st = L.stats()  # reported once, then cleared
+    assert st.req == 0 and st.plans == 0
+    slot_of, key, _, _ = m2c.m2c_debug_read_tables(L.handle, 200, 30)
+    assert (slot_of == -1).all() and (key == -1).all()
+    L.close()
