@@ -260,7 +260,11 @@ m2c_status m2c_cache_fill(m2c_layer* layer, const void* plan, void* stream);
  * neuron's step tier; fp32 accumulation. The result is ADDED to y (a residual
  * stream); zero y first for the plain FFN output.
  *   x dev fp16 [batch][d_model];  y dev fp32 [batch][d_model], in/out.
- * `batch` must equal the batch given to the plan. */
+ * `batch` (1..max_batch) must equal the batch given to the plan. Batch 1 is a
+ * gather-dequant GEMV; larger batches run the gate / up contraction on the
+ * matrix cores (fp16 operands: the codes, exact, and x; fp32 accumulation,
+ * group scales applied in fp32) and are never bit-deterministic (the
+ * deterministic flag applies to batch 1). */
 m2c_status m2c_sparse_ffn(m2c_layer* layer, const uint16_t* x, int32_t batch, const void* plan,
                           float* y, void* stream);
 

@@ -471,7 +471,8 @@ m2c_status m2c_cache_fill(m2c_layer* L, const void* plan, void* stream) {
 m2c_status m2c_sparse_ffn(m2c_layer* L, const uint16_t* x, int32_t batch, const void* plan,
                           float* y, void* stream) {
   if (!L || !x || !plan || !y) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
-  if (batch != 1) return fail(M2C_ERR_CAPACITY, "sparse FFN: batch %d not supported yet", batch);
+  if (batch < 1 || batch > L->desc.max_batch)
+    return fail(M2C_ERR_CAPACITY, "batch %d outside [1, max_batch=%d]", batch, L->desc.max_batch);
   DeviceGuard g(L->desc.device);
   HIPOK(m2c::launch_ffn(L, x, batch, (const uint8_t*)plan, y, (hipStream_t)stream), "ffn launch");
   return M2C_OK;

@@ -91,6 +91,8 @@ hipError_t launch_reset(m2c_layer* L, hipStream_t stream);
 hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
 hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
                       hipStream_t stream);
+hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan,
+                            float* y, hipStream_t stream);
 hipError_t launch_ffn_split(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
                             hipStream_t stream);
 

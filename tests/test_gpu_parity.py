@@ -103,7 +103,7 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flag
         L.predict_rank(x, batch, k, n16, n8, None, tiers)
         L.cache_plan(tiers, batch, t)
         L.cache_fill()
-        if check_ffn and batch == 1:
+        if check_ffn:
             y.zero_()
             L.sparse_ffn(x, batch, y)
         torch.cuda.synchronize()
@@ -120,11 +120,14 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flag
         assert np.array_equal(key, cache.slot_key[:C])
         assert np.array_equal(stier, cache.slot_tier[:C])
         assert np.array_equal(last, cache.slot_last[:C])
-        if check_ffn and batch == 1:
-            y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"])
-            err = r8_errors(y.cpu().numpy(), y_ref).max()
-            worst = max(worst, err)
-            assert err <= FFN_TOL, f"step {t}: FFN error {err:.3e}"
+        if check_ffn:
+            y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"],
+                               o["req_mask"] if batch > 1 else None)
+            yg = y.cpu().numpy()
+            for b in range(batch):
+                err = r8_errors(yg[b], y_ref[b]).max()
+                worst = max(worst, err)
+                assert err <= FFN_TOL, f"step {t} row {b}: FFN error {err:.3e}"
     st = L.stats()
     assert (st.plans, st.req, st.hit, st.refill, st.new_, st.bypass, st.evict) == (
         steps, stats[0], stats[1], stats[2], stats[3], stats[4], stats[5])
@@ -152,10 +155,67 @@ def test_tiny_workload_all_steps():
 
 
 def test_batched_plan_union_and_bypass():
+    """Batch 4 on a ragged layer: union plans with bypasses, and the batched
+    (MFMA) FFN against the oracle's masked FFN, row by row."""
     ld = W.make_layer(77, 0, 384, 700, 48, 6, rhos=(0.5, 0.95, 0.9, 0.7), zipf_bias=True)
     k = 120
     n16, n8 = _counts(k, (1, 10), (2, 5))
-    _run_steps(ld, 6, k, n16, n8, C=200, batch=4, check_ffn=False, label="batched plan")
+    _run_steps(ld, 6, k, n16, n8, C=200, batch=4, label="batched plan")
+
+
+@pytest.mark.parametrize("batch,d,d_ff,r", [(2, 1024, 1000, 64), (20, 512, 900, 32)])
+def test_batched_ffn_shapes(batch, d, d_ff, r):
+    """Batch 2 (one MFMA column tile, one down pass) and batch 20 (two column
+    tiles, two down passes of up to 16 rows), mixed tiers, C below the union."""
+    rhos = tuple(0.5 + 0.45 * (b % 2) for b in range(batch))
+    ld = W.make_layer(300 + batch, 0, d, d_ff, r, 3, rhos=rhos, zipf_bias=True)
+    k = d_ff // 6
+    n16, n8 = _counts(k, (1, 5), (3, 10))
+    worst = _run_steps(ld, 3, k, n16, n8, C=k, batch=batch, label=f"batched B={batch}")
+    say(f"batched B={batch} worst FFN error {worst:.2e}")
+
+
+def test_batched_all_fp16_equals_single_token():
+    """All-FP16: row b of the batched FFN equals the single-token FFN of x_b
+    over row b's own selection (the union only adds neurons masked out of b)."""
+    d, d_ff, r, B = 512, 800, 32, 4
+    ld = W.make_layer(91, 0, d, d_ff, r, 1, rhos=(0.9, 0.5, 0.95, 0.7))
+    k = 100
+    Lb = _layer(ld, k, d_ff, max_batch=B)
+    tiers = torch.empty((B, d_ff), dtype=torch.uint8, device="cuda")
+    x = _x16(ld, 0)
+    Lb.predict_rank(x, B, k, k, 0, None, tiers)
+    Lb.cache_plan(tiers, B, 0)
+    Lb.cache_fill()
+    yb = torch.zeros((B, d), dtype=torch.float32, device="cuda")
+    Lb.sparse_ffn(x, B, yb)
+    torch.cuda.synchronize()
+    tm = tiers.cpu().numpy()
+    for b in range(B):
+        L1 = _layer(ld, k, d_ff)
+        t1 = torch.from_numpy(np.ascontiguousarray(tm[b:b + 1])).cuda()
+        L1.cache_plan(t1, 1, 0)
+        L1.cache_fill()
+        y1 = torch.zeros((1, d), dtype=torch.float32, device="cuda")
+        L1.sparse_ffn(x[b:b + 1], 1, y1)
+        torch.cuda.synchronize()
+        err = r8_errors(yb.cpu().numpy()[b], y1.cpu().numpy()[0].astype(np.float64)).max()
+        assert err <= 1e-4, f"row {b}: batched vs single {err:.2e}"
+        L1.close()
+    Lb.close()
+
+
+def test_batched_llama7b_b8_workload():
+    """The batch-8 decode workload on the 7B-shaped layer (d 4096, d_ff 11008,
+    rank 256, k 2201 per row with tiers 220/880/1101, log-Zipf popularity,
+    rho 0.5 / 0.95 rows, C = 30% of d_ff): plans bit-exact and every row of
+    the batched FFN within tolerance, two steps."""
+    wl = W.WORKLOADS["llama2-7b-b8"]
+    say("7B batch-8 layer: drawing weights")
+    ld = W.workload_layer(wl, 0, steps=2)
+    k, n16, n8 = wl.counts()
+    worst = _run_steps(ld, 2, k, n16, n8, wl.cache_slots(), batch=wl.batch, label="7B b8")
+    say(f"7B batch-8 worst FFN error {worst:.2e}")
 
 
 def test_dense_equivalence_all_fp16():
