@@ -24,6 +24,7 @@ import sys
 import time
 
 import numpy as np
+from fractions import Fraction as F
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -53,11 +54,17 @@ def parse_args():
     p.add_argument("--target-workload", default="llama2-70b",
                    help="second isolated sparse-FFN measurement on this layer shape ('' = skip)")
     p.add_argument("--target-layers", type=int, default=8)
+    p.add_argument("--stage-events", action="store_true",
+                   help="record HIP events around every fill and FFN of the timed steps (their "
+                        "markers add latency to the cross-stream waits; off for the headline)")
     p.add_argument("--deterministic-ffn", action="store_true",
                    help="use the three-kernel sparse FFN whose output repeats bit for bit")
     p.add_argument("--only-ffn", default="", metavar="WORKLOAD",
                    help="run only the isolated sparse-FFN measurement on this layer shape "
                         "(for profiling)")
+    p.add_argument("--batch-sweep", action="store_true",
+                   help="only the batched-decode workload (7B-shaped layer, batch 8): LRU capacity "
+                        "10/30/60%% x tiers 10/40/50 or all FP16, one JSON line")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                    help="only copy a buffer of this many MB device to device, 5 times "
                         "(a plain copy kernel of known size, to scale HBM counters)")
@@ -232,6 +239,76 @@ def ffn_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
             "frac_of_peak": nbytes / avg / 1e9 / PEAK_HBM_GBPS, "host_hidden": bool(covered)}
 
 
+def batched_sweep(steps, warmup, torch, m2c, W):
+    """The batched-decode workload: one 7B-shaped layer, batch 8 (rows with
+    rho 0.5 and 0.95, log-Zipf neuron popularity), predict -> plan -> fill ->
+    batched FFN per step on one stream, for LRU capacity 10 / 30 / 60 % of
+    d_ff and tiers 10/40/50 or all FP16. Per point: step time, tokens/s
+    (batch rows per second), the union's size and hit rate, fill traffic and
+    the FFN's algorithmic bytes over its time."""
+    wl = W.WORKLOADS["llama2-7b-b8"]
+    B = wl.batch
+    k, n16_m, n8_m = wl.counts()
+    ld = W.workload_layer(wl, 0, steps=warmup + steps)
+    x = torch.from_numpy(ld.x.view(np.uint16)).view(torch.float16).cuda()  # [steps][B][d]
+    d, d_ff = wl.d_model, wl.d_ff
+    tiers = torch.empty((B, d_ff), dtype=torch.uint8, device="cuda")
+    y = torch.zeros((B, d), dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    owner, points = None, []
+    for cap in (F(1, 10), F(3, 10), F(3, 5)):
+        for mix in ("10/40/50", "fp16"):
+            n16, n8 = (n16_m, n8_m) if mix != "fp16" else (k, 0)
+            C = int(d_ff * cap // 1)
+            desc = m2c.make_desc(d, d_ff, wl.pred_rank, k, C, max_batch=B)
+            L = m2c.Layer(desc, ld, weights_of=owner)
+            if owner is None:
+                owner = L
+            ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+            for t in range(warmup + steps):
+                e = ev[t - warmup] if t >= warmup else None
+                y.zero_()
+                if e:
+                    e[0].record(s)
+                L.predict_rank(x[t], B, k, n16, n8, None, tiers, stream=s)
+                if e:
+                    e[1].record(s)
+                L.cache_plan(tiers, B, t, stream=s)
+                if e:
+                    e[2].record(s)
+                L.cache_fill(stream=s)
+                if e:
+                    e[3].record(s)
+                L.sparse_ffn(x[t], B, y, stream=s)
+                if e:
+                    e[4].record(s)
+                if t == warmup - 1:
+                    torch.cuda.synchronize()
+                    st0 = L.stats()
+            torch.cuda.synchronize()
+            st1 = L.stats()
+            ms = np.array([[e[i].elapsed_time(e[i + 1]) for i in range(4)] for e in ev])
+            step_ms = np.array([e[0].elapsed_time(e[4]) for e in ev])
+            req = st1.req - st0.req
+            ffn_bytes = (st1.req_bytes - st0.req_bytes) / steps + B * (2 * d + 4 * d)
+            ffn_s = float(ms[:, 3].mean()) * 1e-3
+            points.append({
+                "cache_frac": float(cap), "cache_slots": C, "tiers": mix,
+                "us_per_step": float(step_ms.mean()) * 1e3,
+                "tokens_per_s": B / (float(step_ms.mean()) * 1e-3),
+                "us_predict_plan_fill_ffn": [round(float(v) * 1e3, 2) for v in ms.mean(axis=0)],
+                "union_neurons": req / steps, "hit_rate": (st1.hit - st0.hit) / max(req, 1),
+                "bypass_rate": (st1.bypass - st0.bypass) / max(req, 1),
+                "fill_MB_per_step": (st1.fill_bytes - st0.fill_bytes) / steps / 1e6,
+                "ffn_bytes_per_step": ffn_bytes, "ffn_GBps": ffn_bytes / ffn_s / 1e9})
+            log(f"batched sweep: cache {float(cap):.0%} tiers {mix}: "
+                f"{points[-1]['us_per_step']:.1f} us/step")
+            if L is not owner:
+                L.close()
+    owner.close()
+    return {"workload": wl.name, "batch": B, "steps": steps, "warmup": warmup, "points": points}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -258,6 +335,10 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": n, "launches": 5}), flush=True)
         return
     ffn_flags = m2c.FLAG_DETERMINISTIC_FFN if args.deterministic_ffn else 0
+    if args.batch_sweep:
+        print(json.dumps({"batched_sweep": batched_sweep(min(args.steps, 56), args.warmup, torch,
+                                                          m2c, W)}), flush=True)
+        return
     if args.only_ffn:
         wl_f = W.WORKLOADS[args.only_ffn]
         g = ffn_isolated(wl_f, args.ffn_layers if args.only_ffn == args.workload else args.target_layers,
@@ -322,20 +403,23 @@ def main():
     st0 = [L.stats() for L in layers]
     t0 = time.perf_counter()
     for t in range(args.warmup, steps_total):
-        step(t, True)
+        step(t, args.stage_events)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st1 = [L.stats() for L in layers]
 
-    ffn_ms = np.array([e[0].elapsed_time(e[1]) for e in timing])
-    fill_ms = np.array([e[2].elapsed_time(e[3]) for e in timing])
+    ffn_ms = np.array([e[0].elapsed_time(e[1]) for e in timing]) if timing else None
+    fill_ms = np.array([e[2].elapsed_time(e[3]) for e in timing]) if timing else None
     reqs = sum(b.req - a.req for a, b in zip(st0, st1))
     hits = sum(b.hit - a.hit for a, b in zip(st0, st1))
     refills = sum(b.refill - a.refill for a, b in zip(st0, st1))
     bypass = sum(b.bypass - a.bypass for a, b in zip(st0, st1))
     fill_bytes = sum(b.fill_bytes - a.fill_bytes for a, b in zip(st0, st1))
     n_ls = args.steps * n_layers
-    fill_avg_s = float(fill_ms.mean()) * 1e-3
+    # host-link rate of the fills: from the stage events if recorded, else
+    # the fill bytes over the wall time (a lower bound: fills run back to
+    # back only when nothing else is on the critical path)
+    fill_avg_s = float(fill_ms.mean()) * 1e-3 if fill_ms is not None else wall / n_ls
     fill_Bps = fill_bytes / n_ls / fill_avg_s
     tokens_per_s = args.steps / wall
 
@@ -387,8 +471,9 @@ def main():
         },
         "us_per_layer_step": wall / n_ls * 1e6,
         "pipeline": {
-            "ffn_us_avg": float(ffn_ms.mean()) * 1e3,
-            "fill_us_avg": fill_avg_s * 1e6,
+            "stage_events": bool(args.stage_events),
+            "ffn_us_avg": float(ffn_ms.mean()) * 1e3 if ffn_ms is not None else None,
+            "fill_us_avg": fill_avg_s * 1e6 if fill_ms is not None else None,
             "fill_MB_per_layer_step": fill_bytes / n_ls / 1e6,
             "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
                       "bypass_rate": bypass / max(reqs, 1)},
@@ -408,7 +493,8 @@ def main():
         # the fills are bound by the host link, not by HBM
         "host_link": {"kernel": "fill_kernel (device gather from pinned host memory)",
                       "achieved": fill_Bps / 1e9, "peak": PEAK_HOST_LINK_GBPS, "unit": "GB/s",
-                      "frac": fill_Bps / 1e9 / PEAK_HOST_LINK_GBPS},
+                      "frac": fill_Bps / 1e9 / PEAK_HOST_LINK_GBPS,
+                      "measured_over": "fill kernels" if fill_ms is not None else "wall time"},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -200,6 +200,9 @@ typedef struct {
   int64_t req, hit, refill, new_, bypass, evict;
   int64_t fill[4];        /* fills by tier                                    */
   int64_t fill_bytes;     /* sum of record_bytes over fills                   */
+  int64_t req_tier[4];    /* required neurons by step tier                    */
+  int64_t req_bytes;      /* sum of record_bytes over required neurons: what
+                             the sparse FFN reads from the slots              */
 } m2c_stats;
 
 /* Bytes of one neuron record of `tier` (1..3) for d_model d, or -1. */

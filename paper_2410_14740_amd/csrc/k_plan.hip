@@ -253,6 +253,331 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
     atomicAdd(&st.stats[7], (unsigned long long)F1);
     atomicAdd(&st.stats[8], (unsigned long long)F2);
     atomicAdd(&st.stats[9], (unsigned long long)F3);
+    // required neurons by tier [10..12] = INT4, INT8, FP16
+    atomicAdd(&st.stats[10], (unsigned long long)N1);
+    atomicAdd(&st.stats[11], (unsigned long long)N2);
+    atomicAdd(&st.stats[12], (unsigned long long)N3);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// The same plan for d_ff <= 32768, built from coalesced sweeps: neuron i is
+// handled by thread i % 1024 in chunk i / 1024, so every sweep issues its
+// loads together, and each ordered list (R, NEW, fills, the three tiers of
+// the work list, untouched and touched slots) is a compaction whose
+// positions come from wave ballots plus one block scan over the per-(chunk,
+// wave) counts. A first read-only sweep classifies every neuron (hit codes
+// in LDS, touched slots in an LDS bitmap) and counts; nothing is written
+// before the required set is known to fit in the plan.
+constexpr int kPJ = 32;       // chunks of 1024 neurons (d_ff <= 32768)
+constexpr int kPGroup = 12;   // chunks whose loads are in flight together
+constexpr int kPWaves = kPlanThreads / 64;
+
+__device__ __forceinline__ unsigned long long pk3(uint32_t a, uint32_t b, uint32_t c) {
+  return (unsigned long long)a | ((unsigned long long)b << 21) | ((unsigned long long)c << 42);
+}
+__device__ __forceinline__ int fd3(unsigned long long v, int f) {
+  return (int)((v >> (21 * f)) & 0x1fffffu);
+}
+__device__ __forceinline__ int popc(unsigned long long v) { return __popcll(v); }
+
+// Exclusive prefix of s_v[0..n) (n <= kPlanThreads, one entry per thread), in
+// place; returns the total. Contains barriers.
+template <typename T>
+__device__ T scan_entries(T* s_v, int n, T* tmp) {
+  const int tid = threadIdx.x;
+  const T v = tid < n ? s_v[tid] : T(0);
+  T tot;
+  const T ex = block_exclusive_scan<T>(v, tmp, &tot);
+  if (tid < n) s_v[tid] = ex;
+  __syncthreads();
+  return tot;
+}
+
+// Step tier (max over rows, codes above FP16 read as FP16) and row mask of
+// neuron i.
+__device__ __forceinline__ void neuron_tiers(const uint8_t* __restrict__ tm, int d_ff, int i,
+                                             int B, int& t, uint32_t& m) {
+  t = 0;
+  m = 0;
+  if (B == 1) {
+    const int v = tm[i];
+    t = v;
+    m = v ? 1u : 0u;
+  } else {
+    for (int b0 = 0; b0 < B; b0 += 8) {
+      uint8_t v[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] = tm[(int64_t)min(b0 + q, B - 1) * d_ff + i];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (b0 + q < B) {
+          t = v[q] > t ? v[q] : t;
+          m |= v[q] ? 1u << (b0 + q) : 0u;
+        }
+      }
+    }
+  }
+  t = t > 3 ? 3 : t;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
+    const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step,
+    DeviceState st, PlanPtrs P) {
+  __shared__ uint8_t s_info[kPJ * kPlanThreads];  // tier | code << 2 (1 hit, 2 refill, 0 new)
+  __shared__ uint32_t s_touch[kPJ * kPlanThreads / 32];  // slots touched this step
+  __shared__ unsigned long long s_ca[kPJ * kPWaves];  // R, NEW, fills per (chunk, wave)
+  __shared__ unsigned long long s_cb[kPJ * kPWaves];  // FP16, INT8, INT4 per (chunk, wave)
+  __shared__ uint32_t s_cu[kPJ * kPWaves];            // slot compactions per (chunk, wave)
+  __shared__ unsigned long long scan64[kPWaves + 1];
+  __shared__ uint32_t scan32[kPWaves + 1];
+  __shared__ int sh_hit, sh_refill, sh_empty, sh_f[4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  const int NJ = (d_ff + kPlanThreads - 1) / kPlanThreads;
+  const int NC = (C + kPlanThreads - 1) / kPlanThreads;
+  if (tid == 0) {
+    sh_hit = sh_refill = sh_empty = 0;
+    sh_f[0] = sh_f[1] = sh_f[2] = sh_f[3] = 0;
+  }
+  for (int w = tid; w < (C + 31) / 32; w += kPlanThreads) s_touch[w] = 0;
+  __syncthreads();
+  // ---------------- A1: classify and count (reads only)
+  for (int j0 = 0; j0 < NJ; j0 += kPGroup) {
+    int t[kPGroup], sl[kPGroup];
+    uint32_t m[kPGroup];
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) {
+      const int i = min(tid + kPlanThreads * (j0 + g), d_ff - 1);
+      neuron_tiers(tier_map, d_ff, i, B, t[g], m[g]);
+      sl[g] = st.slot_of[i];
+    }
+    int old[kPGroup];
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) old[g] = sl[g] >= 0 ? st.slot_tier[sl[g]] : 0;
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) {
+      const int j = j0 + g, i = tid + kPlanThreads * j;
+      const bool valid = j < NJ && i < d_ff;
+      const bool req = valid && t[g] > 0;
+      const bool res = req && sl[g] >= 0;
+      const bool hit = res && old[g] == t[g];
+      if (valid) s_info[i] = req ? (uint8_t)(t[g] | ((hit ? 1 : res ? 2 : 0) << 2)) : 0;
+      if (res) atomicOr(&s_touch[sl[g] >> 5], 1u << (sl[g] & 31));
+      const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
+                               b2 = __ballot(req && !hit), b3 = __ballot(req && t[g] == 3),
+                               b4 = __ballot(req && t[g] == 2), b5 = __ballot(req && t[g] == 1),
+                               bh = __ballot(hit), br = __ballot(res && !hit);
+      if (lane == 0 && j < NJ) {
+        s_ca[j * kPWaves + wave] = pk3(popc(b0), popc(b1), popc(b2));
+        s_cb[j * kPWaves + wave] = pk3(popc(b3), popc(b4), popc(b5));
+        if (bh) atomicAdd(&sh_hit, popc(bh));
+        if (br) atomicAdd(&sh_refill, popc(br));
+      }
+    }
+  }
+  __syncthreads();
+  const unsigned long long totA = scan_entries<unsigned long long>(s_ca, NJ * kPWaves, scan64);
+  const unsigned long long totB = scan_entries<unsigned long long>(s_cb, NJ * kPWaves, scan64);
+  const int NREQ = fd3(totA, 0), NNEW = fd3(totA, 1), NF = fd3(totA, 2);
+  const int N3 = fd3(totB, 0), N2 = fd3(totB, 1), N1 = fd3(totB, 2);
+  if (NREQ > cap) {  // workgroup-uniform: an empty plan, the cache untouched
+    if (tid == 0) {
+      for (int q = 0; q < M2C_NCOUNTS; ++q) P.counts[q] = 0;
+      P.counts[M2C_NCOUNTS - 1] = NREQ;
+      atomicOr(st.status, M2C_STATUS_PLAN_OVERFLOW);
+    }
+    return;
+  }
+  // ---------------- A2: required list, NEW list, fill ids, work positions
+  for (int j0 = 0; j0 < NJ; j0 += kPGroup) {
+    int sl[kPGroup];
+    uint32_t m[kPGroup];
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) {
+      const int i = min(tid + kPlanThreads * (j0 + g), d_ff - 1);
+      int tt;
+      neuron_tiers(tier_map, d_ff, i, B, tt, m[g]);
+      sl[g] = st.slot_of[i];
+    }
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) {
+      const int j = j0 + g, i = tid + kPlanThreads * j;
+      const bool valid = j < NJ && i < d_ff;
+      const int info = valid ? s_info[i] : 0;
+      const int t = info & 3, code = info >> 2;
+      const bool req = t > 0, res = code != 0, hit = code == 1;
+      const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
+                               b2 = __ballot(req && !hit), b3 = __ballot(req && t == 3),
+                               b4 = __ballot(req && t == 2), b5 = __ballot(req && t == 1);
+      if (!req) continue;
+      const unsigned long long pa = s_ca[j * kPWaves + wave], pb = s_cb[j * kPWaves + wave];
+      const int pos = fd3(pa, 0) + popc(b0 & lt);
+      const int wp = t == 3 ? fd3(pb, 0) + popc(b3 & lt)
+                     : t == 2 ? N3 + fd3(pb, 1) + popc(b4 & lt)
+                              : N3 + N2 + fd3(pb, 2) + popc(b5 & lt);
+      P.req_ids[pos] = i;
+      P.req_tier[pos] = (uint8_t)t;
+      P.req_mask[pos] = m[g];
+      st.work_pos[pos] = wp;
+      if (res) {
+        P.req_slot[pos] = sl[g];
+        P.req_hit[pos] = hit ? 1 : 2;
+        st.slot_last[sl[g]] = step;
+        if (!hit) st.slot_tier[sl[g]] = (uint8_t)t;
+      } else {
+        st.new_pos[fd3(pa, 1) + popc(b1 & lt)] = pos;
+      }
+      if (!hit) {
+        const int fr = fd3(pa, 2) + popc(b2 & lt);
+        st.fill_pos[pos] = fr;
+        P.fill_ids[fr] = i;
+        P.fill_tier[fr] = (uint8_t)t;
+      } else {
+        st.fill_pos[pos] = -1;
+      }
+    }
+  }
+  // ---------------- C: victims = untouched slots in LRU order
+  const int cur = *st.lru_cur;
+  const int32_t* lru_in = st.lru + (int64_t)cur * C;
+  int32_t* lru_out = st.lru + (int64_t)(1 - cur) * C;
+  for (int j0 = 0; j0 < NC; j0 += kPGroup) {
+    int sv[kPGroup];
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) sv[g] = lru_in[min(tid + kPlanThreads * (j0 + g), C - 1)];
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) {
+      const int j = j0 + g;
+      const bool valid = j < NC && tid + kPlanThreads * j < C;
+      const bool unt = valid && !((s_touch[sv[g] >> 5] >> (sv[g] & 31)) & 1u);
+      const unsigned long long bu = __ballot(unt);
+      if (lane == 0 && j < NC) s_cu[j * kPWaves + wave] = (uint32_t)popc(bu);
+    }
+  }
+  __syncthreads();
+  const int NUNT = (int)scan_entries<uint32_t>(s_cu, NC * kPWaves, scan32);
+  const int NV = NNEW < NUNT ? NNEW : NUNT;
+  {
+    int empties = 0;
+    for (int j0 = 0; j0 < NC; j0 += kPGroup) {
+      int sv[kPGroup];
+#pragma unroll
+      for (int g = 0; g < kPGroup; ++g) sv[g] = lru_in[min(tid + kPlanThreads * (j0 + g), C - 1)];
+#pragma unroll
+      for (int g = 0; g < kPGroup; ++g) {
+        const int j = j0 + g;
+        const bool valid = j < NC && tid + kPlanThreads * j < C;
+        // only this thread looks at slot sv[g]'s bit, so marking victims below
+        // does not disturb the test
+        const bool unt = valid && !((s_touch[sv[g] >> 5] >> (sv[g] & 31)) & 1u);
+        const unsigned long long bu = __ballot(unt);
+        if (!unt) continue;
+        const int u = (int)s_cu[j * kPWaves + wave] + popc(bu & lt);
+        if (u < NV) {
+          const int s = sv[g];
+          const int old = st.slot_key[s];
+          st.vict_slot[u] = s;
+          st.vict_old[u] = old;
+          empties += old < 0;
+          st.slot_last[s] = step;
+          atomicOr(&s_touch[s >> 5], 1u << (s & 31));
+        } else {
+          lru_out[u - NV] = sv[g];
+        }
+      }
+    }
+    if (empties) atomicAdd(&sh_empty, empties);
+  }
+  __syncthreads();
+  const int NEMPTY = sh_empty;
+  // ---------------- C2: NEW neurons take their victims or a staging slot
+  for (int j = tid; j < NNEW; j += kPlanThreads) {
+    const int pos = st.new_pos[j];
+    const int i = P.req_ids[pos];
+    if (j < NV) {
+      const int s = st.vict_slot[j];
+      const int old = st.vict_old[j];
+      if (old >= 0) {
+        st.slot_of[old] = -1;
+        P.evicted_ids[j - NEMPTY] = old;
+      }
+      st.slot_of[i] = s;
+      st.slot_key[s] = i;
+      st.slot_tier[s] = P.req_tier[pos];
+      P.req_slot[pos] = s;
+      P.req_hit[pos] = 0;
+    } else {
+      P.req_slot[pos] = C + (j - NV);
+      P.req_hit[pos] = 3;
+    }
+  }
+  __syncthreads();
+  // ---------------- D: touched slots go to the end of the order, by slot id
+  for (int j0 = 0; j0 < NC; j0 += kPGroup) {
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) {
+      const int j = j0 + g, s = tid + kPlanThreads * j;
+      const bool tch = j < NC && s < C && ((s_touch[s >> 5] >> (s & 31)) & 1u);
+      const unsigned long long bt = __ballot(tch);
+      if (lane == 0 && j < NC) s_cu[j * kPWaves + wave] = (uint32_t)popc(bt);
+    }
+  }
+  __syncthreads();
+  scan_entries<uint32_t>(s_cu, NC * kPWaves, scan32);
+  for (int j0 = 0; j0 < NC; j0 += kPGroup) {
+#pragma unroll
+    for (int g = 0; g < kPGroup; ++g) {
+      const int j = j0 + g, s = tid + kPlanThreads * j;
+      const bool tch = j < NC && s < C && ((s_touch[s >> 5] >> (s & 31)) & 1u);
+      const unsigned long long bt = __ballot(tch);
+      if (tch) lru_out[NUNT - NV + (int)s_cu[j * kPWaves + wave] + popc(bt & lt)] = s;
+    }
+  }
+  // ---------------- E: work list and fill slots
+  for (int q = tid; q < NREQ; q += kPlanThreads) {
+    const int ws = P.req_slot[q];
+    const int wp = st.work_pos[q];
+    P.work_slot[wp] = ws;
+    P.work_mask[wp] = P.req_mask[q];
+    const int fp = st.fill_pos[q];
+    if (fp >= 0) {
+      P.fill_slot[fp] = ws;
+      atomicAdd(&sh_f[P.req_tier[q]], 1);
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const int F3 = sh_f[3], F2 = sh_f[2], F1 = sh_f[1];
+    int32_t c[M2C_NCOUNTS] = {0};
+    c[M2C_CNT_REQ] = NREQ;
+    c[M2C_CNT_HIT] = sh_hit;
+    c[M2C_CNT_REFILL] = sh_refill;
+    c[M2C_CNT_NEW] = NV;
+    c[M2C_CNT_BYPASS] = NNEW - NV;
+    c[M2C_CNT_EVICT] = NV - NEMPTY;
+    c[M2C_CNT_FILL] = NF;
+    c[M2C_CNT_REQ_FP16] = N3;
+    c[M2C_CNT_REQ_INT8] = N2;
+    c[M2C_CNT_REQ_INT4] = N1;
+    c[M2C_CNT_FILL_FP16] = F3;
+    c[M2C_CNT_FILL_INT8] = F2;
+    c[M2C_CNT_FILL_INT4] = F1;
+    for (int q = 0; q < M2C_NCOUNTS; ++q) P.counts[q] = c[q];
+    *st.lru_cur = 1 - cur;
+    atomicAdd(&st.stats[0], 1ull);
+    atomicAdd(&st.stats[1], (unsigned long long)NREQ);
+    atomicAdd(&st.stats[2], (unsigned long long)sh_hit);
+    atomicAdd(&st.stats[3], (unsigned long long)sh_refill);
+    atomicAdd(&st.stats[4], (unsigned long long)NV);
+    atomicAdd(&st.stats[5], (unsigned long long)(NNEW - NV));
+    atomicAdd(&st.stats[6], (unsigned long long)(NV - NEMPTY));
+    atomicAdd(&st.stats[7], (unsigned long long)F1);
+    atomicAdd(&st.stats[8], (unsigned long long)F2);
+    atomicAdd(&st.stats[9], (unsigned long long)F3);
+    atomicAdd(&st.stats[10], (unsigned long long)N1);
+    atomicAdd(&st.stats[11], (unsigned long long)N2);
+    atomicAdd(&st.stats[12], (unsigned long long)N3);
   }
 }
 
@@ -287,8 +612,12 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
   P.evicted_ids = reinterpret_cast<int32_t*>(plan + lay.evicted_ids);
   P.work_slot = reinterpret_cast<int32_t*>(plan + lay.work_slot);
   P.work_mask = reinterpret_cast<uint32_t*>(plan + lay.work_mask);
-  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
-                     L->desc.d_ff, L->desc.cache_slots, L->cap, step, L->st, P);
+  if (L->desc.d_ff <= kPJ * kPlanThreads)
+    hipLaunchKernelGGL(plan_fast_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
+                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, L->st, P);
+  else
+    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
+                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, L->st, P);
   return hipGetLastError();
 }
 

@@ -29,30 +29,43 @@ __device__ __forceinline__ void unpack8(const uint4 v, float* f) {
 }
 
 // z[b][j] for rows b < nb (x, z already offset to the first row of the pass).
+// A lane's partial takes chunks sl, sl + L, ... of its row: all of them are
+// loaded before the first fmaf (NCH >= chunks / L per lane), x of the pass
+// is staged in LDS, and the fmaf chain then runs in the canonical order, so
+// the wave costs one memory round trip instead of one per chunk.
+template <int NCH>
 __global__ __launch_bounds__(256) void pred_z_kernel(const uint16_t* __restrict__ A,
                                                      const uint16_t* __restrict__ x, int d, int r,
                                                      int nb, int L, float* __restrict__ z) {
+  extern __shared__ uint4 xs[];  // [nb][d / 8]
   const int lane = threadIdx.x & 63;
   // wave index as a scalar: loops and shuffles below stay wave-uniform
   const int gw = __builtin_amdgcn_readfirstlane((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
   const int sl = lane & (L - 1);
   const int j = gw * (64 / L) + lane / L;
   const bool valid = j < r;
+  const int chunks = d >> 3;
+  const uint4* arow = reinterpret_cast<const uint4*>(A + (int64_t)(valid ? j : 0) * d);
+  uint4 av[NCH];
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) av[q] = arow[min(sl + q * L, chunks - 1)];
+  for (int c = threadIdx.x; c < nb * chunks; c += blockDim.x)
+    xs[c] = reinterpret_cast<const uint4*>(x)[c];
+  __syncthreads();
   float acc[kPredBatch];
 #pragma unroll
   for (int b = 0; b < kPredBatch; ++b) acc[b] = 0.0f;
-  if (valid) {
-    const uint4* arow = reinterpret_cast<const uint4*>(A + (int64_t)j * d);
-    const int chunks = d >> 3;
-#pragma unroll 2
-    for (int c = sl; c < chunks; c += L) {
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) {
+    const int c = sl + q * L;
+    if (c < chunks) {
       float af[8];
-      unpack8(arow[c], af);
+      unpack8(av[q], af);
 #pragma unroll
       for (int b = 0; b < kPredBatch; ++b) {
         if (b < nb) {
           float xf[8];
-          unpack8(reinterpret_cast<const uint4*>(x + (int64_t)b * d)[c], xf);
+          unpack8(xs[b * chunks + c], xf);
 #pragma unroll
           for (int e = 0; e < 8; ++e) acc[b] = __builtin_fmaf(af[e], xf[e], acc[b]);
         }
@@ -123,26 +136,51 @@ __global__ __launch_bounds__(256) void pred_s_kernel(const uint16_t* __restrict_
   }
 }
 
+template <int NCH>
+static void launch_z(int blocks, size_t lds, hipStream_t stream, const uint16_t* A,
+                     const uint16_t* x, int d, int r, int nb, int L, float* z) {
+  hipLaunchKernelGGL(pred_z_kernel<NCH>, dim3(blocks), dim3(256), lds, stream, A, x, d, r, nb, L,
+                     z);
+}
+
 hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, float* scores,
                           hipStream_t stream) {
   const int d = L->desc.d_model, r = L->desc.pred_rank, d_ff = L->desc.d_ff;
   const int Lz = canon_lanes(d), Ls = canon_lanes(r);
-  for (int b0 = 0; b0 < batch; b0 += kPredBatch) {
-    const int nb = batch - b0 < kPredBatch ? batch - b0 : kPredBatch;
+  const int nch = ((d >> 3) + Lz - 1) / Lz;  // chunks per lane of the z kernel
+  // rows per pass: at most kPredBatch, and x of the pass within 64 KB of LDS
+  int per_pass = 32768 / d;
+  if (per_pass > kPredBatch) per_pass = kPredBatch;
+  if (per_pass < 1) per_pass = 1;
+  for (int b0 = 0; b0 < batch; b0 += per_pass) {
+    const int nb = batch - b0 < per_pass ? batch - b0 : per_pass;
     const int rows_z = 64 / Lz;
     const int waves_z = (r + rows_z - 1) / rows_z;
-    hipLaunchKernelGGL(pred_z_kernel, dim3((waves_z + 3) / 4), dim3(256), 0, stream, L->pred_a,
-                       x + (int64_t)b0 * d, d, r, nb, Lz, L->z + (int64_t)b0 * r);
+    const int bz = (waves_z + 3) / 4;
+    const size_t lz = (size_t)nb * d * 2;
+    const uint16_t* xb = x + (int64_t)b0 * d;
+    float* zb = L->z + (int64_t)b0 * r;
+    if (nch <= 1)
+      launch_z<1>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
+    else if (nch <= 2)
+      launch_z<2>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
+    else if (nch <= 4)
+      launch_z<4>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
+    else if (nch <= 8)
+      launch_z<8>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
+    else if (nch <= 16)
+      launch_z<16>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
+    else
+      launch_z<32>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    // one row group per wave: every wave makes a single pass
     const int rows_s = 64 / Ls;
-    int waves_s = (d_ff + rows_s - 1) / rows_s;
-    int blocks = (waves_s + 3) / 4;
-    const int cap = 8 * L->num_cus;
-    if (blocks > cap) blocks = cap;
+    const int waves_s = (d_ff + rows_s - 1) / rows_s;
+    const int blocks = (waves_s + 3) / 4;
     hipLaunchKernelGGL(pred_s_kernel, dim3(blocks), dim3(256), (size_t)nb * r * sizeof(float),
-                       stream, L->pred_b, L->z + (int64_t)b0 * r, L->bias, d_ff, r, nb, Ls,
-                       (int64_t)d_ff, scores + (int64_t)b0 * d_ff);
+                       stream, L->pred_b, zb, L->bias, d_ff, r, nb, Ls, (int64_t)d_ff,
+                       scores + (int64_t)b0 * d_ff);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -170,7 +170,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_pred_a; void* p_pred_b; void* p_bias; void* p_z; void* p_scores; void* p_slots;
   void* p_h; void* p_ypart; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
-  void* p_vslot; void* p_vold; void* p_stats; void* p_status;
+  void* p_vslot; void* p_vold; void* p_fill_pos; void* p_stats; void* p_status;
   Piece pieces[] = {
       // C resident + S staging slots, then one slot that stays zero: padding
       // lanes of the FFN kernels read it instead of branching around loads
@@ -192,6 +192,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_work_pos, cap * 4},
       {&p_vslot, cap * 4},
       {&p_vold, cap * 4},
+      {&p_fill_pos, cap * 4},
       {&p_stats, 16 * 8},
       {&p_status, 4},
   };
@@ -225,6 +226,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.work_pos = (int32_t*)p_work_pos;
   L->st.vict_slot = (int32_t*)p_vslot;
   L->st.vict_old = (int32_t*)p_vold;
+  L->st.fill_pos = (int32_t*)p_fill_pos;
   L->st.stats = (unsigned long long*)p_stats;
   L->st.status = (int32_t*)p_status;
   L->info.device_bytes = total;
@@ -511,7 +513,13 @@ m2c_status m2c_layer_stats(const m2c_layer* L, m2c_stats* out) {
   out->fill[1] = st[7];
   out->fill[2] = st[8];
   out->fill[3] = st[9];
-  for (int t = 1; t <= 3; ++t) out->fill_bytes += out->fill[t] * L->info.record_bytes[t];
+  out->req_tier[1] = st[10];
+  out->req_tier[2] = st[11];
+  out->req_tier[3] = st[12];
+  for (int t = 1; t <= 3; ++t) {
+    out->fill_bytes += out->fill[t] * L->info.record_bytes[t];
+    out->req_bytes += out->req_tier[t] * L->info.record_bytes[t];
+  }
   return M2C_OK;
 }
 

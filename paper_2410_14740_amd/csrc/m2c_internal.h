@@ -40,6 +40,7 @@ struct DeviceState {
   int32_t* work_pos = nullptr;   // [cap] plan scratch: work position of req p
   int32_t* vict_slot = nullptr;  // [cap] plan scratch
   int32_t* vict_old = nullptr;   // [cap] plan scratch
+  int32_t* fill_pos = nullptr;   // [cap] plan scratch: fill position of req p (-1 for hits)
   unsigned long long* stats = nullptr;  // [16] cumulative counters
   int32_t* status = nullptr;           // [1] M2C_STATUS_* bits set by kernels
 };

@@ -64,7 +64,8 @@ class Stats(ctypes.Structure):
     _fields_ = [("plans", ctypes.c_int64), ("req", ctypes.c_int64), ("hit", ctypes.c_int64),
                 ("refill", ctypes.c_int64), ("new_", ctypes.c_int64), ("bypass", ctypes.c_int64),
                 ("evict", ctypes.c_int64), ("fill", ctypes.c_int64 * 4),
-                ("fill_bytes", ctypes.c_int64)]
+                ("fill_bytes", ctypes.c_int64), ("req_tier", ctypes.c_int64 * 4),
+                ("req_bytes", ctypes.c_int64)]
 
 
 _lib = None
@@ -77,6 +78,10 @@ def load(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise ImportError(f"{path} is not built; run `python -m paper_2410_14740_amd.build`")
+    # torch wheels bundle their own HIP runtime; load it first so that the
+    # library binds to the same runtime instance as the device memory and
+    # streams torch hands it (two runtimes in one process do not share them)
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P, I32, I64, S = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     sig = {

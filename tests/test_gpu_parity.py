@@ -132,6 +132,7 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flag
     assert (st.plans, st.req, st.hit, st.refill, st.new_, st.bypass, st.evict) == (
         steps, stats[0], stats[1], stats[2], stats[3], stats[4], stats[5])
     assert (st.fill[3], st.fill[2], st.fill[1]) == (stats[10], stats[11], stats[12])
+    assert (st.req_tier[3], st.req_tier[2], st.req_tier[1]) == (stats[7], stats[8], stats[9])
     L.close()
     return worst
 
