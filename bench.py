@@ -446,7 +446,7 @@ def main():
     ffn_traffic = None if args.deterministic_ffn else rocprof_summary.read_ffn_traffic(
         os.path.join(ROOT, "profiles", f"sparse_ffn_{wl.name}_layer.md"))
     ffn_kind = ("three kernels (up, down, ordered reduce), deterministic" if args.deterministic_ffn
-                else "two kernels (h, down by column slice)")
+                else "one launch (h tasks, then down tasks that wait on the h words)")
     out = {
         "metric": METRIC,
         "value": tokens_per_s,
@@ -478,11 +478,11 @@ def main():
             "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
                       "bypass_rate": bypass / max(reqs, 1)},
         },
-        # the step's gather-GEMV (m2c_sparse_ffn: ffn_h_kernel + ffn_dn_kernel),
+        # the step's gather-GEMV (m2c_sparse_ffn: ffn_fused_kernel),
         # algorithmic bytes per call over the per-call time of back-to-back calls
         "roofline": {"bound": "hbm", "achieved": iso["achieved_GBps"], "peak": PEAK_HBM_GBPS,
                      "unit": "GB/s", "frac": iso["achieved_GBps"] / PEAK_HBM_GBPS,
-                     "traffic": ffn_traffic, "kernel": "m2c_sparse_ffn (ffn_h_kernel + ffn_dn_kernel)",
+                     "traffic": ffn_traffic, "kernel": "m2c_sparse_ffn (ffn_fused_kernel)",
                      "workload": f"{wl.name} layer shape, {args.ffn_layers} layers cycled",
                      "bytes_per_launch": iso["bytes_per_launch"], "us_per_launch": iso["us_avg"]},
         "roofline_target_layer": None if target is None else {

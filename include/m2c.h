@@ -279,7 +279,10 @@ m2c_status m2c_layer_reset_cache(m2c_layer* layer, void* stream);
  * M2C_ERR_CAPACITY (and clears the condition) if a cache plan since the last
  * call received a tier map with more active neurons than the layer's plan
  * capacity, min(d_ff, max_batch * k_max): such a plan is left empty and the
- * cache unchanged. */
+ * cache unchanged. Returns M2C_ERR_STATE (and clears the condition) if a
+ * batch-1 sparse FFN gave up waiting for one of its own h values (its
+ * workgroups could not all run, for instance because another kernel held the
+ * GPU for a long time); that call's output is wrong. */
 m2c_status m2c_layer_stats(const m2c_layer* layer, m2c_stats* out);
 
 /* Test support. Copies one record of the host store (no device work). */

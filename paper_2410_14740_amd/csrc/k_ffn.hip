@@ -394,7 +394,9 @@ __global__ __launch_bounds__(256) void ffn_reduce_kernel(const float* __restrict
 hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
                       hipStream_t stream) {
   if (batch > 1) return launch_ffn_batch(L, x, batch, plan, y, stream);
-  if (!(L->desc.flags & M2C_FLAG_DETERMINISTIC_FFN)) return launch_ffn_split(L, x, plan, y, stream);
+  if (!(L->desc.flags & M2C_FLAG_DETERMINISTIC_FFN))
+    return ffn_fused_supported(L) ? launch_ffn_fused(L, x, plan, y, stream)
+                                                : launch_ffn_split(L, x, plan, y, stream);
   const int d = L->desc.d_model;
   const m2c_plan_layout& lay = L->layout;
   const int32_t* counts = reinterpret_cast<const int32_t*>(plan + lay.counts);

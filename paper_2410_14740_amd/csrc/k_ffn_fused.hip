@@ -1,0 +1,578 @@
+// Sparse mixed-precision SwiGLU FFN for one token in one launch (Sec. 1 and
+// Sec. 5.2: only the active neurons are computed, each at its precision).
+//
+//   y += sum_i silu(<g_i, x>) * <u_i, x> * d_i
+//
+// The work is a list of equal-sized tasks, one per workgroup (8 sixteen-byte
+// loads per lane of a 512-thread workgroup, all issued at once):
+//
+//   h tasks     gate/up dot products of a few neurons of one tier ("units" of
+//               d bytes, one or more per wave), h_i = silu(a_i) * b_i, each
+//               published as one 64-bit word (call tag, h_i).
+//   down tasks  a 512-column slice of y over a run of neurons of one tier:
+//               a lane owns 32 columns of one neuron per round; lanes 16 and
+//               32 apart share columns and are folded by lane swaps, the
+//               waves through LDS, and one fp32 atomic add per column adds
+//               the run into y.
+//
+// Launch order (= workgroup id): h INT4, h INT8, h FP16, down INT4, down
+// INT8, down FP16. A down workgroup issues its loads first and then polls the
+// h words of its run, which come from workgroups of lower id; on each XCD
+// workgroups are dispatched in id order and an h workgroup waits for
+// nothing, so every producer runs. The hardware dispatcher replaces each
+// finished workgroup at once, so the down loads stream behind the gate/up
+// loads without a second launch. The poll is bounded anyway: past the limit
+// it sets the layer's status word and takes h = 0. At most 80 VGPRs keep
+// three workgroups on a CU, so enough loads are in flight and the
+// dequantization of one workgroup overlaps the loads of the others.
+//
+// Call tag: the grid has a fixed size per layer (the most tasks a plan of
+// the layer can need; workgroups past the plan's tasks exit), and workgroup
+// b adds 1 to its own 64-bit counter gen[b] on every call, so all of them
+// read the same count E and tag the call E + 1 without a host argument (the
+// launch can be captured in a graph and replayed) and without two
+// workgroups touching one counter. A word is written and read with single
+// agent-scope atomic accesses, so no fence is needed and no word of an
+// earlier call is ever taken.
+//
+// Dequantization is exact and cheap: INT8 / INT4 codes are shifted to
+// offset binary (q + 128, q + 8) and placed, by byte permutes or masks, into
+// fp16 lanes as denormals n * 2^-24, which v_fma_mix_f32 multiplies exactly
+// (by an fp16 x element or an fp32 coefficient) and adds with one rounding.
+// The offset comes back out as 128 (or 8) times the sum of x over the chunk
+// (h tasks, sums staged in LDS once) or times the sum of the neuron
+// coefficients (down tasks), and 2^24 is folded into the scale. (The dot2
+// instruction is not used on the offset codes: it does not round its sum to
+// nearest, and the offset would magnify its error.)
+//
+// Padding lanes and invalid slots read slot n_slots, which is all zeros, so
+// no load sits under a per-lane branch; every task kind issues the same
+// number of loads, so the compiler's wait counts do not depend on the kind.
+#include "ffn_device.h"
+
+namespace m2c {
+
+namespace {
+
+constexpr int kFT = 512;                 // threads per workgroup
+constexpr int kFWaves = kFT / 64;
+constexpr int kFL = 8;                   // 16-byte data loads per lane and task
+constexpr int kFSW = 512;                // down tasks: output columns per slice
+constexpr int kFLPN = kFSW / 32;         // lanes per neuron row of a slice
+constexpr int kFNPR = kFT / kFLPN;       // neurons per round of a down task
+constexpr int kFMaxItems = kFL * kFNPR;  // most work items of one task (INT4 down)
+constexpr int kFSpin = 1 << 16;          // polls of one h word before giving up
+constexpr float kTwo24 = 16777216.0f;
+static_assert(kFMaxItems <= kFT, "one slot id / h word per thread");
+static_assert(kFLPN == 16, "the fold pairs lanes 16 and 32 apart");
+
+struct FMap {
+  int n3, n2, n1;  // work items by tier
+  int w1, w2, w3;  // h tasks by tier (INT4, INT8, FP16)
+  int n_slices;
+  int e[6];        // ends of the six task regions in launch order
+};
+
+struct FTask {
+  int kind;  // 0 none, 1 h, 2 down
+  int tier;
+  int lo, hi;
+  int slice;
+};
+
+struct FBuf {
+  uint4 v[kFL];
+  uint32_t s[kFL];
+};
+
+// K: 16-byte loads per lane and unit (a unit is d bytes of a neuron's gate and
+// up rows); a wave takes kFL / K units of an h task.
+// Launch order of the six task regions: (kind, tier) per region.
+constexpr int kOrderKind[6] = {1, 1, 1, 2, 2, 2};
+constexpr int kOrderTier[6] = {1, 2, 3, 1, 2, 3};
+
+template <int K>
+__device__ __forceinline__ FMap make_map(const int32_t* counts, int cap, int d) {
+  constexpr int U = kFWaves * (kFL / K);  // units per h task
+  FMap m;
+  work_counts(counts, cap, m.n3, m.n2, m.n1);
+  m.w1 = (m.n1 + U - 1) / U;
+  m.w2 = (m.n2 + U / 2 - 1) / (U / 2);
+  m.w3 = (m.n3 + U / 4 - 1) / (U / 4);
+  m.n_slices = (d + kFSW - 1) / kFSW;
+  const int u1 = (m.n1 + 8 * kFNPR - 1) / (8 * kFNPR);
+  const int u2 = (m.n2 + 4 * kFNPR - 1) / (4 * kFNPR);
+  const int u3 = (m.n3 + 2 * kFNPR - 1) / (2 * kFNPR);
+  int end = 0;
+#pragma unroll
+  for (int r = 0; r < 6; ++r) {
+    const int tr = kOrderTier[r];
+    end += kOrderKind[r] == 1 ? (tr == 1 ? m.w1 : tr == 2 ? m.w2 : m.w3)
+                              : (tr == 1 ? u1 : tr == 2 ? u2 : u3) * m.n_slices;
+    m.e[r] = end;
+  }
+  return m;
+}
+
+// Task t in launch order. Work items are tier-major in the plan: FP16, INT8,
+// INT4.
+template <int K>
+__device__ __forceinline__ FTask decode(const FMap& m, int t) {
+  constexpr int U = kFWaves * (kFL / K);
+  FTask k;
+  k.kind = 0;
+  k.tier = 1;
+  k.lo = k.hi = 0;
+  k.slice = 0;
+  // region by comparisons (no indexed array: it would live in scratch memory)
+  int kind = 0, tier = 1, start = 0;
+#pragma unroll
+  for (int r = 5; r >= 0; --r) {
+    const int lo_r = r ? m.e[r - 1] : 0;
+    if (t >= lo_r && t < m.e[r]) {
+      kind = kOrderKind[r];
+      tier = kOrderTier[r];
+      start = lo_r;
+    }
+  }
+  if (kind == 0) return k;
+  const int q = t - start;
+  k.tier = tier;
+  // by value (a select between fields would index a stack copy of the map)
+  const int i1 = tier == 1, i2 = tier == 2, i3 = tier == 3;
+  const int base = i1 * (m.n3 + m.n2) + i2 * m.n3;
+  const int n = i1 * m.n1 + i2 * m.n2 + i3 * m.n3;
+  if (kind == 1) {
+    k.kind = 1;
+    const int per = tier == 1 ? U : tier == 2 ? U / 2 : U / 4;
+    k.lo = base + per * q;
+    k.hi = base + min(per * (q + 1), n);
+  } else {
+    k.kind = 2;
+    const int per = (tier == 1 ? 8 : tier == 2 ? 4 : 2) * kFNPR;
+    const int run = q / m.n_slices;
+    k.slice = q - run * m.n_slices;
+    k.lo = base + per * run;
+    k.hi = base + min(per * (run + 1), n);
+  }
+  return k;
+}
+
+__device__ __forceinline__ uint4 ld16(const uint8_t* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+__device__ __forceinline__ uint32_t ld2(const uint8_t* p) {
+  return *reinterpret_cast<const uint16_t*>(p);
+}
+__device__ __forceinline__ float lo_f(uint32_t p) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(p & 0xffffu));
+}
+__device__ __forceinline__ float hi_f(uint32_t p) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)(p >> 16));
+}
+
+// Issue every load of task k into b: kFL data loads and kFL scale loads per
+// lane, whatever the kind. ss: the task's slot ids (n_slots past its items).
+template <int K>
+__device__ __forceinline__ void issue(const FTask& k, const int* ss, int d,
+                                      const uint8_t* __restrict__ slots, uint32_t sb,
+                                      int n_slots, int tid, FBuf& b) {
+  // byte offsets into the slot arena (below 4 GiB: checked at launch), so
+  // every address is the arena base plus one 32-bit register
+  const uint32_t zero = (uint32_t)n_slots * sb;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const uint32_t ud = (uint32_t)d;
+  const uint32_t G = ud >> 7;
+  if (k.kind == 2) {
+    const int r = tid / kFLPN;
+    const uint32_t col = (uint32_t)(k.slice * kFSW + 32 * (tid % kFLPN));
+    const bool colok = col < ud;
+    const int lnv = k.tier == 3 ? 2 : k.tier == 2 ? 1 : 0;  // log2 loads per neuron and round
+    const uint32_t dbase = k.tier == 3 ? 4 * ud + 2 * col : k.tier == 2 ? 2 * ud + col
+                                                                        : ud + (col >> 1);
+    const uint32_t sbase = (k.tier == 1 ? 3 * (ud >> 1) : 3 * ud) + 4 * G + 2 * (col >> 7);
+#pragma unroll
+    for (int j = 0; j < kFL; ++j) {
+      const int q = j >> lnv, e = j & ((1 << lnv) - 1);
+      const uint32_t rec = (uint32_t)ss[q * kFNPR + r] * sb;
+      // the scale of an FP16 record (it has none) is read from the zero slot,
+      // never from the data's own address: every load stays independent
+      const uint32_t dp = colok ? rec + dbase + 16 * e : zero;
+      const uint32_t sp = colok && k.tier != 3 ? rec + sbase : zero;
+      b.v[j] = ld16(slots + dp);
+      b.s[j] = ld2(slots + sp);
+    }
+  } else {
+    // h task (or nothing: kind 0 reads the zero slot with the same pattern)
+    constexpr int UW = kFL / K;
+    const int upi = k.tier == 3 ? 4 : k.tier == 2 ? 2 : 1;  // units per neuron
+    const int ncu = d >> 5;  // 16-byte chunks of each row in a unit
+    const uint32_t row = k.tier == 3 ? 2 * ud : k.tier == 2 ? ud : (ud >> 1);
+    const uint32_t sbase = k.tier == 1 ? 3 * (ud >> 1) : 3 * ud;
+#pragma unroll
+    for (int j = 0; j < kFL; ++j) {
+      const int u = w * UW + j / K;
+      const int item = u / upi, part = u - item * upi;
+      const uint32_t rec = (uint32_t)ss[item] * sb;  // zero slot past the task (and kind 0)
+      int q = lane + 64 * (j % K);
+      const bool in = q < 2 * ncu;
+      q = in ? q : 2 * ncu - 1;
+      const bool up = q >= ncu;
+      const uint32_t c = (uint32_t)(part * ncu + (up ? q - ncu : q));
+      const uint32_t g = k.tier == 2 ? (c >> 3) : (c >> 2);
+      const uint32_t dp = in ? rec + (up ? row : 0) + 16 * c : zero;
+      const uint32_t sp = in && k.tier != 3 ? rec + sbase + 2 * ((up ? G : 0) + g) : zero;
+      b.v[j] = ld16(slots + dp);
+      b.s[j] = ld2(slots + sp);
+    }
+  }
+}
+
+// Gate / up partial dot products of an h task; per unit (a, b) into s_ab.
+template <int K>
+__device__ __forceinline__ void compute_h(const FTask& k, const FBuf& b, int d,
+                                          const uint4* xs, const float* nx16, const float* nx32,
+                                          int tid, float2* s_ab) {
+  constexpr int UW = kFL / K;
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int upi = k.tier == 3 ? 4 : k.tier == 2 ? 2 : 1;
+  const int ncu = d >> 5;
+  float a[UW], bb[UW];
+#pragma unroll
+  for (int uw = 0; uw < UW; ++uw) a[uw] = bb[uw] = 0.0f;
+#pragma unroll
+  for (int j = 0; j < kFL; ++j) {
+    const int uw = j / K;
+    const int u = w * UW + uw;
+    const int part = u % upi;
+    int q = lane + 64 * (j % K);
+    q = q < 2 * ncu ? q : 2 * ncu - 1;
+    const bool up = q >= ncu;
+    const int c = part * ncu + (up ? q - ncu : q);
+    float p;
+    if (k.tier == 3) {
+      // + 0 * (scale read from the zero slot): keeps that load unconditional
+      p = fmaf(0.0f, h2f((uint16_t)b.s[j]), dot8_f16(b.v[j], xs[c], 0.0f));
+    } else if (k.tier == 2) {
+      const uint4 x0 = xs[2 * c], x1 = xs[2 * c + 1];
+      const uint32_t wv[4] = {b.v[j].x, b.v[j].y, b.v[j].z, b.v[j].w};
+      const uint32_t xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      float t = 0.0f;
+#pragma unroll
+      for (int u4 = 0; u4 < 4; ++u4) {
+        const uint32_t ob = wv[u4] ^ 0x80808080u;  // q + 128
+        const uint32_t l = __builtin_amdgcn_perm(0u, ob, 0x0c010c00u);
+        const uint32_t h = __builtin_amdgcn_perm(0u, ob, 0x0c030c02u);
+        t = fmaf(lo_f(l), lo_f(xv[2 * u4]), t);
+        t = fmaf(hi_f(l), hi_f(xv[2 * u4]), t);
+        t = fmaf(lo_f(h), lo_f(xv[2 * u4 + 1]), t);
+        t = fmaf(hi_f(h), hi_f(xv[2 * u4 + 1]), t);
+      }
+      p = h2f((uint16_t)b.s[j]) * fmaf(t, kTwo24, nx16[c]);
+    } else {
+      const uint32_t wv[4] = {b.v[j].x, b.v[j].y, b.v[j].z, b.v[j].w};
+      float t = 0.0f;
+#pragma unroll
+      for (int u4 = 0; u4 < 4; ++u4) {
+        const uint4 xq = xs[4 * c + u4];  // x[8 u4 .. 8 u4 + 7] of the chunk, in pairs
+        const uint32_t xw[4] = {xq.x, xq.y, xq.z, xq.w};
+        const uint32_t ob = wv[u4] ^ 0x88888888u;  // q + 8
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+          // nibbles s4 and s4 + 4 of the word go with x elements s4 and s4 + 4
+          const uint32_t p = (ob >> (4 * s4)) & 0x000f000fu;
+          const uint32_t xa = xw[s4 >> 1], xb = xw[2 + (s4 >> 1)];
+          t = fmaf(lo_f(p), (s4 & 1) ? hi_f(xa) : lo_f(xa), t);
+          t = fmaf(hi_f(p), (s4 & 1) ? hi_f(xb) : lo_f(xb), t);
+        }
+      }
+      p = h2f((uint16_t)b.s[j]) * fmaf(t, kTwo24, nx32[c]);
+    }
+    // lanes past the unit read the zero slot: data 0 (FP16) or scale 0
+    a[uw] += up ? 0.0f : p;
+    bb[uw] += up ? p : 0.0f;
+    // one chunk at a time: keeps the x reads of later chunks from being
+    // hoisted into registers all at once
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int uw = 0; uw < UW; ++uw) {
+    const float sa = wave_sum(a[uw]), sbv = wave_sum(bb[uw]);
+    if (lane == 0) s_ab[w * UW + uw] = make_float2(sa, sbv);
+  }
+}
+
+// Down projection of a down task: columns 16 * HALF .. 16 * HALF + 15 of the
+// lane's 32, for every neuron of the task (the two halves share the loaded
+// data and keep only 16 accumulators live). csum: sum of the lane's
+// coefficients, for the offset of INT8 / INT4 codes.
+template <int HALF>
+__device__ __forceinline__ void compute_dn_half(const FTask& k, const FBuf& b, const float* s_h,
+                                                int tid, float (&acc)[16]) {
+  const int r = tid / kFLPN;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+  if (k.tier == 3) {
+    // 4 loads per neuron and round, 8 columns each: this half is loads 2H, 2H+1
+#pragma unroll
+    for (int q = 0; q < kFL / 4; ++q) {
+      const float c = fmaf(0.0f, h2f((uint16_t)b.s[4 * q]), s_h[q * kFNPR + r]);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const uint4 v = b.v[4 * q + 2 * HALF + e];
+        const uint32_t ws[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc[8 * e + 2 * u] = fmaf(c, lo_f(ws[u]), acc[8 * e + 2 * u]);
+          acc[8 * e + 2 * u + 1] = fmaf(c, hi_f(ws[u]), acc[8 * e + 2 * u + 1]);
+        }
+      }
+    }
+  } else if (k.tier == 2) {
+    // 2 loads per neuron and round, 16 columns each: this half is load H
+    float csum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kFL / 2; ++q) {
+      const float c = s_h[q * kFNPR + r] * h2f((uint16_t)b.s[2 * q]);
+      csum += c;
+      const float cs = c * kTwo24;
+      const uint4 v = b.v[2 * q + HALF];
+      const uint32_t ws[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t ob = ws[u] ^ 0x80808080u;
+        const uint32_t l = __builtin_amdgcn_perm(0u, ob, 0x0c010c00u);
+        const uint32_t h = __builtin_amdgcn_perm(0u, ob, 0x0c030c02u);
+        acc[4 * u] = fmaf(cs, lo_f(l), acc[4 * u]);
+        acc[4 * u + 1] = fmaf(cs, hi_f(l), acc[4 * u + 1]);
+        acc[4 * u + 2] = fmaf(cs, lo_f(h), acc[4 * u + 2]);
+        acc[4 * u + 3] = fmaf(cs, hi_f(h), acc[4 * u + 3]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = fmaf(-128.0f, csum, acc[e]);
+  } else {
+    // 1 load per neuron and round, 32 columns: this half is words 2H, 2H+1
+    float csum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kFL; ++q) {
+      const float c = s_h[q * kFNPR + r] * h2f((uint16_t)b.s[q]);
+      csum += c;
+      const float cs = c * kTwo24;
+      const uint32_t ws[2] = {HALF ? b.v[q].z : b.v[q].x, HALF ? b.v[q].w : b.v[q].y};
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const uint32_t ob = ws[u] ^ 0x88888888u;
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4) {
+          const uint32_t p = (ob >> (4 * s4)) & 0x000f000fu;  // nibbles s4 and s4 + 4
+          acc[8 * u + s4] = fmaf(cs, lo_f(p), acc[8 * u + s4]);
+          acc[8 * u + s4 + 4] = fmaf(cs, hi_f(p), acc[8 * u + s4 + 4]);
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = fmaf(-8.0f, csum, acc[e]);
+  }
+}
+
+__device__ __forceinline__ unsigned long long load_word(const unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+struct FShared {
+  int slot[kFT];
+  float h[kFT];
+  float row[kFWaves][kFSW];
+  float2 ab[kFWaves * kFL];
+  uint32_t epoch;
+};
+
+// Sum of v over lanes l and l ^ 16 (permlane16_swap hands each lane both
+// halves of its pair of 16-lane rows), then over l ^ 32 likewise.
+__device__ __forceinline__ float fold_16_32(float v) {
+  auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+
+// at most 80 VGPRs: three workgroups per CU
+template <int K>
+__global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void ffn_fused_kernel(
+    const uint16_t* __restrict__ x, int d, const int32_t* __restrict__ counts,
+    const int32_t* __restrict__ work_slot, const uint8_t* __restrict__ slots, uint32_t sb,
+    int cap, int n_slots, unsigned long long* __restrict__ gen,
+    unsigned long long* __restrict__ hw, int32_t* __restrict__ status, float* __restrict__ y) {
+  // dynamic LDS: x [d/8] | -128 * sums of 16 elements [d/16] | -8 * sums of 32 [d/32]
+  extern __shared__ uint4 xlds[];
+  __shared__ FShared sh;
+  const int tid = threadIdx.x;
+  const int t = blockIdx.x;
+  const FMap m = make_map<K>(counts, cap, d);
+  const FTask kc = decode<K>(m, t);
+  if (kc.kind == 0) {
+    if (tid == 0) atomicAdd(gen + t, 1ull);  // keep this workgroup's count in step
+    return;
+  }
+  const int n_items = kc.hi - kc.lo;
+  uint4* xs = xlds;
+  float* nx16 = reinterpret_cast<float*>(xlds + (d >> 3));
+  float* nx32 = nx16 + (d >> 4);
+  // the slot ids, the call count (only this workgroup touches gen[t]) and x
+  // (h tasks): one round trip
+  const unsigned long long e0 = gen[t];
+  const bool okslot = tid < n_items;
+  const int sl = work_slot[okslot ? kc.lo + tid : 0];
+  if (kc.kind == 1) {
+    constexpr int XPT = 2;  // d / 8 <= 2 * kFT for d <= 8192
+    static_assert(kFT * XPT * 8 >= 8192, "x staging covers d = 8192");
+    const int nc8 = d >> 3;
+    uint4 xv[XPT];
+#pragma unroll
+    for (int j = 0; j < XPT; ++j)
+      xv[j] = reinterpret_cast<const uint4*>(x)[min(tid + kFT * j, nc8 - 1)];
+#pragma unroll
+    for (int j = 0; j < XPT; ++j) {
+      const int c = tid + kFT * j;
+      if (c < nc8) xs[c] = xv[j];
+    }
+  }
+  sh.slot[tid] = okslot && sl >= 0 && sl < n_slots ? sl : n_slots;
+  __syncthreads();
+  FBuf cur;
+  issue<K>(kc, sh.slot, d, slots, sb, n_slots, tid, cur);
+  const uint32_t epoch = (uint32_t)e0 + 1u;
+  if (kc.kind == 1) {
+    // chunk sums of x while the task's loads are in flight
+    for (int c = tid; c < (d >> 4); c += kFT) {
+      const uint4 v0 = xs[2 * c], v1 = xs[2 * c + 1];
+      const uint32_t ws[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+      float sum = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum += lo_f(ws[e]) + hi_f(ws[e]);
+      nx16[c] = -128.0f * sum;
+    }
+    __syncthreads();
+    // -8 * (sum of 32) = (-128 * sum of the first 16 - 128 * sum of the next 16) / 16
+    for (int c = tid; c < (d >> 5); c += kFT) nx32[c] = (nx16[2 * c] + nx16[2 * c + 1]) * 0.0625f;
+    __syncthreads();
+    compute_h<K>(kc, cur, d, xs, nx16, nx32, tid, sh.ab);
+    __syncthreads();
+    const int upi = kc.tier == 3 ? 4 : kc.tier == 2 ? 2 : 1;
+    if (tid < n_items) {
+      float sa = sh.ab[tid * upi].x, sbv = sh.ab[tid * upi].y;
+      for (int u = 1; u < upi; ++u) {
+        sa += sh.ab[tid * upi + u].x;
+        sbv += sh.ab[tid * upi + u].y;
+      }
+      const float h = sh.slot[tid] < n_slots ? silu_mul(sa, sbv) : 0.0f;
+      const unsigned long long word =
+          ((unsigned long long)epoch << 32) | (unsigned long long)__float_as_uint(h);
+      __hip_atomic_store(hw + kc.lo + tid, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  } else {
+    // the h words of the run, polled after every data load has been issued
+    float h = 0.0f;
+    if (tid < n_items) {
+      unsigned long long hv = load_word(hw + kc.lo + tid);
+      int spins = 0;
+      while ((uint32_t)(hv >> 32) != epoch) {
+        if (++spins > kFSpin) {
+          atomicOr(status, M2C_STATUS_FFN_WAIT);
+          hv = 0;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        hv = load_word(hw + kc.lo + tid);
+      }
+      h = __uint_as_float((uint32_t)hv);
+    }
+    sh.h[tid] = h;
+    __syncthreads();
+    // lanes 16 and 32 apart hold the same columns: fold them, then the waves
+    // through LDS in a fixed order
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    {
+      float acc[16];
+      compute_dn_half<0>(kc, cur, sh.h, tid, acc);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = fold_16_32(acc[e]);
+      if (lane < kFLPN) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sh.row[w][32 * lane + e] = acc[e];
+      }
+    }
+    {
+      float acc[16];
+      compute_dn_half<1>(kc, cur, sh.h, tid, acc);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = fold_16_32(acc[e]);
+      if (lane < kFLPN) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) sh.row[w][32 * lane + 16 + e] = acc[e];
+      }
+    }
+    __syncthreads();
+    for (int c = tid; c < kFSW; c += kFT) {
+      float v = sh.row[0][c];
+#pragma unroll
+      for (int q = 1; q < kFWaves; ++q) v += sh.row[q][c];
+      const int col = kc.slice * kFSW + c;
+      if (col < d) atomicAdd(y + col, v);
+    }
+  }
+  if (tid == 0) gen[t] = e0 + 1;
+}
+
+template <int K>
+hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* counts,
+                        const int32_t* work_slot, float* y, hipStream_t stream) {
+  const int d = L->desc.d_model;
+  const size_t lds = (size_t)d * 2 + (size_t)d / 16 * 4 + (size_t)d / 32 * 4;
+  hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, d, counts,
+                     work_slot, L->slots, (uint32_t)L->info.slot_bytes, L->cap,
+                     L->desc.cache_slots + L->S, L->st.ffn_gen, L->st.ffn_hw, L->st.status, y);
+  return hipGetLastError();
+}
+
+int loads_per_unit(int d) {
+  const int kneed = (d + 1023) / 1024;
+  return kneed <= 1 ? 1 : kneed <= 2 ? 2 : kneed <= 4 ? 4 : 8;
+}
+
+}  // namespace
+
+bool ffn_fused_supported(const m2c_layer* L) {
+  const int64_t arena = (int64_t)(L->desc.cache_slots + L->S + 1) * L->info.slot_bytes;
+  return L->desc.d_model <= 8192 && arena < ((int64_t)1 << 32);
+}
+
+int ffn_fused_grid(int d, int cap, int num_cus) {
+  (void)num_cus;
+  if (cap <= 0) return 0;
+  // h tasks: at most cap / (FP16 neurons per task) + 1 per tier; down tasks:
+  // per slice at most cap / (FP16 neurons per run) + 1 per tier
+  const int U = kFWaves * (kFL / loads_per_unit(d));
+  const int64_t most = (int64_t)cap / (U / 4) + 3 +
+                       (int64_t)((d + kFSW - 1) / kFSW) * (cap / (2 * kFNPR) + 3);
+  return (int)most;
+}
+
+hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
+                            hipStream_t stream) {
+  if (L->cap <= 0 || L->ffn_grid <= 0) return hipSuccess;
+  const int32_t* counts = reinterpret_cast<const int32_t*>(plan + L->layout.counts);
+  const int32_t* work_slot = reinterpret_cast<const int32_t*>(plan + L->layout.work_slot);
+  switch (loads_per_unit(L->desc.d_model)) {
+    case 1: return launch_fused<1>(L, x, counts, work_slot, y, stream);
+    case 2: return launch_fused<2>(L, x, counts, work_slot, y, stream);
+    case 4: return launch_fused<4>(L, x, counts, work_slot, y, stream);
+    default: return launch_fused<8>(L, x, counts, work_slot, y, stream);
+  }
+}
+
+}  // namespace m2c

@@ -171,6 +171,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_h; void* p_ypart; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
   void* p_vslot; void* p_vold; void* p_fill_pos; void* p_stats; void* p_status;
+  void* p_gen; void* p_hw;
   Piece pieces[] = {
       // C resident + S staging slots, then one slot that stays zero: padding
       // lanes of the FFN kernels read it instead of branching around loads
@@ -195,6 +196,8 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_fill_pos, cap * 4},
       {&p_stats, 16 * 8},
       {&p_status, 4},
+      {&p_gen, (int64_t)m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus) * 8},
+      {&p_hw, cap * 8},
   };
   int64_t total = 0;
   int64_t offs[sizeof(pieces) / sizeof(pieces[0])];
@@ -229,10 +232,16 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.fill_pos = (int32_t*)p_fill_pos;
   L->st.stats = (unsigned long long*)p_stats;
   L->st.status = (int32_t*)p_status;
+  L->st.ffn_gen = (unsigned long long*)p_gen;
+  L->st.ffn_hw = (unsigned long long*)p_hw;
   L->info.device_bytes = total;
   HIPOK(hipMemset(L->slots + (C + L->S) * (int64_t)L->info.slot_bytes, 0, L->info.slot_bytes),
         "clear the zero slot");
   HIPOK(hipMemset(L->st.status, 0, 4), "clear the status word");
+  L->ffn_grid = m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus);
+  HIPOK(hipMemset(L->st.ffn_gen, 0, (size_t)(L->ffn_grid > 0 ? L->ffn_grid : 1) * 8),
+        "clear the FFN workgroup counters");
+  HIPOK(hipMemset(L->st.ffn_hw, 0, (size_t)(cap > 0 ? cap : 1) * 8), "clear the FFN h words");
   return M2C_OK;
 }
 
@@ -498,6 +507,9 @@ m2c_status m2c_layer_stats(const m2c_layer* L, m2c_stats* out) {
   HIPOK(hipMemcpy(&status, L->st.status, 4, hipMemcpyDeviceToHost), "read status");
   if (status) {
     HIPOK(hipMemset(L->st.status, 0, 4), "clear the status word");
+    if (status & m2c::M2C_STATUS_FFN_WAIT)
+      return fail(M2C_ERR_STATE, "a sparse FFN call gave up waiting for an h value and used 0 "
+                  "(status 0x%x): its output is wrong", status);
     return fail(M2C_ERR_CAPACITY, "a cache plan since the last check had more active neurons than "
                 "the layer was created for (k_max * max_batch); it was left empty (status 0x%x)",
                 status);

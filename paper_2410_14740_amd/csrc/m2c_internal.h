@@ -12,6 +12,7 @@ namespace m2c {
 // Bits of the per-layer device status word, reported (and cleared) by
 // m2c_layer_stats.
 constexpr int M2C_STATUS_PLAN_OVERFLOW = 2;  // a tier map had more active neurons than cap
+constexpr int M2C_STATUS_FFN_WAIT = 4;      // a sparse FFN gave up waiting for an h value
 
 // ---------------------------------------------------------------------------
 // Host-side layer object
@@ -43,6 +44,8 @@ struct DeviceState {
   int32_t* fill_pos = nullptr;   // [cap] plan scratch: fill position of req p (-1 for hits)
   unsigned long long* stats = nullptr;  // [16] cumulative counters
   int32_t* status = nullptr;           // [1] M2C_STATUS_* bits set by kernels
+  unsigned long long* ffn_gen = nullptr;  // [ffn_grid] per-workgroup call counters of the one-launch FFN
+  unsigned long long* ffn_hw = nullptr;   // [cap] (call tag, h) words of the one-launch FFN
 };
 
 }  // namespace m2c
@@ -67,6 +70,7 @@ struct m2c_layer {
   float2* ab = nullptr;        // [4 * cap] partial gate/up dot products per FFN unit
   float* y_part = nullptr;     // [ffn_groups][d] down-projection partial rows
   int ffn_groups = 1;
+  int ffn_grid = 0;  // workgroups of the one-launch FFN
   m2c::DeviceState st;
   int64_t last_step = -1;
 };
@@ -95,6 +99,10 @@ hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t*
 hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan,
                             float* y, hipStream_t stream);
 hipError_t launch_ffn_split(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
+                            hipStream_t stream);
+bool ffn_fused_supported(const m2c_layer* L);
+int ffn_fused_grid(int d_model, int cap, int num_cus);  // workgroups (and gen counters) of the one-launch FFN
+hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
                             hipStream_t stream);
 
 // ---------------------------------------------------------------------------

@@ -27,8 +27,8 @@ import re
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-FFN_SOURCES = ("csrc/k_ffn_split.hip", "csrc/ffn_device.h")
-FFN_KERNELS = ("ffn_h_kernel", "ffn_dn_kernel")
+FFN_SOURCES = ("csrc/k_ffn_fused.hip", "csrc/ffn_device.h")
+FFN_KERNELS = ("ffn_fused_kernel",)
 
 
 def ffn_source_hash() -> str:
