@@ -385,18 +385,20 @@ __device__ __forceinline__ unsigned long long load_word(const unsigned long long
 struct FShared {
   int slot[kFT];
   float h[kFT];
-  float row[kFWaves][kFSW];
   float2 ab[kFWaves * kFL];
   uint32_t epoch;
 };
 
-// Sum of v over lanes l and l ^ 16 (permlane16_swap hands each lane both
-// halves of its pair of 16-lane rows), then over l ^ 32 likewise.
-__device__ __forceinline__ float fold_16_32(float v) {
-  auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
-  auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+// Down fold: kFT / kFLPN lane groups (lanes with equal tid / kFLPN) each hold
+// 16 columns of half a slice per lane; the groups are summed through LDS.
+constexpr int kFGroups = kFT / kFLPN;
+constexpr size_t kFFoldBytes = (size_t)kFGroups * kFLPN * 16 * 4;
+
+// Dynamic LDS: x [d/8] | -128 * sums of 16 elements [d/16] | -8 * sums of 32
+// [d/32] for h tasks; the same bytes hold the fold of a down task.
+inline size_t fused_lds_bytes(int d) {
+  const size_t xb = (size_t)d * 2 + (size_t)d / 16 * 4 + (size_t)d / 32 * 4;
+  return xb > kFFoldBytes ? xb : kFFoldBytes;
 }
 
 // at most 80 VGPRs: three workgroups per CU
@@ -406,8 +408,7 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
     const int32_t* __restrict__ work_slot, const uint8_t* __restrict__ slots, uint32_t sb,
     int cap, int n_slots, unsigned long long* __restrict__ gen,
     unsigned long long* __restrict__ hw, int32_t* __restrict__ status, float* __restrict__ y) {
-  // dynamic LDS: x [d/8] | -128 * sums of 16 elements [d/16] | -8 * sums of 32 [d/32]
-  extern __shared__ uint4 xlds[];
+  extern __shared__ uint4 xlds[];  // fused_lds_bytes(d)
   __shared__ FShared sh;
   const int tid = threadIdx.x;
   const int t = blockIdx.x;
@@ -492,37 +493,34 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
     }
     sh.h[tid] = h;
     __syncthreads();
-    // lanes 16 and 32 apart hold the same columns: fold them, then the waves
-    // through LDS in a fixed order
-    const int lane = tid & 63;
-    const int w = tid >> 6;
+    // Lanes tid % kFLPN of every group share columns. Per half slice, each
+    // lane writes its 16 sums to LDS and thread c < 256 adds column c's
+    // kFGroups partials in a fixed order, then one fp32 atomic per column.
+    float* part = reinterpret_cast<float*>(xlds);
+    const int grp = tid / kFLPN, mcol = tid % kFLPN;
+    auto fold_half = [&](const float (&acc)[16], int half) {
+      float4* dst = reinterpret_cast<float4*>(part + (grp * kFLPN + mcol) * 16);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        dst[q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+      __syncthreads();
+      if (tid < kFLPN * 16) {
+        float v = 0.0f;
+        for (int g = 0; g < kFGroups; ++g) v += part[g * kFLPN * 16 + tid];
+        const int col = kc.slice * kFSW + 32 * (tid >> 4) + 16 * half + (tid & 15);
+        if (col < d) atomicAdd(y + col, v);
+      }
+      __syncthreads();
+    };
     {
       float acc[16];
       compute_dn_half<0>(kc, cur, sh.h, tid, acc);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[e] = fold_16_32(acc[e]);
-      if (lane < kFLPN) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sh.row[w][32 * lane + e] = acc[e];
-      }
+      fold_half(acc, 0);
     }
     {
       float acc[16];
       compute_dn_half<1>(kc, cur, sh.h, tid, acc);
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[e] = fold_16_32(acc[e]);
-      if (lane < kFLPN) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) sh.row[w][32 * lane + 16 + e] = acc[e];
-      }
-    }
-    __syncthreads();
-    for (int c = tid; c < kFSW; c += kFT) {
-      float v = sh.row[0][c];
-#pragma unroll
-      for (int q = 1; q < kFWaves; ++q) v += sh.row[q][c];
-      const int col = kc.slice * kFSW + c;
-      if (col < d) atomicAdd(y + col, v);
+      fold_half(acc, 1);
     }
   }
   if (tid == 0) gen[t] = e0 + 1;
@@ -532,7 +530,7 @@ template <int K>
 hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* counts,
                         const int32_t* work_slot, float* y, hipStream_t stream) {
   const int d = L->desc.d_model;
-  const size_t lds = (size_t)d * 2 + (size_t)d / 16 * 4 + (size_t)d / 32 * 4;
+  const size_t lds = fused_lds_bytes(d);
   hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, d, counts,
                      work_slot, L->slots, (uint32_t)L->info.slot_bytes, L->cap,
                      L->desc.cache_slots + L->S, L->st.ffn_gen, L->st.ffn_hw, L->st.status, y);
