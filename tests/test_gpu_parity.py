@@ -381,3 +381,70 @@ def test_plan_overflow_is_reported():
     slot_of, key, _, _ = m2c.m2c_debug_read_tables(L.handle, 200, 30)
     assert (slot_of == -1).all() and (key == -1).all()
     L.close()
+
+
+def test_one_launch_ffn_call_tags_and_graph_replay():
+    """The batch-1 FFN tags its h values with a per-call count kept on the
+    device: calls that reuse one plan with different x never read an h of an
+    earlier call, and a graph that captured the launch is correct on every
+    replay (the count advances without any host argument)."""
+    ld = W.make_layer(W.WORKLOADS["tiny"].seed, 3, 1024, 2752, 128, 6)
+    k = 688
+    n16, n8 = _counts(k)
+    L = _layer(ld, k, 1376)
+    tiers = torch.empty((1, ld.d_ff), dtype=torch.uint8, device="cuda")
+    say("call tags: plan")
+    L.predict_rank(_x16(ld, 0), 1, k, n16, n8, None, tiers)
+    L.cache_plan(tiers, 1, 0)
+    L.cache_fill()
+    torch.cuda.synchronize()
+    plan = L.read_plan()
+
+    def ref(t):
+        return oracle_ffn(ld, ld.x[t], plan["req_ids"], plan["req_tier"])[0]
+
+    # eager calls on one plan, x changing every call
+    for t in (1, 2, 1, 3):
+        say(f"call tags: eager x[{t}]")
+        y = torch.zeros((1, ld.d_model), dtype=torch.float32, device="cuda")
+        L.sparse_ffn(_x16(ld, t), 1, y)
+        torch.cuda.synchronize()
+        assert r8_errors(y.cpu().numpy()[0], ref(t)).max() <= FFN_TOL, f"eager call with x[{t}]"
+    # graph: zero y (a kernel, not a memset) and the FFN on a fixed x buffer
+    xg = _x16(ld, 0).clone()
+    yg = torch.zeros((1, ld.d_model), dtype=torch.float32, device="cuda")
+    ye = torch.zeros((1, ld.d_model), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    say("call tags: capture")
+    with torch.cuda.graph(g, stream=s):
+        yg.zero_()
+        L.sparse_ffn(xg, 1, yg)
+    torch.cuda.synchronize()
+    for t in (4, 5, 4):
+        say(f"call tags: replay with x[{t}]")
+        xg.copy_(_x16(ld, t))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert r8_errors(yg.cpu().numpy()[0], ref(t)).max() <= FFN_TOL, f"replay with x[{t}]"
+        # eager work between replays advances the same counters
+        ye.zero_()
+        L.sparse_ffn(_x16(ld, 2), 1, ye)
+        torch.cuda.synchronize()
+        assert r8_errors(ye.cpu().numpy()[0], ref(2)).max() <= FFN_TOL
+    del g
+    L.stats()  # no wait was given up
+    L.close()
+
+
+def test_widest_layer_uses_two_kernel_ffn():
+    """d_model = 16384, the widest layer the library takes: the batch-1 FFN
+    runs as two kernels there (the one-launch kernel stages x for d <= 8192);
+    every stage against the oracle over two steps."""
+    ld = W.make_layer(29, 0, 16384, 600, 32, 2)
+    k = 150
+    n16, n8 = _counts(k)
+    worst = _run_steps(ld, 2, k, n16, n8, 300, label="d=16384")
+    say(f"d=16384 worst FFN error {worst:.2e}")
