@@ -40,7 +40,7 @@ def ffn_source_hash() -> str:
 
 
 def _short(name: str) -> str:
-    return name.split("(")[0].replace("void ", "")
+    return name.replace("(anonymous namespace)::", "").split("(")[0].replace("void ", "")
 
 
 def _per_kernel_counter(path: str, kernels) -> dict:
