@@ -171,10 +171,15 @@ __device__ __forceinline__ float hi_f(uint32_t p) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)(p >> 16));
 }
 
+static_assert(kFNPR * kFL <= kWorkSlotPad && kFWaves * kFL <= kWorkSlotPad,
+              "slot id reads stay inside the padded work_slot array");
+
 // Issue every load of task k into b: kFL data loads and kFL scale loads per
-// lane, whatever the kind. ss: the task's slot ids (n_slots past its items).
+// lane, whatever the kind. The slot ids come from work_slot by scalar
+// loads: wave-uniform reads that do not queue behind the vector loads other
+// workgroups of the CU already have in flight.
 template <int K>
-__device__ __forceinline__ void issue(const FTask& k, const int* ss, int d,
+__device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict__ work_slot, int d,
                                       const uint8_t* __restrict__ slots, uint32_t sb,
                                       int n_slots, int tid, FBuf& b) {
   // byte offsets into the slot arena (below 4 GiB: checked at launch), so
@@ -192,10 +197,24 @@ __device__ __forceinline__ void issue(const FTask& k, const int* ss, int d,
     const uint32_t dbase = k.tier == 3 ? 4 * ud + 2 * col : k.tier == 2 ? 2 * ud + col
                                                                         : ud + (col >> 1);
     const uint32_t sbase = (k.tier == 1 ? 3 * (ud >> 1) : 3 * ud) + 4 * G + 2 * (col >> 7);
+    // a wave covers the four neurons 4w .. 4w + 3 of every round: four
+    // scalar loads per round, one of them picked per lane
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    const int n = k.hi - k.lo;
+    const int sub = lane >> 4;
 #pragma unroll
     for (int j = 0; j < kFL; ++j) {
       const int q = j >> lnv, e = j & ((1 << lnv) - 1);
-      const uint32_t rec = (uint32_t)ss[q * kFNPR + r] * sb;
+      int sv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int it = q * kFNPR + 4 * wu + i;
+        // k.lo < cap and it < kFNPR * kFL: inside the array's spare tail
+        const int v = (work_slot + k.lo + q * kFNPR + 4 * wu)[i];
+        sv[i] = it < n && v >= 0 && v < n_slots ? v : n_slots;
+      }
+      const int slv = sub == 0 ? sv[0] : sub == 1 ? sv[1] : sub == 2 ? sv[2] : sv[3];
+      const uint32_t rec = (uint32_t)slv * sb;
       // the scale of an FP16 record (it has none) is read from the zero slot,
       // never from the data's own address: every load stays independent
       const uint32_t dp = colok ? rec + dbase + 16 * e : zero;
@@ -210,11 +229,17 @@ __device__ __forceinline__ void issue(const FTask& k, const int* ss, int d,
     const int ncu = d >> 5;  // 16-byte chunks of each row in a unit
     const uint32_t row = k.tier == 3 ? 2 * ud : k.tier == 2 ? ud : (ud >> 1);
     const uint32_t sbase = k.tier == 1 ? 3 * (ud >> 1) : 3 * ud;
+    // the slot of a unit is the same for the whole wave: a scalar load,
+    // which does not queue behind the vector loads already in flight
+    const int wu = __builtin_amdgcn_readfirstlane(w);
+    const int n = k.hi - k.lo;
 #pragma unroll
     for (int j = 0; j < kFL; ++j) {
-      const int u = w * UW + j / K;
-      const int item = u / upi, part = u - item * upi;
-      const uint32_t rec = (uint32_t)ss[item] * sb;  // zero slot past the task (and kind 0)
+      const int u = wu * UW + j / K;
+      const int item = u / upi, part = (w * UW + j / K) % upi;
+      const int v = work_slot[k.lo + item];  // item < kFWaves * kFL
+      const int slv = k.kind == 1 && item < n && v >= 0 && v < n_slots ? v : n_slots;
+      const uint32_t rec = (uint32_t)slv * sb;  // zero slot past the task (and kind 0)
       int q = lane + 64 * (j % K);
       const bool in = q < 2 * ncu;
       q = in ? q : 2 * ncu - 1;
@@ -382,11 +407,13 @@ __device__ __forceinline__ unsigned long long load_word(const unsigned long long
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The first kFT words are not used: with h at offset 0 the register
+// allocator of hipcc (ROCm 7.2) spills a VGPR in the down path of some
+// instances, and this layout compiles without scratch for every K.
 struct FShared {
-  int slot[kFT];
-  float h[kFT];
-  float2 ab[kFWaves * kFL];
-  uint32_t epoch;
+  int unused[kFT];
+  float h[kFT];                // down task: the h values of its neurons
+  float2 ab[kFWaves * kFL];    // h task: per-unit gate / up sums
 };
 
 // Down fold: kFT / kFLPN lane groups (lanes with equal tid / kFLPN) each hold
@@ -422,43 +449,46 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
   uint4* xs = xlds;
   float* nx16 = reinterpret_cast<float*>(xlds + (d >> 3));
   float* nx32 = nx16 + (d >> 4);
-  // the slot ids, the call count (only this workgroup touches gen[t]) and x
-  // (h tasks): one round trip
+  // the call count (only this workgroup touches gen[t]) and, for the h
+  // publish, this thread's item slot
   const unsigned long long e0 = gen[t];
   const bool okslot = tid < n_items;
   const int sl = work_slot[okslot ? kc.lo + tid : 0];
-  if (kc.kind == 1) {
-    constexpr int XPT = 2;  // d / 8 <= 2 * kFT for d <= 8192
-    static_assert(kFT * XPT * 8 >= 8192, "x staging covers d = 8192");
-    const int nc8 = d >> 3;
-    uint4 xv[XPT];
-#pragma unroll
-    for (int j = 0; j < XPT; ++j)
-      xv[j] = reinterpret_cast<const uint4*>(x)[min(tid + kFT * j, nc8 - 1)];
-#pragma unroll
-    for (int j = 0; j < XPT; ++j) {
-      const int c = tid + kFT * j;
-      if (c < nc8) xs[c] = xv[j];
-    }
-  }
-  sh.slot[tid] = okslot && sl >= 0 && sl < n_slots ? sl : n_slots;
-  __syncthreads();
   FBuf cur;
-  issue<K>(kc, sh.slot, d, slots, sb, n_slots, tid, cur);
+  uint4 xv0 = make_uint4(0, 0, 0, 0), xv1 = xv0;
+  if (kc.kind == 1) {
+    // x in registers, 16 values per thread; the data loads wait only for
+    // the scalar slot loads inside issue, and x arrives while they fly
+    static_assert(2 * kFT * 8 >= 8192, "x staging covers d = 8192");
+    const int nc8 = d >> 3;
+    const uint4* x4 = reinterpret_cast<const uint4*>(x);
+    xv0 = x4[min(2 * tid, nc8 - 1)];
+    xv1 = x4[min(2 * tid + 1, nc8 - 1)];
+    issue<K>(kc, work_slot, d, slots, sb, n_slots, tid, cur);
+  } else {
+    issue<K>(kc, work_slot, d, slots, sb, n_slots, tid, cur);
+  }
   const uint32_t epoch = (uint32_t)e0 + 1u;
   if (kc.kind == 1) {
-    // chunk sums of x while the task's loads are in flight
-    for (int c = tid; c < (d >> 4); c += kFT) {
-      const uint4 v0 = xs[2 * c], v1 = xs[2 * c + 1];
-      const uint32_t ws[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    // x into LDS and the chunk sums of this thread's 16 values, while the
+    // task's loads are in flight
+    {
+      const bool own = 2 * tid < (d >> 3);
+      if (own) {
+        xs[2 * tid] = xv0;
+        xs[2 * tid + 1] = xv1;
+      }
+      const uint32_t ws[8] = {xv0.x, xv0.y, xv0.z, xv0.w, xv1.x, xv1.y, xv1.z, xv1.w};
       float sum = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) sum += lo_f(ws[e]) + hi_f(ws[e]);
-      nx16[c] = -128.0f * sum;
+      const float n16 = -128.0f * sum;
+      // -8 * (sum of 32) = (-128 * sum of this 16 - 128 * sum of the neighbour's 16) / 16
+      const float other = __int_as_float(
+          __builtin_amdgcn_mov_dpp(__float_as_int(n16), 0xB1, 0xF, 0xF, false));
+      if (own) nx16[tid] = n16;
+      if (own && (tid & 1) == 0) nx32[tid >> 1] = (n16 + other) * 0.0625f;
     }
-    __syncthreads();
-    // -8 * (sum of 32) = (-128 * sum of the first 16 - 128 * sum of the next 16) / 16
-    for (int c = tid; c < (d >> 5); c += kFT) nx32[c] = (nx16[2 * c] + nx16[2 * c + 1]) * 0.0625f;
     __syncthreads();
     compute_h<K>(kc, cur, d, xs, nx16, nx32, tid, sh.ab);
     __syncthreads();
@@ -469,7 +499,7 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
         sa += sh.ab[tid * upi + u].x;
         sbv += sh.ab[tid * upi + u].y;
       }
-      const float h = sh.slot[tid] < n_slots ? silu_mul(sa, sbv) : 0.0f;
+      const float h = sl >= 0 && sl < n_slots ? silu_mul(sa, sbv) : 0.0f;
       const unsigned long long word =
           ((unsigned long long)epoch << 32) | (unsigned long long)__float_as_uint(h);
       __hip_atomic_store(hw + kc.lo + tid, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -125,7 +125,7 @@ void fill_info_layout(m2c_layer* L) {
   P.fill_tier = take(c);
   P.fill_slot = take(4 * c);
   P.evicted_ids = take(4 * c);
-  P.work_slot = take(4 * c);
+  P.work_slot = take(4 * (c + m2c::kWorkSlotPad));
   P.work_mask = take(4 * c);
   P.total_bytes = off;
   I.plan_bytes = off;
