@@ -197,22 +197,29 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
     const uint32_t dbase = k.tier == 3 ? 4 * ud + 2 * col : k.tier == 2 ? 2 * ud + col
                                                                         : ud + (col >> 1);
     const uint32_t sbase = (k.tier == 1 ? 3 * (ud >> 1) : 3 * ud) + 4 * G + 2 * (col >> 7);
-    // a wave covers the four neurons 4w .. 4w + 3 of every round: four
-    // scalar loads per round, one of them picked per lane
+    // A wave covers the four neurons 4w .. 4w + 3 of every round. Their slot
+    // ids for all kFL rounds are read by scalar loads before the first one
+    // is used (one round trip; a tier with fewer rounds ignores the rest),
+    // then each lane picks its own.
     const int wu = __builtin_amdgcn_readfirstlane(w);
     const int n = k.hi - k.lo;
     const int sub = lane >> 4;
+    const int32_t* wp = work_slot + k.lo + 4 * wu;  // k.lo < cap: inside the spare tail
+    int ids[kFL][4];
 #pragma unroll
-    for (int j = 0; j < kFL; ++j) {
-      const int q = j >> lnv, e = j & ((1 << lnv) - 1);
-      int sv[4];
+    for (int q = 0; q < kFL; ++q)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int it = q * kFNPR + 4 * wu + i;
-        // k.lo < cap and it < kFNPR * kFL: inside the array's spare tail
-        const int v = (work_slot + k.lo + q * kFNPR + 4 * wu)[i];
-        sv[i] = it < n && v >= 0 && v < n_slots ? v : n_slots;
+        const int v = __builtin_amdgcn_readfirstlane(wp[q * kFNPR + i]);
+        ids[q][i] = q * kFNPR + 4 * wu + i < n && v >= 0 && v < n_slots ? v : n_slots;
       }
+#pragma unroll
+    for (int j = 0; j < kFL; ++j) {
+      const int e = j & ((1 << lnv) - 1);
+      int sv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)  // round j >> lnv
+        sv[i] = k.tier == 3 ? ids[j >> 2][i] : k.tier == 2 ? ids[j >> 1][i] : ids[j][i];
       const int slv = sub == 0 ? sv[0] : sub == 1 ? sv[1] : sub == 2 ? sv[2] : sv[3];
       const uint32_t rec = (uint32_t)slv * sb;
       // the scale of an FP16 record (it has none) is read from the zero slot,
@@ -229,17 +236,26 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
     const int ncu = d >> 5;  // 16-byte chunks of each row in a unit
     const uint32_t row = k.tier == 3 ? 2 * ud : k.tier == 2 ? ud : (ud >> 1);
     const uint32_t sbase = k.tier == 1 ? 3 * (ud >> 1) : 3 * ud;
-    // the slot of a unit is the same for the whole wave: a scalar load,
-    // which does not queue behind the vector loads already in flight
+    // The slot of a unit is the same for the whole wave: the UW slot ids of
+    // the wave's units are read by scalar loads before the first is used.
     const int wu = __builtin_amdgcn_readfirstlane(w);
     const int n = k.hi - k.lo;
+    int ids[UW];
+#pragma unroll
+    for (int uw = 0; uw < UW; ++uw)  // item < kFWaves * kFL: inside the spare tail
+      ids[uw] = __builtin_amdgcn_readfirstlane(work_slot[k.lo + (wu * UW + uw) / upi]);
+    __builtin_amdgcn_sched_barrier(0);  // every load goes out before the first check
+#pragma unroll
+    for (int uw = 0; uw < UW; ++uw) {
+      const int item = (wu * UW + uw) / upi;
+      const int v = ids[uw];
+      // the zero slot past the task (and for kind 0)
+      ids[uw] = k.kind == 1 && item < n && v >= 0 && v < n_slots ? v : n_slots;
+    }
 #pragma unroll
     for (int j = 0; j < kFL; ++j) {
-      const int u = wu * UW + j / K;
-      const int item = u / upi, part = (w * UW + j / K) % upi;
-      const int v = work_slot[k.lo + item];  // item < kFWaves * kFL
-      const int slv = k.kind == 1 && item < n && v >= 0 && v < n_slots ? v : n_slots;
-      const uint32_t rec = (uint32_t)slv * sb;  // zero slot past the task (and kind 0)
+      const int part = (w * UW + j / K) % upi;
+      const uint32_t rec = (uint32_t)ids[j / K] * sb;
       int q = lane + 64 * (j % K);
       const bool in = q < 2 * ncu;
       q = in ? q : 2 * ncu - 1;
@@ -418,8 +434,12 @@ struct FShared {
 
 // Down fold: kFT / kFLPN lane groups (lanes with equal tid / kFLPN) each hold
 // 16 columns of half a slice per lane; the groups are summed through LDS.
+// Lane t stores its q-th four sums as the 16-byte granule q * kFFoldStride + t
+// (consecutive lanes, consecutive granules); the 4-granule pad per q puts the
+// 64 reads of a wave (4 q x 4 column groups x 4 words) on 64 distinct banks.
 constexpr int kFGroups = kFT / kFLPN;
-constexpr size_t kFFoldBytes = (size_t)kFGroups * kFLPN * 16 * 4;
+constexpr int kFFoldStride = kFT + 4;
+constexpr size_t kFFoldBytes = (size_t)(3 * kFFoldStride + kFT) * 16;
 
 // Dynamic LDS: x [d/8] | -128 * sums of 16 elements [d/16] | -8 * sums of 32
 // [d/32] for h tasks; the same bytes hold the fold of a down task.
@@ -525,18 +545,21 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
     __syncthreads();
     // Lanes tid % kFLPN of every group share columns. Per half slice, each
     // lane writes its 16 sums to LDS and thread c < 256 adds column c's
-    // kFGroups partials in a fixed order, then one fp32 atomic per column.
+    // kFGroups partials in a fixed order, then one fp32 atomic per column
+    // (a workgroup barrier does not wait for it).
     float* part = reinterpret_cast<float*>(xlds);
-    const int grp = tid / kFLPN, mcol = tid % kFLPN;
     auto fold_half = [&](const float (&acc)[16], int half) {
-      float4* dst = reinterpret_cast<float4*>(part + (grp * kFLPN + mcol) * 16);
+      float4* dst = reinterpret_cast<float4*>(part) + tid;
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        dst[q] = make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
+        dst[q * kFFoldStride] =
+            make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
       __syncthreads();
       if (tid < kFLPN * 16) {
+        // column tid of the half slice: lane group member tid >> 4, sum (tid & 15)
+        const float* src = part + 4 * ((tid & 15) >> 2) * kFFoldStride + 4 * (tid >> 4) + (tid & 3);
         float v = 0.0f;
-        for (int g = 0; g < kFGroups; ++g) v += part[g * kFLPN * 16 + tid];
+        for (int g = 0; g < kFGroups; ++g) v += src[g * kFLPN * 4];
         const int col = kc.slice * kFSW + 32 * (tid >> 4) + 16 * half + (tid & 15);
         if (col < d) atomicAdd(y + col, v);
       }
