@@ -62,7 +62,7 @@ def _load():
             "orc_dequant_record": (I, [I, I, P, P, P, P]),
             "orc_predict": (I, [I, I, I, P, P, P, P, P, P]),
             "orc_select_tiers": (I, [I, P, I, I, I, P, P]),
-            "orc_lru_plan": (I, [I, I, I, I, P, I] + [P] * 4 + [P] * 12),
+            "orc_lru_plan": (I, [I, I, I, I, P, I] + [P] * 4 + [P] * 13),
             "orc_sparse_ffn": (I, [I, I, I, P, P, P, P, I64, P, I64, P, I64, P, P]),
             "orc_dense_ffn": (I, [I, I, P, P, P, P, P]),
         }
@@ -179,6 +179,7 @@ class LRUCache:
             req_hit=np.zeros(n, np.uint8), req_slot=np.zeros(n, np.int32),
             req_mask=np.zeros(n, np.uint32), fill_ids=np.zeros(n, np.int32),
             fill_tier=np.zeros(n, np.uint8), fill_slot=np.zeros(n, np.int32),
+            fill_from=np.zeros(n, np.uint8),
             evicted_ids=np.zeros(n, np.int32), work_slot=np.zeros(n, np.int32),
             work_mask=np.zeros(n, np.uint32),
         )
@@ -187,7 +188,8 @@ class LRUCache:
             _p(self.slot_of), _p(self.slot_key), _p(self.slot_tier), _p(self.slot_last),
             _p(counts), _p(out["req_ids"]), _p(out["req_tier"]), _p(out["req_hit"]),
             _p(out["req_slot"]), _p(out["req_mask"]), _p(out["fill_ids"]), _p(out["fill_tier"]),
-            _p(out["fill_slot"]), _p(out["evicted_ids"]), _p(out["work_slot"]), _p(out["work_mask"]),
+            _p(out["fill_slot"]), _p(out["fill_from"]), _p(out["evicted_ids"]),
+            _p(out["work_slot"]), _p(out["work_mask"]),
         )
         if rc != 0:
             raise RuntimeError(f"orc_lru_plan failed ({rc})")
@@ -195,7 +197,7 @@ class LRUCache:
         res = {"counts": counts}
         for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "work_slot", "work_mask"):
             res[key] = out[key][:nreq].copy()
-        for key in ("fill_ids", "fill_tier", "fill_slot"):
+        for key in ("fill_ids", "fill_tier", "fill_slot", "fill_from"):
             res[key] = out[key][:nfill].copy()
         res["evicted_ids"] = out["evicted_ids"][:nev].copy()
         return res

@@ -295,17 +295,23 @@ int orc_select_tiers(int d_ff, const float* s, int k, int n16, int n8, uint8_t* 
  * Outputs: counts [16] (same order as the library's plan counts), the
  * required list (ids, tier, hit code 0 NEW 1 HIT 2 REFILL 3 BYPASS, slot,
  * row mask), the fill list, evicted ids, and the FFN work order
- * (tier-major FP16, INT8, INT4; ascending id inside a tier).               */
+ * (tier-major FP16, INT8, INT4; ascending id inside a tier).
+ * fill_from[f]: for a REFILL, the tier of the record the slot held for the
+ * same neuron before the step, else 0. counts[13] counts the fills whose
+ * slot held the neuron's FP16 record and that need INT8 or INT4: the record
+ * they need is a function of bytes already in the slot (every tier record is
+ * quantized from the same fp16 weights), so no host copy is needed.        */
 
 int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int step,
                  int32_t* slot_of, int32_t* slot_key, uint8_t* slot_tier, int32_t* slot_last,
                  int32_t* counts, int32_t* req_ids, uint8_t* req_tier, uint8_t* req_hit,
                  int32_t* req_slot, uint32_t* req_mask, int32_t* fill_ids, uint8_t* fill_tier,
-                 int32_t* fill_slot, int32_t* evicted_ids, int32_t* work_slot,
-                 uint32_t* work_mask) {
+                 int32_t* fill_slot, uint8_t* fill_from, int32_t* evicted_ids,
+                 int32_t* work_slot, uint32_t* work_mask) {
   if (d_ff <= 0 || C < 0 || S < 0 || B < 1 || B > 32) return -1;
   for (int c = 0; c < 16; c++) counts[c] = 0;
   uint8_t* touched = (uint8_t*)calloc((size_t)(C > 0 ? C : 1), 1);
+  uint8_t* before = (uint8_t*)calloc((size_t)(d_ff > 0 ? d_ff : 1), 1); /* by position */
   int n = 0;
   for (int i = 0; i < d_ff; i++) {
     int t = 0;
@@ -327,6 +333,7 @@ int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int ste
     int i = req_ids[p], s = slot_of[i];
     if (s >= 0) {
       touched[s] = 1;
+      before[p] = slot_tier[s];
       if (slot_tier[s] == req_tier[p]) { req_hit[p] = 1; counts[1]++; }
       else { req_hit[p] = 2; counts[2]++; slot_tier[s] = req_tier[p]; }
       req_slot[p] = s;
@@ -345,7 +352,7 @@ int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int ste
       if (v < 0 || slot_last[s] < slot_last[v]) v = s; /* ties keep the lower slot */
     }
     if (v < 0) {
-      if (n_bypass >= S) { free(touched); return -2; } /* staging overflow */
+      if (n_bypass >= S) { free(touched); free(before); return -2; } /* staging overflow */
       req_hit[p] = 3;
       req_slot[p] = C + n_bypass;
       n_bypass++;
@@ -373,7 +380,9 @@ int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int ste
     fill_ids[nf] = req_ids[p];
     fill_tier[nf] = req_tier[p];
     fill_slot[nf] = req_slot[p];
+    fill_from[nf] = req_hit[p] == 2 ? before[p] : 0;
     counts[10 + (3 - req_tier[p])]++;
+    if (fill_from[nf] == 3 && req_tier[p] < 3) counts[13]++;
     nf++;
   }
   counts[6] = nf;
@@ -389,6 +398,7 @@ int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int ste
     for (int p = 0; p < n; p++) counts[7 + (3 - t)] += (req_tier[p] == t);
   }
   free(touched);
+  free(before);
   return 0;
 }
 

@@ -247,7 +247,7 @@ def _brute_lru_step(state, tiers, step, C):
         if i in slot_of:
             s = slot_of[i]
             touched.add(s)
-            res[i] = ("HIT" if stier[s] == tiers[i] else "REFILL", s)
+            res[i] = ("HIT" if stier[s] == tiers[i] else "REFILL", s, stier[s])
             stier[s] = tiers[i]
     free = sorted((last[s], s) for s in range(C) if s not in touched)
     new = [i for i in req if i not in slot_of]
@@ -276,6 +276,7 @@ def test_lru_matches_brute_force(d_ff, C, B):
     cache = oracle.LRUCache(d_ff, C, S)
     st = ({}, [None] * C, [0] * C, [-1] * C)
     code = {"NEW": 0, "HIT": 1, "REFILL": 2, "BYPASS": 3}
+    derived = 0
     for step in range(30):
         tm = np.zeros((B, d_ff), np.uint8)
         for b in range(B):
@@ -289,7 +290,12 @@ def test_lru_matches_brute_force(d_ff, C, B):
         assert [res[i][1] for i in req] == list(p["req_slot"])
         assert list(p["evicted_ids"]) == ev
         assert list(p["fill_ids"]) == [i for i in req if res[i][0] != "HIT"]
+        # the tier a REFILL's slot held before the step (0 for NEW / BYPASS)
+        frm = [res[i][2] if res[i][0] == "REFILL" else 0 for i in req if res[i][0] != "HIT"]
+        assert list(p["fill_from"]) == frm
         c = p["counts"]
+        assert c[13] == sum(1 for f, i in zip(frm, p["fill_ids"]) if f == 3 and tiers[i] < 3)
+        derived += int(c[13])
         assert c[0] == c[1] + c[2] + c[3] + c[4] == len(req)
         assert c[6] == c[2] + c[3] + c[4] == c[10] + c[11] + c[12]
         # masks: bit b set iff row b selected the neuron
@@ -306,6 +312,7 @@ def test_lru_matches_brute_force(d_ff, C, B):
             assert cache.slot_last[s_] == st[3][s_]
             if k_ >= 0:
                 assert cache.slot_of[k_] == s_ and cache.slot_tier[s_] == st[2][s_]
+    assert C == 0 or derived > 0  # the FP16 -> lower-tier refill case was exercised
 
 
 def test_lru_atu_closed_form():
