@@ -299,7 +299,9 @@ def batched_sweep(steps, warmup, torch, m2c, W):
                 "us_predict_plan_fill_ffn": [round(float(v) * 1e3, 2) for v in ms.mean(axis=0)],
                 "union_neurons": req / steps, "hit_rate": (st1.hit - st0.hit) / max(req, 1),
                 "bypass_rate": (st1.bypass - st0.bypass) / max(req, 1),
-                "fill_MB_per_step": (st1.fill_bytes - st0.fill_bytes) / steps / 1e6,
+                "fill_MB_per_step": (st1.host_bytes - st0.host_bytes) / steps / 1e6,
+                "derived_MB_per_step": ((st1.fill_bytes - st0.fill_bytes)
+                                        - (st1.host_bytes - st0.host_bytes)) / steps / 1e6,
                 "ffn_bytes_per_step": ffn_bytes, "ffn_GBps": ffn_bytes / ffn_s / 1e9})
             log(f"batched sweep: cache {float(cap):.0%} tiers {mix}: "
                 f"{points[-1]['us_per_step']:.1f} us/step")
@@ -414,7 +416,10 @@ def main():
     hits = sum(b.hit - a.hit for a, b in zip(st0, st1))
     refills = sum(b.refill - a.refill for a, b in zip(st0, st1))
     bypass = sum(b.bypass - a.bypass for a, b in zip(st0, st1))
-    fill_bytes = sum(b.fill_bytes - a.fill_bytes for a, b in zip(st0, st1))
+    # bytes the fills read over the host link (fills derived on the GPU from a
+    # resident FP16 record read none)
+    fill_bytes = sum(b.host_bytes - a.host_bytes for a, b in zip(st0, st1))
+    derived_bytes = sum(b.fill_bytes - a.fill_bytes for a, b in zip(st0, st1)) - fill_bytes
     n_ls = args.steps * n_layers
     # host-link rate of the fills: from the stage events if recorded, else
     # the fill bytes over the wall time (a lower bound: fills run back to
@@ -475,6 +480,7 @@ def main():
             "ffn_us_avg": float(ffn_ms.mean()) * 1e3 if ffn_ms is not None else None,
             "fill_us_avg": fill_avg_s * 1e6 if fill_ms is not None else None,
             "fill_MB_per_layer_step": fill_bytes / n_ls / 1e6,
+            "derived_MB_per_layer_step": derived_bytes / n_ls / 1e6,
             "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
                       "bypass_rate": bypass / max(reqs, 1)},
         },

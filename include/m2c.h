@@ -175,6 +175,9 @@ enum {
   M2C_CNT_FILL_FP16 = 10, /* fills by tier                                    */
   M2C_CNT_FILL_INT8 = 11,
   M2C_CNT_FILL_INT4 = 12,
+  M2C_CNT_FILL_DERIVED = 13, /* INT8 / INT4 fills of a neuron whose slot held its
+                             FP16 record: made on the GPU from that record,
+                             no host read (fill_from == 3)                     */
   M2C_NCOUNTS = 16
 };
 typedef struct {
@@ -187,6 +190,8 @@ typedef struct {
   int64_t fill_ids;    /* int32 [cap] misses in ascending neuron id           */
   int64_t fill_tier;   /* uint8 [cap]                                         */
   int64_t fill_slot;   /* int32 [cap]                                         */
+  int64_t fill_from;   /* uint8 [cap] REFILL: tier of the record the slot held
+                          for the neuron before the step; NEW / BYPASS: 0     */
   int64_t evicted_ids; /* int32 [cap] evicted neurons in victim order         */
   int64_t work_slot;   /* int32 [cap] R regrouped tier-major (FP16, INT8,
                           INT4), ascending id inside a tier: FFN work order;
@@ -201,6 +206,9 @@ typedef struct {
   int64_t req, hit, refill, new_, bypass, evict;
   int64_t fill[4];        /* fills by tier                                    */
   int64_t fill_bytes;     /* sum of record_bytes over fills                   */
+  int64_t derived[4];     /* fills by tier made from the resident FP16 record */
+  int64_t host_bytes;     /* sum of record_bytes over fills read from the host
+                             store: fill_bytes minus the derived fills'       */
   int64_t req_tier[4];    /* required neurons by step tier                    */
   int64_t req_bytes;      /* sum of record_bytes over required neurons: what
                              the sparse FFN reads from the slots              */
@@ -255,8 +263,12 @@ m2c_status m2c_cache_plan(m2c_layer* layer, const uint8_t* tier_map, int32_t bat
 
 /* Copy every fill of `plan` from the pinned host store into its slot, on
  * `stream`, by a device gather kernel that reads host memory over the host
- * link. Must run after the plan on the same stream or behind an event, and
- * before the FFN that reads the plan. No host synchronization. */
+ * link. A fill to INT8 / INT4 whose slot holds the neuron's FP16 record
+ * (fill_from == 3) is instead quantized in place from that record, which
+ * gives the bytes of the store's record (both are the group-128 quantization
+ * of the same fp16 values). Must run after the plan on the same stream or
+ * behind an event, and before the FFN that reads the plan. No host
+ * synchronization. */
 m2c_status m2c_cache_fill(m2c_layer* layer, const void* plan, void* stream);
 
 /* y += sum over i in R of silu(<g_i, x>) * <u_i, x> * d_i, per batch row b

@@ -7,7 +7,13 @@
 // no device-to-host round trip is needed to learn what to copy, and the
 // whole step stays on the GPU's queues. One workgroup copies one record at a
 // time with 16-byte loads, four in flight per thread.
-#include "m2c_internal.h"
+//
+// A fill to INT8 / INT4 of a neuron whose slot holds its FP16 record (a
+// neuron that fell out of the FP16 tier) is made on the GPU instead: the
+// workgroup stages the FP16 record's rows in LDS and quantizes them over the
+// record with the create-time quantizer, which yields the store's record byte
+// for byte and takes nothing from the host link.
+#include "quant_device.h"
 
 namespace m2c {
 
@@ -28,9 +34,11 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
                                                             const int32_t* __restrict__ fill_ids,
                                                             const uint8_t* __restrict__ fill_tier,
                                                             const int32_t* __restrict__ fill_slot,
+                                                            const uint8_t* __restrict__ fill_from,
                                                             FillSrc src, uint8_t* __restrict__ slots,
                                                             int64_t slot_bytes, int cap, int d_ff,
-                                                            int n_slots) {
+                                                            int d, int n_slots) {
+  extern __shared__ u32x4 stage[];  // 2 d + 6 d / 128 bytes: one FP16 row and the scales
   int n = counts[M2C_CNT_FILL];
   n = n < 0 ? 0 : n > cap ? cap : n;
   for (int e = blockIdx.x; e < n; e += gridDim.x) {
@@ -38,6 +46,38 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
     const int id = fill_ids[e], slot = fill_slot[e];
     // plans written by m2c_cache_plan always pass; anything else is skipped
     if (t < 1 || t > 3 || id < 0 || id >= d_ff || slot < 0 || slot >= n_slots) continue;
+    if (fill_from[e] == 3 && t < 3) {
+      // Derive in place (uniform over the workgroup), one d-element row at a
+      // time: row v's codes land below byte 2 d (v + 1), which the staged
+      // rows 0..v cover; the scales, which overlap the up row's FP16 bytes
+      // for INT8, are written last.
+      uint8_t* rec = slots + (int64_t)slot * slot_bytes;
+      uint16_t* sc_stage = reinterpret_cast<uint16_t*>(stage + ((2 * d) >> 4));
+      const uint32_t* w = reinterpret_cast<const uint32_t*>(stage);
+      const int G = d >> 7, lane = threadIdx.x & 63;
+      for (int v = 0; v < 3; ++v) {
+        const u32x4* row = reinterpret_cast<const u32x4*>(rec + (int64_t)v * 2 * d);
+        for (int c = threadIdx.x; c < (2 * d) >> 4; c += kFillThreads) stage[c] = row[c];
+        __syncthreads();
+        for (int g = threadIdx.x >> 6; g < G; g += kFillThreads / 64) {  // one wave per group
+          const uint32_t pair = w[g * 64 + lane];
+          const float amax = group_amax(pair);
+          uint16_t sc;
+          if (t == 2)
+            *reinterpret_cast<uint16_t*>(rec + (int64_t)v * d + g * 128 + 2 * lane) =
+                int8_codes(pair, amax, sc);
+          else
+            rec[(int64_t)v * (d / 2) + g * 64 + lane] = int4_codes(pair, amax, sc);
+          if (lane == 0) sc_stage[v * G + g] = sc;
+        }
+        __syncthreads();  // the staging area takes the next row
+      }
+      const int64_t sbase = t == 2 ? 3 * (int64_t)d : 3 * (int64_t)(d / 2);
+      for (int q = threadIdx.x; q < 3 * G; q += kFillThreads)
+        *reinterpret_cast<uint16_t*>(rec + sbase + 2 * q) = sc_stage[q];
+      __syncthreads();  // and the scales the next record's
+      continue;
+    }
     const int64_t bytes = src.stride[t];  // multiple of 16, <= slot_bytes
     const u32x4* s = reinterpret_cast<const u32x4*>(src.host[t] + (int64_t)id * bytes);
     u32x4* dst = reinterpret_cast<u32x4*>(slots + (int64_t)slot * slot_bytes);
@@ -45,14 +85,14 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
     int v = threadIdx.x;
     for (; v + 3 * kFillThreads < nvec; v += 4 * kFillThreads) {
       // host records are read once: non-temporal loads keep them out of the caches
-      const u32x4 a = __builtin_nontemporal_load(s + v);
-      const u32x4 b = __builtin_nontemporal_load(s + v + kFillThreads);
-      const u32x4 c = __builtin_nontemporal_load(s + v + 2 * kFillThreads);
-      const u32x4 d = __builtin_nontemporal_load(s + v + 3 * kFillThreads);
-      dst[v] = a;
-      dst[v + kFillThreads] = b;
-      dst[v + 2 * kFillThreads] = c;
-      dst[v + 3 * kFillThreads] = d;
+      const u32x4 r0 = __builtin_nontemporal_load(s + v);
+      const u32x4 r1 = __builtin_nontemporal_load(s + v + kFillThreads);
+      const u32x4 r2 = __builtin_nontemporal_load(s + v + 2 * kFillThreads);
+      const u32x4 r3 = __builtin_nontemporal_load(s + v + 3 * kFillThreads);
+      dst[v] = r0;
+      dst[v + kFillThreads] = r1;
+      dst[v + 2 * kFillThreads] = r2;
+      dst[v + 3 * kFillThreads] = r3;
     }
     for (; v < nvec; v += kFillThreads) dst[v] = __builtin_nontemporal_load(s + v);
   }
@@ -70,11 +110,13 @@ hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stre
   // CUs and the memory system's request queues to the kernels that overlap.
   int blocks = kFillBlocks;
   if (blocks > L->cap) blocks = L->cap > 0 ? L->cap : 1;
-  hipLaunchKernelGGL(fill_kernel, dim3(blocks), dim3(kFillThreads), 0, stream,
+  const int d = L->desc.d_model;
+  const size_t lds = (size_t)2 * d + 6 * (d / 128);
+  hipLaunchKernelGGL(fill_kernel, dim3(blocks), dim3(kFillThreads), lds, stream,
                      reinterpret_cast<const int32_t*>(plan + lay.counts),
                      reinterpret_cast<const int32_t*>(plan + lay.fill_ids), plan + lay.fill_tier,
-                     reinterpret_cast<const int32_t*>(plan + lay.fill_slot), src, L->slots,
-                     (int64_t)L->info.slot_bytes, L->cap, L->desc.d_ff,
+                     reinterpret_cast<const int32_t*>(plan + lay.fill_slot), plan + lay.fill_from,
+                     src, L->slots, (int64_t)L->info.slot_bytes, L->cap, L->desc.d_ff, d,
                      L->desc.cache_slots + L->S);
   return hipGetLastError();
 }

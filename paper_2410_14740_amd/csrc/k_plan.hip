@@ -33,6 +33,7 @@ struct PlanPtrs {
   int32_t* fill_ids;
   uint8_t* fill_tier;
   int32_t* fill_slot;
+  uint8_t* fill_from;
   int32_t* evicted_ids;
   int32_t* work_slot;
   uint32_t* work_mask;
@@ -51,10 +52,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
                                                             int step, DeviceState st, PlanPtrs P) {
   __shared__ unsigned long long scan64[kPlanThreads / 64 + 1];
   __shared__ uint32_t scan32[kPlanThreads / 64 + 1];
-  __shared__ int sh_hit, sh_refill, sh_empty;
+  __shared__ int sh_hit, sh_refill, sh_empty, sh_der[2];
   const int tid = threadIdx.x;
   if (tid == 0) {
     sh_hit = 0;
+    sh_der[0] = sh_der[1] = 0;
     sh_refill = 0;
     sh_empty = 0;
   }
@@ -120,6 +122,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
         P.req_hit[pos] = same ? 1 : 2;
         P.req_slot[pos] = s;
         st.slot_last[s] = step;
+        st.prev_tier[pos] = st.slot_tier[s];
         if (!same) st.slot_tier[s] = (uint8_t)t;
         hits += same;
         refills += !same;
@@ -216,12 +219,16 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
     P.work_slot[w] = ws;
     P.work_mask[w] = P.req_mask[q];
     if (P.req_hit[q] != 1) {
+      const int from = P.req_hit[q] == 2 ? st.prev_tier[q] : 0;
       P.fill_ids[f] = P.req_ids[q];
       P.fill_tier[f] = P.req_tier[q];
       P.fill_slot[f] = ws;
+      P.fill_from[f] = (uint8_t)from;
+      if (from == 3 && P.req_tier[q] < 3) atomicAdd(&sh_der[P.req_tier[q] - 1], 1);
       ++f;
     }
   }
+  __syncthreads();
   if (tid == 0) {
     const int F3 = (int)(ftot & 0x1fffff), F2 = (int)((ftot >> 21) & 0x1fffff),
               F1 = (int)((ftot >> 42) & 0x1fffff);
@@ -238,6 +245,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
     c[M2C_CNT_REQ_INT4] = N1;
     c[M2C_CNT_FILL_FP16] = F3;
     c[M2C_CNT_FILL_INT8] = F2;
+    c[M2C_CNT_FILL_DERIVED] = sh_der[0] + sh_der[1];
     c[M2C_CNT_FILL_INT4] = F1;
     for (int q = 0; q < M2C_NCOUNTS; ++q) P.counts[q] = c[q];
     *st.lru_cur = 1 - cur;
@@ -257,6 +265,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
     atomicAdd(&st.stats[10], (unsigned long long)N1);
     atomicAdd(&st.stats[11], (unsigned long long)N2);
     atomicAdd(&st.stats[12], (unsigned long long)N3);
+    atomicAdd(&st.stats[13], (unsigned long long)sh_der[1]);  // INT8
+    atomicAdd(&st.stats[14], (unsigned long long)sh_der[0]);  // INT4
   }
 }
 
@@ -331,13 +341,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
   __shared__ uint32_t s_cu[kPJ * kPWaves];            // slot compactions per (chunk, wave)
   __shared__ unsigned long long scan64[kPWaves + 1];
   __shared__ uint32_t scan32[kPWaves + 1];
-  __shared__ int sh_hit, sh_refill, sh_empty, sh_f[4];
+  __shared__ int sh_hit, sh_refill, sh_empty, sh_f[4], sh_der[2];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const unsigned long long lt = (1ull << lane) - 1ull;
   const int NJ = (d_ff + kPlanThreads - 1) / kPlanThreads;
   const int NC = (C + kPlanThreads - 1) / kPlanThreads;
   if (tid == 0) {
     sh_hit = sh_refill = sh_empty = 0;
+    sh_der[0] = sh_der[1] = 0;
     sh_f[0] = sh_f[1] = sh_f[2] = sh_f[3] = 0;
   }
   for (int w = tid; w < (C + 31) / 32; w += kPlanThreads) s_touch[w] = 0;
@@ -420,10 +431,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
       P.req_tier[pos] = (uint8_t)t;
       P.req_mask[pos] = m[g];
       st.work_pos[pos] = wp;
+      int from = 0;
       if (res) {
         P.req_slot[pos] = sl[g];
         P.req_hit[pos] = hit ? 1 : 2;
         st.slot_last[sl[g]] = step;
+        from = st.slot_tier[sl[g]];
         if (!hit) st.slot_tier[sl[g]] = (uint8_t)t;
       } else {
         st.new_pos[fd3(pa, 1) + popc(b1 & lt)] = pos;
@@ -433,6 +446,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
         st.fill_pos[pos] = fr;
         P.fill_ids[fr] = i;
         P.fill_tier[fr] = (uint8_t)t;
+        P.fill_from[fr] = (uint8_t)from;
+        if (from == 3 && t < 3) atomicAdd(&sh_der[t - 1], 1);
       } else {
         st.fill_pos[pos] = -1;
       }
@@ -562,6 +577,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
     c[M2C_CNT_REQ_INT4] = N1;
     c[M2C_CNT_FILL_FP16] = F3;
     c[M2C_CNT_FILL_INT8] = F2;
+    c[M2C_CNT_FILL_DERIVED] = sh_der[0] + sh_der[1];
     c[M2C_CNT_FILL_INT4] = F1;
     for (int q = 0; q < M2C_NCOUNTS; ++q) P.counts[q] = c[q];
     *st.lru_cur = 1 - cur;
@@ -578,6 +594,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
     atomicAdd(&st.stats[10], (unsigned long long)N1);
     atomicAdd(&st.stats[11], (unsigned long long)N2);
     atomicAdd(&st.stats[12], (unsigned long long)N3);
+    atomicAdd(&st.stats[13], (unsigned long long)sh_der[1]);  // INT8
+    atomicAdd(&st.stats[14], (unsigned long long)sh_der[0]);  // INT4
   }
 }
 
@@ -609,6 +627,7 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
   P.fill_ids = reinterpret_cast<int32_t*>(plan + lay.fill_ids);
   P.fill_tier = plan + lay.fill_tier;
   P.fill_slot = reinterpret_cast<int32_t*>(plan + lay.fill_slot);
+  P.fill_from = plan + lay.fill_from;
   P.evicted_ids = reinterpret_cast<int32_t*>(plan + lay.evicted_ids);
   P.work_slot = reinterpret_cast<int32_t*>(plan + lay.work_slot);
   P.work_mask = reinterpret_cast<uint32_t*>(plan + lay.work_mask);

@@ -4,7 +4,7 @@
 // footnote); lower-scored neurons are loaded at lower precision (Sec. 5.2).
 // The INT8 / INT4 copies use symmetric group-128 quantization with fp16
 // scales: s = fp16_rne(fp32(amax) / qmax), q = clamp(rne(w / s)).
-#include "m2c_internal.h"
+#include "quant_device.h"
 
 namespace m2c {
 
@@ -26,20 +26,6 @@ __global__ __launch_bounds__(256) void transpose_u16_kernel(const uint16_t* __re
   }
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
-  return v;
-}
-
-// q = clamp(rne(w / s), -qmax, qmax); 0 when s == 0.
-__device__ __forceinline__ int quant_code(float w, float s, float qmax) {
-  if (s == 0.0f) return 0;
-  float r = rintf(__fdiv_rn(w, s));
-  r = fminf(fmaxf(r, -qmax), qmax);
-  return (int)r;
-}
-
 // One wave per (neuron, vector). Lane l owns elements 2l and 2l+1 of every
 // 128-element group. Records are written into chunk buffers that hold
 // neurons i0 .. i0+n-1 (record index = neuron - i0).
@@ -55,29 +41,19 @@ __global__ __launch_bounds__(64) void quantize_records_kernel(
   const uint16_t* src = (v == 0 ? wg : v == 1 ? wu : wdT) + i * d;
   uint8_t* f16 = r16 + local * st16 + (int64_t)v * 2 * d;
   uint8_t* c8 = r8 + local * st8 + (int64_t)v * d;
-  uint8_t* s8 = r8 + local * st8 + 3 * (int64_t)d + (int64_t)v * 2 * G;
+  uint8_t* s8p = r8 + local * st8 + 3 * (int64_t)d + (int64_t)v * 2 * G;
   uint8_t* c4 = r4 + local * st4 + (int64_t)v * (d / 2);
-  uint8_t* s4 = r4 + local * st4 + 3 * (int64_t)(d / 2) + (int64_t)v * 2 * G;
+  uint8_t* s4p = r4 + local * st4 + 3 * (int64_t)(d / 2) + (int64_t)v * 2 * G;
   for (int g = 0; g < G; ++g) {
     const uint32_t pair = *reinterpret_cast<const uint32_t*>(src + g * 128 + 2 * lane);
     *reinterpret_cast<uint32_t*>(f16 + 2 * (g * 128 + 2 * lane)) = pair;
-    const float w0 = h2f((uint16_t)(pair & 0xffffu));
-    const float w1 = h2f((uint16_t)(pair >> 16));
-    const float amax = wave_max(fmaxf(fabsf(w0), fabsf(w1)));
-    {  // INT8
-      const __half sh = __float2half_rn(__fdiv_rn(amax, 127.0f));
-      const float s = __half2float(sh);
-      const int q0 = quant_code(w0, s, 127.0f), q1 = quant_code(w1, s, 127.0f);
-      *reinterpret_cast<uint16_t*>(c8 + g * 128 + 2 * lane) =
-          (uint16_t)((uint8_t)(int8_t)q0 | ((uint16_t)(uint8_t)(int8_t)q1 << 8));
-      if (lane == 0) *reinterpret_cast<uint16_t*>(s8 + 2 * g) = __half_as_ushort(sh);
-    }
-    {  // INT4
-      const __half sh = __float2half_rn(__fdiv_rn(amax, 7.0f));
-      const float s = __half2float(sh);
-      const int q0 = quant_code(w0, s, 7.0f), q1 = quant_code(w1, s, 7.0f);
-      c4[g * 64 + lane] = (uint8_t)((q0 & 0xf) | ((q1 & 0xf) << 4));
-      if (lane == 0) *reinterpret_cast<uint16_t*>(s4 + 2 * g) = __half_as_ushort(sh);
+    const float amax = group_amax(pair);
+    uint16_t s8, s4b;
+    *reinterpret_cast<uint16_t*>(c8 + g * 128 + 2 * lane) = int8_codes(pair, amax, s8);
+    c4[g * 64 + lane] = int4_codes(pair, amax, s4b);
+    if (lane == 0) {
+      *reinterpret_cast<uint16_t*>(s8p + 2 * g) = s8;
+      *reinterpret_cast<uint16_t*>(s4p + 2 * g) = s4b;
     }
   }
 }

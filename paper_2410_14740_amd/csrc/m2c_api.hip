@@ -124,6 +124,7 @@ void fill_info_layout(m2c_layer* L) {
   P.fill_ids = take(4 * c);
   P.fill_tier = take(c);
   P.fill_slot = take(4 * c);
+  P.fill_from = take(c);
   P.evicted_ids = take(4 * c);
   P.work_slot = take(4 * (c + m2c::kWorkSlotPad));
   P.work_mask = take(4 * c);
@@ -170,7 +171,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_pred_a; void* p_pred_b; void* p_bias; void* p_z; void* p_scores; void* p_slots;
   void* p_h; void* p_ypart; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
-  void* p_vslot; void* p_vold; void* p_fill_pos; void* p_stats; void* p_status;
+  void* p_vslot; void* p_vold; void* p_fill_pos; void* p_prev_tier; void* p_stats; void* p_status;
   void* p_gen; void* p_hw;
   Piece pieces[] = {
       // C resident + S staging slots, then one slot that stays zero: padding
@@ -194,6 +195,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_vslot, cap * 4},
       {&p_vold, cap * 4},
       {&p_fill_pos, cap * 4},
+      {&p_prev_tier, cap},
       {&p_stats, 16 * 8},
       {&p_status, 4},
       {&p_gen, (int64_t)m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus) * 8},
@@ -230,6 +232,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.vict_slot = (int32_t*)p_vslot;
   L->st.vict_old = (int32_t*)p_vold;
   L->st.fill_pos = (int32_t*)p_fill_pos;
+  L->st.prev_tier = (uint8_t*)p_prev_tier;
   L->st.stats = (unsigned long long*)p_stats;
   L->st.status = (int32_t*)p_status;
   L->st.ffn_gen = (unsigned long long*)p_gen;
@@ -528,8 +531,11 @@ m2c_status m2c_layer_stats(const m2c_layer* L, m2c_stats* out) {
   out->req_tier[1] = st[10];
   out->req_tier[2] = st[11];
   out->req_tier[3] = st[12];
+  out->derived[1] = st[13];
+  out->derived[2] = st[14];
   for (int t = 1; t <= 3; ++t) {
     out->fill_bytes += out->fill[t] * L->info.record_bytes[t];
+    out->host_bytes += (out->fill[t] - out->derived[t]) * L->info.record_bytes[t];
     out->req_bytes += out->req_tier[t] * L->info.record_bytes[t];
   }
   return M2C_OK;

@@ -24,6 +24,7 @@ TIER_NONE, TIER_INT4, TIER_INT8, TIER_FP16 = range(4)
 # plan count indices (m2c.h)
 CNT_REQ, CNT_HIT, CNT_REFILL, CNT_NEW, CNT_BYPASS, CNT_EVICT, CNT_FILL = range(7)
 CNT_REQ_FP16, CNT_REQ_INT8, CNT_REQ_INT4, CNT_FILL_FP16, CNT_FILL_INT8, CNT_FILL_INT4 = range(7, 13)
+CNT_FILL_DERIVED = 13
 NCOUNTS = 16
 
 
@@ -53,7 +54,8 @@ class LayerInfo(ctypes.Structure):
 
 
 PLAN_FIELDS = ("counts", "req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "fill_ids",
-               "fill_tier", "fill_slot", "evicted_ids", "work_slot", "work_mask", "total_bytes")
+               "fill_tier", "fill_slot", "fill_from", "evicted_ids", "work_slot", "work_mask",
+               "total_bytes")
 
 
 class PlanLayout(ctypes.Structure):
@@ -64,7 +66,8 @@ class Stats(ctypes.Structure):
     _fields_ = [("plans", ctypes.c_int64), ("req", ctypes.c_int64), ("hit", ctypes.c_int64),
                 ("refill", ctypes.c_int64), ("new_", ctypes.c_int64), ("bypass", ctypes.c_int64),
                 ("evict", ctypes.c_int64), ("fill", ctypes.c_int64 * 4),
-                ("fill_bytes", ctypes.c_int64), ("req_tier", ctypes.c_int64 * 4),
+                ("fill_bytes", ctypes.c_int64), ("derived", ctypes.c_int64 * 4),
+                ("host_bytes", ctypes.c_int64), ("req_tier", ctypes.c_int64 * 4),
                 ("req_bytes", ctypes.c_int64)]
 
 
@@ -299,7 +302,8 @@ class Layer:
                       ("req_slot", np.int32), ("req_mask", np.uint32), ("work_slot", np.int32),
                       ("work_mask", np.uint32)):
             res[f] = arr(f, dt, min(nreq, cap))
-        for f, dt in (("fill_ids", np.int32), ("fill_tier", np.uint8), ("fill_slot", np.int32)):
+        for f, dt in (("fill_ids", np.int32), ("fill_tier", np.uint8), ("fill_slot", np.int32),
+                      ("fill_from", np.uint8)):
             res[f] = arr(f, dt, min(nfill, cap))
         res["evicted_ids"] = arr("evicted_ids", np.int32, min(nev, cap))
         return res

@@ -11,7 +11,7 @@ import oracle
 from paper_2410_14740_amd import m2c
 from paper_2410_14740_amd import workloads as W
 
-from helpers import FFN_TOL, oracle_ffn, r8_errors, say
+from helpers import FFN_TOL, oracle_ffn, r8_errors, say, subset_records
 
 pytestmark = pytest.mark.gpu
 
@@ -82,9 +82,9 @@ def test_predict_and_tiers_bit_exact(name, d, d_ff, r, seed, batch):
 
 def _compare_plan(g, o, step):
     for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "fill_ids",
-                "fill_tier", "fill_slot", "evicted_ids", "work_slot", "work_mask"):
+                "fill_tier", "fill_slot", "fill_from", "evicted_ids", "work_slot", "work_mask"):
         assert np.array_equal(g[key], o[key]), f"step {step}: plan field {key} differs"
-    assert np.array_equal(g["counts"][:13], o["counts"][:13]), f"step {step}: counts differ"
+    assert np.array_equal(g["counts"][:14], o["counts"][:14]), f"step {step}: counts differ"
 
 
 def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flags=0):
@@ -120,6 +120,17 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flag
         assert np.array_equal(key, cache.slot_key[:C])
         assert np.array_equal(stier, cache.slot_tier[:C])
         assert np.array_equal(last, cache.slot_last[:C])
+        # fills made on the GPU from the resident FP16 record: the store's bytes
+        der = [(int(i), int(tr), int(sl)) for i, tr, sl, fr in
+               zip(o["fill_ids"], o["fill_tier"], o["fill_slot"], o["fill_from"])
+               if fr == 3 and tr < 3]
+        if der:
+            recs, row = subset_records(ld, [i for i, _, _ in der])
+            for i, tr, sl in der:
+                nb = L.info.record_bytes[tr]
+                got = m2c.m2c_debug_read_slot(L.handle, sl, nb)
+                assert np.array_equal(got, recs[tr][row[i]][:nb]), \
+                    f"step {t}: derived tier-{tr} record of neuron {i} differs"
         if check_ffn:
             y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"],
                                o["req_mask"] if batch > 1 else None)
@@ -133,8 +144,11 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flag
         steps, stats[0], stats[1], stats[2], stats[3], stats[4], stats[5])
     assert (st.fill[3], st.fill[2], st.fill[1]) == (stats[10], stats[11], stats[12])
     assert (st.req_tier[3], st.req_tier[2], st.req_tier[1]) == (stats[7], stats[8], stats[9])
+    assert st.derived[1] + st.derived[2] == stats[13] and st.derived[3] == 0
+    rb = L.info.record_bytes
+    assert st.host_bytes == st.fill_bytes - st.derived[1] * rb[1] - st.derived[2] * rb[2]
     L.close()
-    return worst
+    return worst, int(stats[13])
 
 
 @pytest.mark.parametrize("flags", [0, m2c.FLAG_DETERMINISTIC_FFN])
@@ -144,14 +158,16 @@ def test_end_to_end_steps(name, d, d_ff, r, seed, flags):
     k = d_ff // 4
     n16, n8 = _counts(k)
     # C < k forces evictions and bypasses every step
-    _run_steps(ld, 10, k, n16, n8, C=(2 * k) // 3, label=f"e2e {name} flags={flags}", flags=flags)
+    _, derived = _run_steps(ld, 10, k, n16, n8, C=(2 * k) // 3, label=f"e2e {name} flags={flags}",
+                            flags=flags)
+    assert derived > 0  # FP16 -> lower-tier refills were made on the GPU and checked
 
 
 def test_tiny_workload_all_steps():
     wl = W.WORKLOADS["tiny"]
     ld = W.workload_layer(wl, 0)
     k, n16, n8 = wl.counts()
-    worst = _run_steps(ld, wl.steps, k, n16, n8, wl.cache_slots(), label="tiny workload")
+    worst, _ = _run_steps(ld, wl.steps, k, n16, n8, wl.cache_slots(), label="tiny workload")
     say(f"tiny workload worst FFN error {worst:.2e}")
 
 
@@ -172,7 +188,7 @@ def test_batched_ffn_shapes(batch, d, d_ff, r):
     ld = W.make_layer(300 + batch, 0, d, d_ff, r, 3, rhos=rhos, zipf_bias=True)
     k = d_ff // 6
     n16, n8 = _counts(k, (1, 5), (3, 10))
-    worst = _run_steps(ld, 3, k, n16, n8, C=k, batch=batch, label=f"batched B={batch}")
+    worst, _ = _run_steps(ld, 3, k, n16, n8, C=k, batch=batch, label=f"batched B={batch}")
     say(f"batched B={batch} worst FFN error {worst:.2e}")
 
 
@@ -215,7 +231,7 @@ def test_batched_llama7b_b8_workload():
     say("7B batch-8 layer: drawing weights")
     ld = W.workload_layer(wl, 0, steps=2)
     k, n16, n8 = wl.counts()
-    worst = _run_steps(ld, 2, k, n16, n8, wl.cache_slots(), batch=wl.batch, label="7B b8")
+    worst, _ = _run_steps(ld, 2, k, n16, n8, wl.cache_slots(), batch=wl.batch, label="7B b8")
     say(f"7B batch-8 worst FFN error {worst:.2e}")
 
 
@@ -318,7 +334,7 @@ def test_llama70b_layer_shape():
     say("70B layer: drawing weights")
     ld = W.workload_layer(wl, 0, steps=3)
     k, n16, n8 = wl.counts()
-    worst = _run_steps(ld, 3, k, n16, n8, wl.cache_slots(), label="70B layer")
+    worst, _ = _run_steps(ld, 3, k, n16, n8, wl.cache_slots(), label="70B layer")
     say(f"70B layer worst FFN error {worst:.2e}")
 
 
@@ -446,5 +462,5 @@ def test_widest_layer_uses_two_kernel_ffn():
     ld = W.make_layer(29, 0, 16384, 600, 32, 2)
     k = 150
     n16, n8 = _counts(k)
-    worst = _run_steps(ld, 2, k, n16, n8, 300, label="d=16384")
+    worst, _ = _run_steps(ld, 2, k, n16, n8, 300, label="d=16384")
     say(f"d=16384 worst FFN error {worst:.2e}")
