@@ -22,7 +22,7 @@
 //                   and added up, so the dequantization stays exact. The
 //                   waves' partials meet in LDS; h_{b,i} = silu(a) * u, zero
 //                   where row b did not select neuron i.
-//   ffn_bdn_kernel  y by column slice and single-tier run of 512 neurons, on
+//   ffn_bdn_kernel  y by column slice and single-tier run of 128 neurons, on
 //                   the VALU: a lane owns 8 columns and keeps one accumulator
 //                   per batch row, so every down byte is loaded once and
 //                   feeds B fused multiply-adds.
@@ -136,12 +136,22 @@ struct GroupA {
 template <int TIER, int NT>
 __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, const uint16_t* x,
                                         const uint16_t* zero_row, const uint8_t* rec,
-                                        const uint16_t* s_scale, float4v (&acc_g)[NT],
+                                        const uint8_t* const (&srec)[4], float4v (&acc_g)[NT],
                                         float4v (&acc_u)[NT]) {
   const int j = lane >> 4, col = lane & 15;
+  // scales of the lane's result rows 4j + i, read with the group's codes
+  const int64_t sbase = TIER == 1 ? 3 * (int64_t)(d >> 1) : 3 * (int64_t)d;
   for (int grp = w; grp < G; grp += kBHWaves) {
     GroupA<TIER> A;
     A.load(rec, d, grp, j);
+    uint32_t sgu[4][2];
+    if (TIER != 3) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        sgu[i][0] = *reinterpret_cast<const uint16_t*>(srec[i] + sbase + 2 * (int64_t)grp);
+        sgu[i][1] = *reinterpret_cast<const uint16_t*>(srec[i] + sbase + 2 * (int64_t)(G + grp));
+      }
+    }
     uint4 xv[NT][4];  // x[n][128 grp + 32 j .. + 32] for the lane's batch column n
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -173,8 +183,8 @@ __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, co
     for (int i = 0; i < 4; ++i) {
       float sg = 1.0f, su = 1.0f;
       if (TIER != 3) {
-        sg = h2f(s_scale[(4 * j + i) * 2 * G + grp]);
-        su = h2f(s_scale[(4 * j + i) * 2 * G + G + grp]);
+        sg = h2f((uint16_t)sgu[i][0]);
+        su = h2f((uint16_t)sgu[i][1]);
       }
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
@@ -191,8 +201,9 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     const int32_t* __restrict__ work_slot, const uint32_t* __restrict__ work_mask,
     const uint8_t* __restrict__ slots, int64_t slot_bytes, int cap, int n_slots,
     float* __restrict__ hB) {
-  extern __shared__ float s_part[];  // [waves][2][16][16 NT], then scales
+  extern __shared__ float s_part[];  // [waves][2][16][16 NT]
   __shared__ int s_slot[16];
+  __shared__ uint32_t s_mask[16];
   int n3, n2, n1;
   work_counts(counts, cap, n3, n2, n1);
   int tier, item0, nitems;
@@ -201,22 +212,18 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
   const int G = d >> 7;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  uint16_t* s_scale = reinterpret_cast<uint16_t*>(s_part + kBHWaves * 2 * 16 * 16 * NT);
   if (threadIdx.x < 16) {
-    const int s = threadIdx.x < nitems ? work_slot[item0 + threadIdx.x] : -1;
-    s_slot[threadIdx.x] = s >= 0 && s < n_slots ? s : n_slots;  // zero slot for padding
-  }
-  __syncthreads();
-  // gate and up scales of the 16 neurons: [16][2G] halves
-  if (tier != 3) {
-    const int64_t sbase = tier == 1 ? 3 * (int64_t)(d >> 1) : 3 * (int64_t)d;
-    for (int t = threadIdx.x; t < 16 * 2 * G; t += kBHThreads) {
-      const uint8_t* rec = slots + (int64_t)s_slot[t / (2 * G)] * slot_bytes;
-      s_scale[t] = *reinterpret_cast<const uint16_t*>(rec + sbase + 2 * (int64_t)(t % (2 * G)));
-    }
+    const bool in = threadIdx.x < nitems;
+    const int s = in ? work_slot[item0 + threadIdx.x] : -1;
+    const bool ok = s >= 0 && s < n_slots;
+    s_slot[threadIdx.x] = ok ? s : n_slots;  // zero slot for padding
+    s_mask[threadIdx.x] = in && ok ? work_mask[item0 + threadIdx.x] : 0u;
   }
   __syncthreads();
   const uint8_t* rec = slots + (int64_t)s_slot[lane & 15] * slot_bytes;
+  const uint8_t* srec[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) srec[i] = slots + (int64_t)s_slot[4 * (lane >> 4) + i] * slot_bytes;
   const uint16_t* zero_row = reinterpret_cast<const uint16_t*>(slots + (int64_t)n_slots * slot_bytes);
   float4v acc_g[NT], acc_u[NT];
 #pragma unroll
@@ -225,11 +232,11 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     acc_u[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
   }
   if (tier == 3)
-    bh_tier<3, NT>(lane, w, d, G, B, x, zero_row, rec, s_scale, acc_g, acc_u);
+    bh_tier<3, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
   else if (tier == 2)
-    bh_tier<2, NT>(lane, w, d, G, B, x, zero_row, rec, s_scale, acc_g, acc_u);
+    bh_tier<2, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
   else
-    bh_tier<1, NT>(lane, w, d, G, B, x, zero_row, rec, s_scale, acc_g, acc_u);
+    bh_tier<1, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
   // partials of the waves -> LDS: [w][gate/up][row][col]
   const int j = lane >> 4, col = lane & 15;
   constexpr int NC = 16 * NT;
@@ -249,16 +256,14 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
       a += s_part[((q * 2 + 0) * 16 + r) * NC + b];
       u += s_part[((q * 2 + 1) * 16 + r) * NC + b];
     }
-    const int it = item0 + r;
-    const bool sel = (work_mask[it] >> b) & 1u;
-    const int s = work_slot[it];
-    hB[(int64_t)b * cap + it] = (sel && s >= 0 && s < n_slots) ? silu_mul(a, u) : 0.0f;
+    // zero where row b did not select neuron r (or its slot is invalid)
+    hB[(int64_t)b * cap + item0 + r] = (s_mask[r] >> b) & 1u ? silu_mul(a, u) : 0.0f;
   }
 }
 
 constexpr int kBDThreads = 256;
 constexpr int kBDRounds = 8;   // rounds of neurons whose loads are in flight together
-constexpr int kBDRun = 512;    // neurons per workgroup (one tier)
+constexpr int kBDRun = 128;    // neurons per workgroup (one tier)
 
 // Run b of a column slice: up to kBDRun consecutive items of one tier.
 __device__ __forceinline__ void bdn_run(int b, int n3, int n2, int n1, int& tier, int& lo, int& hi) {
@@ -454,13 +459,12 @@ hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const ui
   float* hB = reinterpret_cast<float*>(L->ab);  // [batch][cap]
   // tiles of 16 items: at most ceil(cap/16) + 2 for any split into tiers
   const int tiles = (cap + 15) / 16 + 2;
-  const int G = d >> 7;
   if (batch <= 16) {
-    const size_t lds = (size_t)kBHWaves * 2 * 16 * 16 * 4 + (size_t)16 * 2 * G * 2;
+    const size_t lds = (size_t)kBHWaves * 2 * 16 * 16 * 4;
     hipLaunchKernelGGL(ffn_bh_kernel<1>, dim3(tiles), dim3(kBHThreads), lds, stream, x, d, batch,
                        counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
   } else {
-    const size_t lds = (size_t)kBHWaves * 2 * 16 * 32 * 4 + (size_t)16 * 2 * G * 2;
+    const size_t lds = (size_t)kBHWaves * 2 * 16 * 32 * 4;
     hipLaunchKernelGGL(ffn_bh_kernel<2>, dim3(tiles), dim3(kBHThreads), lds, stream, x, d, batch,
                        counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
   }
