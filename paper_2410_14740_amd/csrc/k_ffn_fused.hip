@@ -190,7 +190,6 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
   const uint32_t ud = (uint32_t)d;
   const uint32_t G = ud >> 7;
   if (k.kind == 2) {
-    const int r = tid / kFLPN;
     const uint32_t col = (uint32_t)(k.slice * kFSW + 32 * (tid % kFLPN));
     const bool colok = col < ud;
     const int lnv = k.tier == 3 ? 2 : k.tier == 2 ? 1 : 0;  // log2 loads per neuron and round
