@@ -599,7 +599,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
   }
 }
 
-__global__ void reset_kernel(DeviceState st, int d_ff, int C) {
+__global__ void reset_kernel(DeviceState st, int d_ff, int C, int S) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   const int n = gridDim.x * blockDim.x;
   for (int i = idx; i < d_ff; i += n) st.slot_of[i] = -1;
@@ -610,6 +610,7 @@ __global__ void reset_kernel(DeviceState st, int d_ff, int C) {
     st.lru[s] = s;
     st.lru[C + s] = s;
   }
+  for (int s = idx; s < C + S; s += n) st.slot_have[s] = 0;
   if (idx == 0) *st.lru_cur = 0;
   if (idx < 16) st.stats[idx] = 0;
 }
@@ -646,7 +647,7 @@ hipError_t launch_reset(m2c_layer* L, hipStream_t stream) {
   if (blocks < 1) blocks = 1;
   if (blocks > 1024) blocks = 1024;
   hipLaunchKernelGGL(reset_kernel, dim3(blocks), dim3(256), 0, stream, L->st, L->desc.d_ff,
-                     L->desc.cache_slots);
+                     L->desc.cache_slots, L->S);
   return hipGetLastError();
 }
 

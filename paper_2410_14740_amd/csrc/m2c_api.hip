@@ -171,7 +171,8 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_pred_a; void* p_pred_b; void* p_bias; void* p_z; void* p_scores; void* p_slots;
   void* p_h; void* p_ypart; void* p_slot_of; void* p_slot_key; void* p_slot_tier;
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
-  void* p_vslot; void* p_vold; void* p_fill_pos; void* p_prev_tier; void* p_stats; void* p_status;
+  void* p_vslot; void* p_vold; void* p_fill_pos; void* p_prev_tier; void* p_have; void* p_stats;
+  void* p_status;
   void* p_gen; void* p_hw;
   Piece pieces[] = {
       // C resident + S staging slots, then one slot that stays zero: padding
@@ -196,6 +197,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_vold, cap * 4},
       {&p_fill_pos, cap * 4},
       {&p_prev_tier, cap},
+      {&p_have, C + L->S},
       {&p_stats, 16 * 8},
       {&p_status, 4},
       {&p_gen, (int64_t)m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus) * 8},
@@ -233,6 +235,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.vict_old = (int32_t*)p_vold;
   L->st.fill_pos = (int32_t*)p_fill_pos;
   L->st.prev_tier = (uint8_t*)p_prev_tier;
+  L->st.slot_have = (uint8_t*)p_have;
   L->st.stats = (unsigned long long*)p_stats;
   L->st.status = (int32_t*)p_status;
   L->st.ffn_gen = (unsigned long long*)p_gen;

@@ -283,6 +283,50 @@ def test_k_zero_and_all_equal_scores():
     L.close()
 
 
+def test_fill_twice_and_cache_reset_keep_derived_records_exact():
+    """A fill derived on the GPU quantizes the FP16 bytes in the slot. Running
+    the fill of a plan a second time must not quantize the INT8 / INT4 bytes
+    again (it copies from the store instead), and after a cache reset no slot
+    counts as holding an FP16 record."""
+    ld = W.make_layer(41, 0, 512, 900, 32, 8, rhos=(0.7,))
+    k = 300
+    n16, n8 = _counts(k)
+    L = _layer(ld, k, 250)
+    tiers = torch.empty((1, 900), dtype=torch.uint8, device="cuda")
+    y = torch.empty((1, 512), dtype=torch.float32, device="cuda")
+    checked = 0
+    for rnd in range(2):
+        for t in range(8):
+            say(f"fill twice: round {rnd} step {t}")
+            x = _x16(ld, t)
+            L.predict_rank(x, 1, k, n16, n8, None, tiers)
+            L.cache_plan(tiers, 1, 8 * rnd + t)
+            L.cache_fill()
+            L.cache_fill()  # again, on the same plan
+            y.zero_()
+            L.sparse_ffn(x, 1, y)
+            torch.cuda.synchronize()
+            g = L.read_plan()
+            der = [(int(i), int(tr), int(sl)) for i, tr, sl, fr in
+                   zip(g["fill_ids"], g["fill_tier"], g["fill_slot"], g["fill_from"])
+                   if fr == 3 and tr < 3]
+            if der:
+                recs, row = subset_records(ld, [i for i, _, _ in der])
+                for i, tr, sl in der:
+                    nb = L.info.record_bytes[tr]
+                    got = m2c.m2c_debug_read_slot(L.handle, sl, nb)
+                    assert np.array_equal(got, recs[tr][row[i]][:nb]), \
+                        f"round {rnd} step {t}: tier-{tr} record of neuron {i} differs"
+                checked += len(der)
+            y_ref = oracle_ffn(ld, ld.x[t], g["req_ids"], g["req_tier"])
+            err = r8_errors(y.cpu().numpy()[0], y_ref[0]).max()
+            assert err <= FFN_TOL, f"round {rnd} step {t}: FFN error {err:.3e}"
+        L.reset_cache()
+        torch.cuda.synchronize()
+    assert checked > 0
+    L.close()
+
+
 def test_host_errors_leave_layer_usable():
     ld = W.make_layer(3, 0, 256, 200, 16, 3)
     L = _layer(ld, 50, 60)
