@@ -266,9 +266,10 @@ m2c_status m2c_cache_plan(m2c_layer* layer, const uint8_t* tier_map, int32_t bat
  * link. A fill to INT8 / INT4 whose slot holds the neuron's FP16 record
  * (fill_from == 3) is instead quantized in place from that record, which
  * gives the bytes of the store's record (both are the group-128 quantization
- * of the same fp16 values). Must run after the plan on the same stream or
- * behind an event, and before the FFN that reads the plan. No host
- * synchronization. */
+ * of the same fp16 values); the layer tracks which slots hold FP16 bytes, so
+ * running the fill of a plan again copies instead and gives the same slots.
+ * Must run after the plan on the same stream or behind an event, and before
+ * the FFN that reads the plan. No host synchronization. */
 m2c_status m2c_cache_fill(m2c_layer* layer, const void* plan, void* stream);
 
 /* y += sum over i in R of silu(<g_i, x>) * <u_i, x> * d_i, per batch row b
