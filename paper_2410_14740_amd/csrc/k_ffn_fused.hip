@@ -158,8 +158,13 @@ __device__ __forceinline__ FTask decode(const FMap& m, int t) {
   return k;
 }
 
+// Record data is read once per call: non-temporal loads keep it from
+// evicting what is reused (slot ids, x, h words, scales, the kernel's code).
+// Scales stay normal loads: the lanes and slices of a group share them.
+typedef uint32_t ntv4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 ld16(const uint8_t* p) {
-  return *reinterpret_cast<const uint4*>(p);
+  const ntv4 v = __builtin_nontemporal_load(reinterpret_cast<const ntv4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
 }
 __device__ __forceinline__ uint32_t ld2(const uint8_t* p) {
   return *reinterpret_cast<const uint16_t*>(p);
