@@ -382,6 +382,21 @@ def test_llama70b_layer_shape():
     say(f"70B layer worst FFN error {worst:.2e}")
 
 
+@pytest.mark.parametrize("name", ["llama2-7b", "llama2-13b"])
+def test_llama7b_13b_layer_shapes(name):
+    """One layer at the 7B shape (d 4096, d_ff 11008, rank 256, k 2201 =
+    220/880/1101, C 3302) and at the 13B shape (d 5120 -- not a power of two:
+    padded lanes in every gate/up unit -- d_ff 13824, k 2073 = 414/622/1037,
+    C 2764), batch 1, over four steps: scores, tiers, plans, slot tables and
+    derived records bit-exact, every FFN output within tolerance."""
+    wl = W.WORKLOADS[name]
+    say(f"{name} layer: drawing weights")
+    ld = W.workload_layer(wl, 0, steps=4)
+    k, n16, n8 = wl.counts()
+    worst, _ = _run_steps(ld, 4, k, n16, n8, wl.cache_slots(), label=f"{name} layer")
+    say(f"{name} layer worst FFN error {worst:.2e}")
+
+
 @pytest.mark.parametrize("d,d_ff", [(1024, 2752), (4096, 3000), (8192, 3000)])
 def test_ffn_modes_accumulate_and_determinism(d, d_ff):
     """Both FFN paths add into y; the deterministic path repeats bit for bit
