@@ -54,6 +54,9 @@ def parse_args():
     p.add_argument("--target-workload", default="llama2-70b",
                    help="second isolated sparse-FFN measurement on this layer shape ('' = skip)")
     p.add_argument("--target-layers", type=int, default=8)
+    p.add_argument("--overlap-steps", type=int, default=4,
+                   help="untimed steps after the timed ones with events around every stage, "
+                        "to measure how much of the fill time overlaps compute")
     p.add_argument("--stage-events", action="store_true",
                    help="record HIP events around every fill and FFN of the timed steps (their "
                         "markers add latency to the cross-stream waits; off for the headline)")
@@ -170,6 +173,51 @@ def hold_stream(torch, s, host_seconds):
         start.record(s)
         torch.cuda._sleep(cycles)
     return start
+
+
+def _union(iv):
+    """Sorted, merged list of (start, end) intervals."""
+    out = []
+    for a, b in sorted(iv):
+        if out and a <= out[-1][1]:
+            out[-1] = (out[-1][0], max(out[-1][1], b))
+        else:
+            out.append((a, b))
+    return out
+
+
+def _measure(iv):
+    return sum(b - a for a, b in iv)
+
+
+def _intersect(u, v):
+    """Measure of the intersection of two merged interval lists."""
+    i = j = 0
+    tot = 0.0
+    while i < len(u) and j < len(v):
+        a, b = max(u[i][0], v[j][0]), min(u[i][1], v[j][1])
+        tot += max(0.0, b - a)
+        if u[i][1] < v[j][1]:
+            i += 1
+        else:
+            j += 1
+    return tot
+
+
+def stage_overlap(spans):
+    """From per layer-step events (aux start/end, fill start/end, FFN
+    start/end, all on one clock): the fraction of the fills' busy time during
+    which predict / plan or the FFN was also running, and the fraction of the
+    compute's busy time that ran under a fill."""
+    base = spans[0][0]
+    t = [[base.elapsed_time(e) for e in sp] for sp in spans]
+    fill = _union([(r[2], r[3]) for r in t])
+    comp = _union([(r[0], r[1]) for r in t] + [(r[4], r[5]) for r in t])
+    both = _intersect(fill, comp)
+    return {"fill_time_overlapped_with_compute": both / max(_measure(fill), 1e-12),
+            "compute_time_under_fills": both / max(_measure(comp), 1e-12),
+            "fill_busy_frac_of_span": _measure(fill) / max(t[-1][5] - t[0][0], 1e-12),
+            "layer_steps": len(spans)}
 
 
 def timed_back_to_back(torch, s, calls, host_seconds):
@@ -372,31 +420,47 @@ def main():
     lag = min(2, n_layers)
     timing = []  # (ffn_start, ffn_end, fill_start, fill_end) per timed layer-step
 
-    def step(t, timed):
+    overlap_ev = []  # (aux start, aux end, fill start, fill end, ffn start, ffn end)
+
+    def step(t, timed, spans=False):
         for l in range(n_layers):
             f = t * n_layers + l
             L = layers[l]
             if f - lag >= 0:
                 aux_s.wait_event(ev_ffn[(f - lag) % n_layers])
-            x = x_dev[l, t]
+            x = x_dev[l, t % steps_total]
+            if spans:
+                sp = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+                sp[0].record(aux_s)
             L.predict_rank(x, 1, k, n16, n8, None, tiers[l], stream=aux_s)
             L.cache_plan(tiers[l], 1, t, stream=aux_s)
+            if spans:
+                sp[1].record(aux_s)
             ev_plan[l].record(aux_s)
             copy_s.wait_event(ev_plan[l])
             if timed:
                 ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
                 ev[2].record(copy_s)
+            if spans:
+                sp[2].record(copy_s)
             L.cache_fill(stream=copy_s)
             if timed:
                 ev[3].record(copy_s)
+            if spans:
+                sp[3].record(copy_s)
             ev_fill[l].record(copy_s)
             main_s.wait_event(ev_fill[l])
             if timed:
                 ev[0].record(main_s)
-            L.sparse_ffn(x, 1, y[t, l], stream=main_s)
+            if spans:
+                sp[4].record(main_s)
+            L.sparse_ffn(x, 1, y[t % steps_total, l], stream=main_s)
             if timed:
                 ev[1].record(main_s)
                 timing.append(ev)
+            if spans:
+                sp[5].record(main_s)
+                overlap_ev.append(sp)
             ev_ffn[l].record(main_s)
 
     for t in range(args.warmup):
@@ -409,6 +473,19 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st1 = [L.stats() for L in layers]
+    # A few more steps, untimed, with events around every stage: how much of
+    # the fills' time runs while predict / plan or the FFN runs on another
+    # stream (the events themselves delay the cross-stream waits a little, so
+    # they stay out of the timed steps).
+    # The aux stream (and through the events the other two) is held by a spin
+    # kernel while the host enqueues, so the extra calls do not space the
+    # stages out.
+    if args.overlap_steps:
+        hold_stream(torch, aux_s, 0.03 * args.overlap_steps)
+    for t in range(steps_total, steps_total + args.overlap_steps):
+        step(t, False, spans=True)
+    torch.cuda.synchronize()
+    overlap = stage_overlap(overlap_ev) if overlap_ev else None
 
     ffn_ms = np.array([e[0].elapsed_time(e[1]) for e in timing]) if timing else None
     fill_ms = np.array([e[2].elapsed_time(e[3]) for e in timing]) if timing else None
@@ -483,6 +560,7 @@ def main():
             "derived_MB_per_layer_step": derived_bytes / n_ls / 1e6,
             "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
                       "bypass_rate": bypass / max(reqs, 1)},
+            "overlap": overlap,
         },
         # the step's gather-GEMV (m2c_sparse_ffn: ffn_fused_kernel),
         # algorithmic bytes per call over the per-call time of back-to-back calls
