@@ -13,9 +13,9 @@
 // workgroup stages the FP16 record's rows in LDS and quantizes them over the
 // record with the create-time quantizer, which yields the store's record byte
 // for byte and takes nothing from the host link. The kernel keeps, per slot,
-// the tier of the record bytes it last wrote there, and derives only from
-// bytes that are an FP16 record: a fill run twice on one plan copies the
-// second time instead of quantizing the INT8 / INT4 bytes again.
+// which record (neuron and tier) it last wrote there, and derives only from
+// bytes that are the same neuron's FP16 record: a fill run twice on one plan
+// copies the second time instead of quantizing the INT8 / INT4 bytes again.
 #include "quant_device.h"
 
 namespace m2c {
@@ -38,7 +38,7 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
                                                             const uint8_t* __restrict__ fill_tier,
                                                             const int32_t* __restrict__ fill_slot,
                                                             const uint8_t* __restrict__ fill_from,
-                                                            uint8_t* __restrict__ slot_have,
+                                                            int32_t* __restrict__ slot_rec,
                                                             FillSrc src, uint8_t* __restrict__ slots,
                                                             int64_t slot_bytes, int cap, int d_ff,
                                                             int d, int n_slots) {
@@ -50,9 +50,9 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
     const int id = fill_ids[e], slot = fill_slot[e];
     // plans written by m2c_cache_plan always pass; anything else is skipped
     if (t < 1 || t > 3 || id < 0 || id >= d_ff || slot < 0 || slot >= n_slots) continue;
-    const bool derive = fill_from[e] == 3 && t < 3 && slot_have[slot] == 3;
-    __syncthreads();  // every thread has read slot_have[slot] before it changes
-    if (threadIdx.x == 0) slot_have[slot] = (uint8_t)t;
+    const bool derive = fill_from[e] == 3 && t < 3 && slot_rec[slot] == 4 * id + 3;
+    __syncthreads();  // every thread has read slot_rec[slot] before it changes
+    if (threadIdx.x == 0) slot_rec[slot] = 4 * id + t;
     if (derive) {
       // Derive in place (uniform over the workgroup), one d-element row at a
       // time: row v's codes land below byte 2 d (v + 1), which the staged
@@ -123,8 +123,8 @@ hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stre
                      reinterpret_cast<const int32_t*>(plan + lay.counts),
                      reinterpret_cast<const int32_t*>(plan + lay.fill_ids), plan + lay.fill_tier,
                      reinterpret_cast<const int32_t*>(plan + lay.fill_slot), plan + lay.fill_from,
-                     L->st.slot_have, src, L->slots, (int64_t)L->info.slot_bytes, L->cap, L->desc.d_ff, d,
-                     L->desc.cache_slots + L->S);
+                     L->st.slot_rec, src, L->slots, (int64_t)L->info.slot_bytes, L->cap,
+                     L->desc.d_ff, d, L->desc.cache_slots + L->S);
   return hipGetLastError();
 }
 

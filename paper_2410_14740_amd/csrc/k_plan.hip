@@ -610,7 +610,7 @@ __global__ void reset_kernel(DeviceState st, int d_ff, int C, int S) {
     st.lru[s] = s;
     st.lru[C + s] = s;
   }
-  for (int s = idx; s < C + S; s += n) st.slot_have[s] = 0;
+  for (int s = idx; s < C + S; s += n) st.slot_rec[s] = -1;
   if (idx == 0) *st.lru_cur = 0;
   if (idx < 16) st.stats[idx] = 0;
 }

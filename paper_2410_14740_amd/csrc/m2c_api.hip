@@ -197,7 +197,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_vold, cap * 4},
       {&p_fill_pos, cap * 4},
       {&p_prev_tier, cap},
-      {&p_have, C + L->S},
+      {&p_have, (C + L->S) * 4},
       {&p_stats, 16 * 8},
       {&p_status, 4},
       {&p_gen, (int64_t)m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus) * 8},
@@ -235,7 +235,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.vict_old = (int32_t*)p_vold;
   L->st.fill_pos = (int32_t*)p_fill_pos;
   L->st.prev_tier = (uint8_t*)p_prev_tier;
-  L->st.slot_have = (uint8_t*)p_have;
+  L->st.slot_rec = (int32_t*)p_have;
   L->st.stats = (unsigned long long*)p_stats;
   L->st.status = (int32_t*)p_status;
   L->st.ffn_gen = (unsigned long long*)p_gen;

@@ -46,7 +46,7 @@ struct DeviceState {
   int32_t* vict_old = nullptr;   // [cap] plan scratch
   int32_t* fill_pos = nullptr;   // [cap] plan scratch: fill position of req p (-1 for hits)
   uint8_t* prev_tier = nullptr;  // [cap] plan scratch: tier a REFILL's slot held before the step
-  uint8_t* slot_have = nullptr;  // [C + S] tier of the record bytes in a slot (0: none), kept by the fill
+  int32_t* slot_rec = nullptr;   // [C + S] record a slot's bytes hold, 4 * neuron + tier (-1: none), kept by the fill
   unsigned long long* stats = nullptr;  // [16] cumulative counters
   int32_t* status = nullptr;           // [1] M2C_STATUS_* bits set by kernels
   unsigned long long* ffn_gen = nullptr;  // [ffn_grid] per-workgroup call counters of the one-launch FFN
