@@ -22,6 +22,10 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     # no packed-fp32 instructions in generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the first kernel arguments arrive in SGPRs at wave launch (gfx950), which
+    # saves a dependent scalar load at the start of every workgroup; the code
+    # keeps a loading prologue for runtimes that do not preload
+    "-mllvm", "-amdgpu-kernarg-preload-count=16",
     "-Wall", "-Wno-unused-result", f"-I{os.path.join(ROOT, 'include')}",
 ]
 
