@@ -195,7 +195,7 @@ typedef struct {
   int64_t evicted_ids; /* int32 [cap] evicted neurons in victim order         */
   int64_t work_slot;   /* int32 [cap] R regrouped tier-major (FP16, INT8,
                           INT4), ascending id inside a tier: FFN work order;
-                          256 spare entries follow (read, never used)         */
+                          512 spare entries follow (read, never used)         */
   int64_t work_mask;   /* uint32[cap] row masks in work order                 */
   int64_t total_bytes;
 } m2c_plan_layout;

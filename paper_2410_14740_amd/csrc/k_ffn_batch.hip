@@ -9,7 +9,8 @@
 // With several tokens the gate / up side is a real dense contraction, a
 // gathered (2|R| x d) by (d x B) product, so it runs on the matrix cores:
 //
-//   ffn_bh_kernel   a workgroup takes a tile of 16 neurons of one tier; its 8
+//   ffn_bh_kernel   a workgroup takes a tile of 16 neurons of one tier (8 for
+//                   FP16, padded with the zero slot); its 8
 //                   waves split d by quantization group (group g to wave
 //                   g % 8). For each group a wave issues
 //                   v_mfma_f32_16x16x16f16 over the 128 elements: A = the 16
@@ -22,10 +23,8 @@
 //                   and added up, so the dequantization stays exact. The
 //                   waves' partials meet in LDS; h_{b,i} = silu(a) * u, zero
 //                   where row b did not select neuron i.
-//   ffn_bdn_kernel  y by column slice and single-tier run of 128 neurons, on
-//                   the VALU: a lane owns 8 columns and keeps one accumulator
-//                   per batch row, so every down byte is loaded once and
-//                   feeds B fused multiply-adds.
+//   ffn_bdm_kernel  the down projection, also on the matrix cores, by
+//                   quantization group and single-tier run (below).
 #include "ffn_device.h"
 
 namespace m2c {
@@ -73,14 +72,17 @@ __device__ __forceinline__ half4v i8x4_to_h4(uint32_t w) {
   return r;
 }
 
-// Tile b of 16 consecutive work items of one tier.
+// Tile b: up to 16 consecutive work items of one tier. An FP16 tile takes 8
+// items (the MFMA rows past them read the zero slot), so that it carries about
+// as many record bytes as an INT8 tile of 16 and the workgroups finish
+// together instead of the FP16 tiles trailing.
 __device__ __forceinline__ void bh_tile(int b, int n3, int n2, int n1, int& tier, int& item0,
                                         int& nitems) {
-  const int t3 = (n3 + 15) >> 4, t2 = (n2 + 15) >> 4, t1 = (n1 + 15) >> 4;
+  const int t3 = (n3 + 7) >> 3, t2 = (n2 + 15) >> 4, t1 = (n1 + 15) >> 4;
   if (b < t3) {
     tier = 3;
-    item0 = 16 * b;
-    nitems = min(16, n3 - item0);
+    item0 = 8 * b;
+    nitems = min(8, n3 - item0);
   } else if (b < t3 + t2) {
     tier = 2;
     item0 = 16 * (b - t3);
@@ -261,188 +263,333 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
   }
 }
 
-constexpr int kBDThreads = 256;
-constexpr int kBDRounds = 8;   // rounds of neurons whose loads are in flight together
-constexpr int kBDRun = 128;    // neurons per workgroup (one tier)
+// ---------------------------------------------------------------------------
+// Batched down projection on the matrix cores. The contraction runs over the
+// neurons: for one quantization group of 128 columns,
+//   y[b][c] += sum_n (h[b][n] s[n]) q[n][c],
+// so each neuron's scale folds into the h side and the codes q enter the
+// matrix cores exactly, as fp16. The h side is split into an fp16 high and low
+// part (two MFMAs per tile) after a power-of-two normalisation per wave, which
+// keeps the products at fp32-level precision whatever the magnitudes.
+//
+// Workgroup: one group by a run of one tier; its 8 waves take consecutive
+// parts of the run, in steps of 16 neurons. In a step lane (x, j) (x = lane % 16, j = lane / 16) loads the 8
+// codes at columns 8x .. 8x + 7 of the group from neurons 4j .. 4j + 3; MFMA e
+// (e = 0..7) takes code e of each, so that its 16 result columns are 8x + e,
+// and the lane's A operand is h s of batch row x for the same four neurons.
 
-// Run b of a column slice: up to kBDRun consecutive items of one tier.
-__device__ __forceinline__ void bdn_run(int b, int n3, int n2, int n1, int& tier, int& lo, int& hi) {
-  const int w3 = (n3 + kBDRun - 1) / kBDRun, w2 = (n2 + kBDRun - 1) / kBDRun,
-            w1 = (n1 + kBDRun - 1) / kBDRun;
+constexpr int kDMThreads = 512;
+constexpr int kDMWaves = kDMThreads / 64;
+constexpr int kDMRegions = kDMWaves / 2;  // LDS partial results per workgroup
+#ifndef M2C_DM_STEPS
+#define M2C_DM_STEPS 1
+#endif
+// 16-neuron steps per wave: INT8 runs take twice and INT4 runs four times the
+// FP16 count, so that every workgroup carries the same record bytes (32 KB).
+template <int TIER>
+__host__ __device__ constexpr int dm_steps() {
+  return M2C_DM_STEPS << (3 - TIER);
+}
+template <int TIER>
+__host__ __device__ constexpr int dm_run_len() {
+  return kDMWaves * 16 * dm_steps<TIER>();
+}
+
+// a wave reads slot ids up to one run length past its run's first item
+static_assert(dm_run_len<1>() <= kWorkSlotPad, "runs longer than the plan's spare work_slot entries");
+
+// Run b of a group: up to dm_run_len<tier>() consecutive items of one tier.
+__device__ __forceinline__ void dm_run(int b, int n3, int n2, int n1, int& tier, int& lo, int& hi) {
+  constexpr int R3 = dm_run_len<3>(), R2 = dm_run_len<2>(), R1 = dm_run_len<1>();
+  const int w3 = (n3 + R3 - 1) / R3, w2 = (n2 + R2 - 1) / R2, w1 = (n1 + R1 - 1) / R1;
   if (b < w3) {
     tier = 3;
-    lo = b * kBDRun;
-    hi = min(lo + kBDRun, n3);
+    lo = b * R3;
+    hi = min(lo + R3, n3);
   } else if (b < w3 + w2) {
     tier = 2;
-    lo = n3 + (b - w3) * kBDRun;
-    hi = min(lo + kBDRun, n3 + n2);
+    lo = n3 + (b - w3) * R2;
+    hi = min(lo + R2, n3 + n2);
   } else if (b < w3 + w2 + w1) {
     tier = 1;
-    lo = n3 + n2 + (b - w3 - w2) * kBDRun;
-    hi = min(lo + kBDRun, n3 + n2 + n1);
+    lo = n3 + n2 + (b - w3 - w2) * R1;
+    hi = min(lo + R1, n3 + n2 + n1);
   } else {
     tier = 0;
     lo = hi = 0;
   }
 }
 
-// Down projection of one tier over the run (s_slot / s_h hold its items,
-// s_slot the zero slot past the run) for the lane's 8 columns from `col`.
-// BT: batch rows of this pass (accumulators per lane: BT x 8); LPN lanes per
-// neuron.
-template <int TIER, int BT, int LPN>
-__device__ __forceinline__ void bdn_tier(int nrun, int col, int d, int G, int nb,
-                                         const int* s_slot, const float* s_h, const uint8_t* slots,
-                                         int64_t slot_bytes, float (&acc)[BT][8]) {
-  constexpr int NPR = kBDThreads / LPN;
-  const int r = threadIdx.x / LPN;
-  for (int base = 0; base < nrun; base += NPR * kBDRounds) {
-    uint4 v[kBDRounds];
-    float sc[kBDRounds];
+// The 8 codes of one neuron at the lane's columns: 16 bytes of FP16, 8 of
+// INT8, 4 of INT4.
+template <int TIER>
+struct DmWord {
+  typedef uint32_t T;
+};
+template <>
+struct DmWord<3> {
+  typedef uint4 T;
+};
+template <>
+struct DmWord<2> {
+  typedef uint2 T;
+};
+
+__device__ __forceinline__ uint32_t dm_dword(const uint4& v, int q) {
+  return q == 0 ? v.x : q == 1 ? v.y : q == 2 ? v.z : v.w;
+}
+__device__ __forceinline__ uint32_t dm_dword(const uint2& v, int q) { return q == 0 ? v.x : v.y; }
+
+// B operands of the 8 MFMAs of a step from the codes of the lane's neurons
+// 4j + m (m = 0..3): element m of operand e is code e of neuron m, exact.
+// INT8 / INT4 words arrive in offset binary (code + 128 per byte, code + 8
+// per nibble); ORing the offset code under fp16 exponent 10 gives 1024 +
+// offset code, and one packed subtraction restores the code.
+template <int TIER>
+__device__ __forceinline__ void dm_operands(const typename DmWord<TIER>::T (&c)[4],
+                                            half4v (&bop)[8]) {
+  if constexpr (TIER == 3) {
 #pragma unroll
-    for (int q = 0; q < kBDRounds; ++q) {
-      const int ii = base + q * NPR + r;  // < kBDRun, so s_slot[ii] exists
-      const uint8_t* rec = slots + (int64_t)s_slot[ii] * slot_bytes;
-      if (TIER == 3) {
-        v[q] = *reinterpret_cast<const uint4*>(rec + 4 * (int64_t)d + 2 * (int64_t)col);
-        sc[q] = 1.0f;
-      } else if (TIER == 2) {
-        const uint2 t = *reinterpret_cast<const uint2*>(rec + 2 * (int64_t)d + col);
-        v[q] = make_uint4(t.x, t.y, 0u, 0u);
-        sc[q] = h2f(*reinterpret_cast<const uint16_t*>(rec + 3 * (int64_t)d + 4 * G + 2 * (col >> 7)));
-      } else {
-        const uint32_t t = *reinterpret_cast<const uint32_t*>(rec + (int64_t)d + (col >> 1));
-        v[q] = make_uint4(t, 0u, 0u, 0u);
-        sc[q] = h2f(*reinterpret_cast<const uint16_t*>(rec + 3 * (int64_t)(d >> 1) + 4 * G +
-                                                       2 * (col >> 7)));
-      }
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;  // halves e & 1 of two words
+      const int q = e >> 1;
+      bop[e] = h4(__builtin_amdgcn_perm(dm_dword(c[1], q), dm_dword(c[0], q), sel),
+                  __builtin_amdgcn_perm(dm_dword(c[3], q), dm_dword(c[2], q), sel));
     }
+  } else if constexpr (TIER == 2) {
+    const half4v bias = {(_Float16)1152.0f, (_Float16)1152.0f, (_Float16)1152.0f,
+                         (_Float16)1152.0f};
 #pragma unroll
-    for (int q = 0; q < kBDRounds; ++q) {
-      float wv[8];
-      if (TIER == 3) {
-        const uint32_t ws[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+    for (int e = 0; e < 8; e += 2) {
+      const int q = e >> 2;
+      const uint32_t p = e & 3;
+      // bytes (neuron 0 code e, neuron 1 code e, neuron 0 code e + 1, neuron 1 code e + 1)
+      const uint32_t sel = p | ((4 + p) << 8) | ((p + 1) << 16) | ((5 + p) << 24);
+      const uint32_t t01 = __builtin_amdgcn_perm(dm_dword(c[1], q), dm_dword(c[0], q), sel);
+      const uint32_t t23 = __builtin_amdgcn_perm(dm_dword(c[3], q), dm_dword(c[2], q), sel);
+      bop[e] = h4(__builtin_amdgcn_perm(0x64646464u, t01, 0x04010400u),
+                  __builtin_amdgcn_perm(0x64646464u, t23, 0x04010400u)) -
+               bias;
+      bop[e + 1] = h4(__builtin_amdgcn_perm(0x64646464u, t01, 0x04030402u),
+                      __builtin_amdgcn_perm(0x64646464u, t23, 0x04030402u)) -
+                   bias;
+    }
+  } else {
+    const half4v bias = {(_Float16)1032.0f, (_Float16)1032.0f, (_Float16)1032.0f,
+                         (_Float16)1032.0f};
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          wv[2 * u] = h2f((uint16_t)(ws[u] & 0xffffu));
-          wv[2 * u + 1] = h2f((uint16_t)(ws[u] >> 16));
-        }
-      } else if (TIER == 2) {
-        const uint32_t ws[2] = {v[q].x, v[q].y};
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int bb = 0; bb < 4; ++bb) wv[4 * u + bb] = (float)(int8_t)((ws[u] >> (8 * bb)) & 0xffu);
-      } else {
-#pragma unroll
-        for (int n = 0; n < 8; ++n) {
-          const int nib = (int)((v[q].x >> (4 * n)) & 0xfu);
-          wv[n] = (float)(nib >= 8 ? nib - 16 : nib);
-        }
-      }
-      // items past the run read the zero slot: data 0, scale 0, h 0
-      const int ii = base + q * NPR + r;
-#pragma unroll
-      for (int b = 0; b < BT; ++b) {
-        if (b < nb) {
-          const float c = sc[q] * s_h[b * kBDRun + ii];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[b][e] = fmaf(c, wv[e], acc[b][e]);
-        }
-      }
+    for (int e = 0; e < 8; e += 2) {
+      const uint32_t p = e >> 1;
+      // bytes (neuron 0 byte p, 0, neuron 1 byte p, 0): codes e (low nibbles) and e + 1 (high)
+      const uint32_t sel = p | (0x0cu << 8) | ((4 + p) << 16) | (0x0cu << 24);
+      const uint32_t t01 = __builtin_amdgcn_perm(c[1], c[0], sel);
+      const uint32_t t23 = __builtin_amdgcn_perm(c[3], c[2], sel);
+      bop[e] = h4((t01 & 0x000f000fu) | 0x64006400u, (t23 & 0x000f000fu) | 0x64006400u) - bias;
+      bop[e + 1] = h4(((t01 >> 4) & 0x000f000fu) | 0x64006400u,
+                      ((t23 >> 4) & 0x000f000fu) | 0x64006400u) -
+                   bias;
     }
   }
 }
 
-// SW: slice width (128 or 256 columns); blockIdx.x = slice + n_slices * run.
-template <int BT, int SW>
-__global__ __launch_bounds__(kBDThreads) void ffn_bdn_kernel(
+__device__ __forceinline__ uint4 dm_offset(uint4 v) { return v; }
+__device__ __forceinline__ uint2 dm_offset(uint2 v) {
+  return make_uint2(v.x ^ 0x80808080u, v.y ^ 0x80808080u);
+}
+__device__ __forceinline__ uint32_t dm_offset(uint32_t v) { return v ^ 0x88888888u; }
+
+// One wave's share of a run: neurons [first, first + 16 S) of the run's
+// items, group grp; acc[t][e] gets the lane's D rows 16 t + 4 j + i of MFMA e.
+template <int TIER, int NT>
+__device__ __forceinline__ void dm_wave(int first, int hi, int grp, int d, int G, int B, int cap,
+                                        const int32_t* __restrict__ work_slot,
+                                        const float* __restrict__ hB,
+                                        const uint8_t* __restrict__ slots, int64_t slot_bytes,
+                                        int n_slots, float4v (&acc)[NT][8]) {
+  constexpr int S = dm_steps<TIER>();
+  typedef typename DmWord<TIER>::T Word;
+  const int lane = threadIdx.x & 63, x = lane & 15, j = lane >> 4;
+  // byte offsets in a record: the lane's 8 down codes of group grp, and the group's down scale
+  const int64_t doff = TIER == 3   ? 4 * (int64_t)d + 2 * (128 * grp + 8 * x)
+                       : TIER == 2 ? 2 * (int64_t)d + 128 * grp + 8 * x
+                                   : (int64_t)d + 64 * grp + 4 * x;
+  const int64_t soff = (TIER == 1 ? 3 * (int64_t)(d >> 1) : 3 * (int64_t)d) + 4 * G + 2 * grp;
+  // Every vector load is unconditional (indices clamped into the run and the
+  // batch, values masked afterwards), so that all of them are in flight at
+  // once. The slot ids come first, through the scalar cache: the wave's 16
+  // ids of a step are one wave-uniform range (inside the plan's spare
+  // work_slot entries past the run), and a scalar load does not queue behind
+  // the vector loads of other waves.
+  int sl[S][4];
+  // lane group j takes ids 4 j .. 4 j + 3 of each step (branch-free select)
+  const int mj0 = -(j == 0), mj1 = -(j == 1), mj2 = -(j == 2), mj3 = -(j == 3);
+#pragma unroll
+  for (int st = 0; st < S; ++st) {
+    int u[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) u[k] = __builtin_amdgcn_readfirstlane(work_slot[first + 16 * st + k]);
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+      sl[st][m] = (u[m] & mj0) | (u[4 + m] & mj1) | (u[8 + m] & mj2) | (u[12 + m] & mj3);
+  }
+  float a[S][NT][4];
+#pragma unroll
+  for (int st = 0; st < S; ++st)
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const int idx = min(first + 16 * st + 4 * j + m, hi - 1);
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        a[st][t][m] = hB[(int64_t)min(16 * t + x, B - 1) * cap + idx];
+    }
+  // phase 2: per neuron its group scale and its codes (the zero slot past the run)
+  half2v sc[S][2];  // two fp16 scales per register
+  Word cw[S][4];
+#pragma unroll
+  for (int st = 0; st < S; ++st)
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const int s = first + 16 * st + 4 * j + m < hi ? sl[st][m] : -1;
+      const uint8_t* rec = slots + (int64_t)(s >= 0 && s < n_slots ? s : n_slots) * slot_bytes;
+      if (TIER != 3) sc[st][m >> 1][m & 1] = *reinterpret_cast<const _Float16*>(rec + soff);
+      cw[st][m] = *reinterpret_cast<const Word*>(rec + doff);
+    }
+  __builtin_amdgcn_sched_barrier(0);  // keep every load issued before the first use
+  // h of rows past the batch and of items past the run is 0
+#pragma unroll
+  for (int st = 0; st < S; ++st)
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        if (16 * t + x >= B || first + 16 * st + 4 * j + m >= hi) a[st][t][m] = 0.0f;
+  // A = h s, normalised so that the wave's largest |A| lies in [2^14, 2^15)
+  float mx = 0.0f;
+#pragma unroll
+  for (int st = 0; st < S; ++st)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        if (TIER != 3) a[st][t][m] *= (float)sc[st][m >> 1][m & 1];
+        mx = fmaxf(mx, fabsf(a[st][t][m]));
+      }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  const int E = mx > 0.0f ? 15 - __builtin_amdgcn_frexp_expf(mx) : 0;
+  half4v ahi[S][NT], alo[S][NT];
+#pragma unroll
+  for (int st = 0; st < S; ++st)
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const float v = ldexpf(a[st][t][m], E);
+        const _Float16 h = (_Float16)v;
+        ahi[st][t][m] = h;
+        alo[st][t][m] = (_Float16)(v - (float)h);
+      }
+#pragma unroll
+  for (int st = 0; st < S; ++st) {
+    Word c[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) c[m] = dm_offset(cw[st][m]);
+    half4v bop[8];
+    dm_operands<TIER>(c, bop);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        acc[t][e] = __builtin_amdgcn_mfma_f32_16x16x16f16(ahi[st][t], bop[e], acc[t][e], 0, 0, 0);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+        acc[t][e] = __builtin_amdgcn_mfma_f32_16x16x16f16(alo[st][t], bop[e], acc[t][e], 0, 0, 0);
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[t][e][i] = ldexpf(acc[t][e][i], -E);
+}
+
+// NT: 16-row tiles of the batch (1 for B <= 16, 2 for B <= 32).
+// blockIdx.x = group + G * run.
+template <int NT>
+__global__ __launch_bounds__(kDMThreads) void ffn_bdm_kernel(
     int d, int B, const int32_t* __restrict__ counts, const int32_t* __restrict__ work_slot,
     const float* __restrict__ hB, const uint8_t* __restrict__ slots, int64_t slot_bytes, int cap,
     int n_slots, float* __restrict__ y) {
-  constexpr int LPN = SW / 8;  // lanes per neuron, 8 columns each
-  constexpr int NW = kBDThreads / 64;
-  extern __shared__ float s_mem[];
-  int* s_slot = reinterpret_cast<int*>(s_mem);  // [kBDRun]
-  float* s_h = s_mem + kBDRun;                  // [BT][kBDRun]
-  float* s_row = s_h;                           // [NW][BT][SW], after s_h is read
-  const int n_slices = d / SW;
-  const int slice = blockIdx.x % n_slices;
+  constexpr int kRow = 132;  // 128 columns (in the order 16 e + x) and a pad against bank conflicts
+  // [region][batch row][column]: waves 0..3 store their partial rows, then
+  // waves 4..7 add theirs to them, so that every LDS word has one writer at a
+  // time (LDS float atomics are slow)
+  __shared__ float s_y[kDMRegions][16 * NT][kRow];
+  const int G = d >> 7;
+  const int grp = blockIdx.x % G;
   int n3, n2, n1;
   work_counts(counts, cap, n3, n2, n1);
   int tier, lo, hi;
-  bdn_run(blockIdx.x / n_slices, n3, n2, n1, tier, lo, hi);
+  dm_run(blockIdx.x / G, n3, n2, n1, tier, lo, hi);
   if (lo >= hi) return;  // workgroup-uniform
-  const int G = d >> 7;
-  const int m = threadIdx.x % LPN;
-  const int col = slice * SW + 8 * m;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int nrun = hi - lo;
-  for (int t = threadIdx.x; t < kBDRun; t += kBDThreads) {
-    const int s = t < nrun ? work_slot[lo + t] : -1;
-    s_slot[t] = s >= 0 && s < n_slots ? s : n_slots;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+  float4v acc[NT][8];
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[t][e] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+  if (tier == 3)
+    dm_wave<3, NT>(lo + w * 16 * dm_steps<3>(), hi, grp, d, G, B, cap, work_slot, hB, slots,
+                   slot_bytes, n_slots, acc);
+  else if (tier == 2)
+    dm_wave<2, NT>(lo + w * 16 * dm_steps<2>(), hi, grp, d, G, B, cap, work_slot, hB, slots,
+                   slot_bytes, n_slots, acc);
+  else
+    dm_wave<1, NT>(lo + w * 16 * dm_steps<1>(), hi, grp, d, G, B, cap, work_slot, hB, slots,
+                   slot_bytes, n_slots, acc);
+  const int lane = threadIdx.x & 63, x = lane & 15, j = lane >> 4;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    if (w / kDMRegions == pass) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * t + 4 * j + i;
+          if (row < B) {
+            float* dst = &s_y[w % kDMRegions][row][x];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) dst[16 * e] = pass ? dst[16 * e] + acc[t][e][i] : acc[t][e][i];
+          }
+        }
+    }
+    __syncthreads();
   }
-  for (int b0 = 0; b0 < B; b0 += BT) {
-    const int nb = min(BT, B - b0);
-    for (int t = threadIdx.x; t < BT * kBDRun; t += kBDThreads) {
-      const int b = t / kBDRun, i = t % kBDRun;
-      s_h[t] = b < nb && i < nrun ? hB[(int64_t)(b0 + b) * cap + lo + i] : 0.0f;
-    }
-    __syncthreads();
-    float acc[BT][8];
+  for (int q = threadIdx.x; q < B * 128; q += kDMThreads) {
+    const int b = q >> 7, c = q & 127;
+    float v = 0.0f;
 #pragma unroll
-    for (int b = 0; b < BT; ++b)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[b][e] = 0.0f;
-    if (tier == 3)
-      bdn_tier<3, BT, LPN>(nrun, col, d, G, nb, s_slot, s_h, slots, slot_bytes, acc);
-    else if (tier == 2)
-      bdn_tier<2, BT, LPN>(nrun, col, d, G, nb, s_slot, s_h, slots, slot_bytes, acc);
-    else
-      bdn_tier<1, BT, LPN>(nrun, col, d, G, nb, s_slot, s_h, slots, slot_bytes, acc);
-    // lanes m, m + LPN, ... of a wave share columns; then the waves via LDS
-#pragma unroll
-    for (int off = LPN; off < 64; off <<= 1)
-#pragma unroll
-      for (int b = 0; b < BT; ++b)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[b][e] += __shfl_xor(acc[b][e], off);
-    __syncthreads();  // every wave is done with s_h, which s_row overlays
-    if (lane < LPN) {
-#pragma unroll
-      for (int b = 0; b < BT; ++b)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s_row[(w * BT + b) * SW + 8 * lane + e] = acc[b][e];
-    }
-    __syncthreads();
-    for (int t = threadIdx.x; t < nb * SW; t += kBDThreads) {
-      const int b = t / SW, c = t % SW;
-      float v = s_row[b * SW + c];
-#pragma unroll
-      for (int q = 1; q < NW; ++q) v += s_row[(q * BT + b) * SW + c];
-      atomicAdd(y + (int64_t)(b0 + b) * d + slice * SW + c, v);
-    }
-    __syncthreads();  // s_h and s_row are reused by the next batch chunk
+    for (int r = 0; r < kDMRegions; ++r) v += s_y[r][b][16 * (c & 7) + (c >> 3)];
+    atomicAdd(y + (int64_t)b * d + 128 * grp + c, v);
   }
 }
 
-template <int BT>
-static void launch_bdn(int d, int batch, int cap, hipStream_t stream, const int32_t* counts,
+static void launch_bdm(int d, int batch, int cap, hipStream_t stream, const int32_t* counts,
                        const int32_t* work_slot, const float* hB, const uint8_t* slots,
                        int64_t sb, int n_slots, float* y) {
-  // runs of kBDRun items: at most ceil(cap / kBDRun) + 2 per slice
-  const int runs = (cap + kBDRun - 1) / kBDRun + 2;
-  // 16 batch rows per pass use 128-column slices to stay within 64 KB of LDS
-  const int sw = (d % 256 == 0 && BT <= 8) ? 256 : 128;
-  const int hrow = BT * kBDRun, rrow = (kBDThreads / 64) * BT * sw;
-  const size_t lds = (size_t)(kBDRun + (hrow > rrow ? hrow : rrow)) * 4;
-  if (sw == 256)
-    hipLaunchKernelGGL((ffn_bdn_kernel<BT, 256>), dim3((d / 256) * runs), dim3(kBDThreads), lds,
-                       stream, d, batch, counts, work_slot, hB, slots, sb, cap, n_slots, y);
+  // runs of dm_run_len<tier>() items: at most ceil(cap / R_FP16) + 2 per group
+  constexpr int R3 = dm_run_len<3>();
+  const int runs = (cap + R3 - 1) / R3 + 2;
+  const int G = d >> 7;
+  if (batch <= 16)
+    hipLaunchKernelGGL(ffn_bdm_kernel<1>, dim3(G * runs), dim3(kDMThreads), 0, stream, d, batch,
+                       counts, work_slot, hB, slots, sb, cap, n_slots, y);
   else
-    hipLaunchKernelGGL((ffn_bdn_kernel<BT, 128>), dim3((d / 128) * runs), dim3(kBDThreads), lds,
-                       stream, d, batch, counts, work_slot, hB, slots, sb, cap, n_slots, y);
+    hipLaunchKernelGGL(ffn_bdm_kernel<2>, dim3(G * runs), dim3(kDMThreads), 0, stream, d, batch,
+                       counts, work_slot, hB, slots, sb, cap, n_slots, y);
 }
 
 hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan,
@@ -457,8 +604,8 @@ hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const ui
   const int cap = L->cap;
   if (cap <= 0) return hipSuccess;
   float* hB = reinterpret_cast<float*>(L->ab);  // [batch][cap]
-  // tiles of 16 items: at most ceil(cap/16) + 2 for any split into tiers
-  const int tiles = (cap + 15) / 16 + 2;
+  // tiles of 8 (FP16) and 16 items: at most ceil(cap/8) + 2 for any split into tiers
+  const int tiles = (cap + 7) / 8 + 2;
   if (batch <= 16) {
     const size_t lds = (size_t)kBHWaves * 2 * 16 * 16 * 4;
     hipLaunchKernelGGL(ffn_bh_kernel<1>, dim3(tiles), dim3(kBHThreads), lds, stream, x, d, batch,
@@ -470,10 +617,7 @@ hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const ui
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (batch <= 8)
-    launch_bdn<8>(d, batch, cap, stream, counts, work_slot, hB, L->slots, sb, n_slots, y);
-  else
-    launch_bdn<16>(d, batch, cap, stream, counts, work_slot, hB, L->slots, sb, n_slots, y);
+  launch_bdm(d, batch, cap, stream, counts, work_slot, hB, L->slots, sb, n_slots, y);
   return hipGetLastError();
 }
 

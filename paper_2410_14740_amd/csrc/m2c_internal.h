@@ -13,9 +13,10 @@ namespace m2c {
 // m2c_layer_stats.
 constexpr int M2C_STATUS_PLAN_OVERFLOW = 2;  // a tier map had more active neurons than cap
 constexpr int M2C_STATUS_FFN_WAIT = 4;      // a sparse FFN gave up waiting for an h value
-// Spare entries after the plan's work_slot array: the batch-1 FFN reads a
-// task's slot ids in groups of four that may run past the last item.
-constexpr int kWorkSlotPad = 256;
+// Spare entries after the plan's work_slot array: the FFN kernels read slot
+// ids in wave-uniform blocks (groups of four at batch 1, a whole run of up to
+// 512 items in the batched down projection) that may run past the last item.
+constexpr int kWorkSlotPad = 512;
 
 // ---------------------------------------------------------------------------
 // Host-side layer object
