@@ -134,7 +134,9 @@ struct GroupA {
   }
 };
 
-// NT: 16-column tiles of the batch (1 for B <= 16, 2 for B <= 32).
+// NT: 16-column tiles of the batch (1 for B <= 16, 2 for B <= 32). Pairs of
+// groups with both groups' loads in flight measured slower: they need more
+// than 128 VGPRs, one workgroup per CU.
 template <int TIER, int NT>
 __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, const uint16_t* x,
                                         const uint16_t* zero_row, const uint8_t* rec,
@@ -144,8 +146,7 @@ __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, co
   // scales of the lane's result rows 4j + i, read with the group's codes
   const int64_t sbase = TIER == 1 ? 3 * (int64_t)(d >> 1) : 3 * (int64_t)d;
   for (int grp = w; grp < G; grp += kBHWaves) {
-    GroupA<TIER> A;
-    A.load(rec, d, grp, j);
+    // every load of the group is issued before the first use
     uint32_t sgu[4][2];
     if (TIER != 3) {
 #pragma unroll
@@ -163,6 +164,9 @@ __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, co
       for (int e = 0; e < 4; ++e)
         xv[t][e] = *reinterpret_cast<const uint4*>(xr + 128 * grp + 32 * j + 8 * e);
     }
+    GroupA<TIER> A;
+    A.load(rec, d, grp, j);
+    __builtin_amdgcn_sched_barrier(0);
     float4v tg[NT], tu[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -204,7 +208,6 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     const uint8_t* __restrict__ slots, int64_t slot_bytes, int cap, int n_slots,
     float* __restrict__ hB) {
   extern __shared__ float s_part[];  // [waves][2][16][16 NT]
-  __shared__ int s_slot[16];
   __shared__ uint32_t s_mask[16];
   int n3, n2, n1;
   work_counts(counts, cap, n3, n2, n1);
@@ -214,18 +217,26 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
   const int G = d >> 7;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (threadIdx.x < 16) {
-    const bool in = threadIdx.x < nitems;
-    const int s = in ? work_slot[item0 + threadIdx.x] : -1;
-    const bool ok = s >= 0 && s < n_slots;
-    s_slot[threadIdx.x] = ok ? s : n_slots;  // zero slot for padding
-    s_mask[threadIdx.x] = in && ok ? work_mask[item0 + threadIdx.x] : 0u;
-  }
-  __syncthreads();
-  const uint8_t* rec = slots + (int64_t)s_slot[lane & 15] * slot_bytes;
-  const uint8_t* srec[4];
+  // The tile's slot ids by scalar loads (a wave-uniform range, inside the
+  // plan's spare work_slot entries past the list), which do not queue behind
+  // other workgroups' vector loads; each lane then picks the ids it needs with
+  // branch-free masks.
+  int u[16];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) srec[i] = slots + (int64_t)s_slot[4 * (lane >> 4) + i] * slot_bytes;
+  for (int k = 0; k < 16; ++k) {
+    const int s = __builtin_amdgcn_readfirstlane(work_slot[item0 + k]);
+    u[k] = k < nitems && s >= 0 && s < n_slots ? s : n_slots;  // zero slot for padding
+  }
+  int my_slot = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) my_slot |= u[k] & -((lane & 15) == k);
+  const uint32_t my_mask = work_mask[min(item0 + (lane & 15), cap - 1)];  // stored after the main loop
+  const uint8_t* rec = slots + (int64_t)my_slot * slot_bytes;
+  const uint8_t* srec[4];
+  const int q = lane >> 4, mq0 = -(q == 0), mq1 = -(q == 1), mq2 = -(q == 2), mq3 = -(q == 3);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    srec[i] = slots + (int64_t)((u[i] & mq0) | (u[4 + i] & mq1) | (u[8 + i] & mq2) | (u[12 + i] & mq3)) * slot_bytes;
   const uint16_t* zero_row = reinterpret_cast<const uint16_t*>(slots + (int64_t)n_slots * slot_bytes);
   float4v acc_g[NT], acc_u[NT];
 #pragma unroll
@@ -239,6 +250,7 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     bh_tier<2, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
   else
     bh_tier<1, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
+  if (threadIdx.x < 16) s_mask[threadIdx.x] = my_slot < n_slots ? my_mask : 0u;
   // partials of the waves -> LDS: [w][gate/up][row][col]
   const int j = lane >> 4, col = lane & 15;
   constexpr int NC = 16 * NT;
