@@ -180,16 +180,33 @@ def test_batched_plan_union_and_bypass():
     _run_steps(ld, 6, k, n16, n8, C=200, batch=4, label="batched plan")
 
 
-@pytest.mark.parametrize("batch,d,d_ff,r", [(2, 1024, 1000, 64), (20, 512, 900, 32)])
+@pytest.mark.parametrize("batch,d,d_ff,r", [(2, 1024, 1000, 64), (16, 256, 600, 32),
+                                             (17, 256, 600, 32), (20, 512, 900, 32),
+                                             (32, 384, 700, 48)])
 def test_batched_ffn_shapes(batch, d, d_ff, r):
-    """Batch 2 (one MFMA column tile, one down pass) and batch 20 (two column
-    tiles, two down passes of up to 16 rows), mixed tiers, C below the union."""
+    """Batch 2 and 16 (one 16-row MFMA batch tile), 17, 20 and 32 (two tiles;
+    32 is the largest batch), an odd number of quantization groups (d 384),
+    mixed tiers, C below the union."""
     rhos = tuple(0.5 + 0.45 * (b % 2) for b in range(batch))
     ld = W.make_layer(300 + batch, 0, d, d_ff, r, 3, rhos=rhos, zipf_bias=True)
     k = d_ff // 6
     n16, n8 = _counts(k, (1, 5), (3, 10))
     worst, _ = _run_steps(ld, 3, k, n16, n8, C=k, batch=batch, label=f"batched B={batch}")
     say(f"batched B={batch} worst FFN error {worst:.2e}")
+
+
+@pytest.mark.parametrize("scale_exp", [-8, 6])
+def test_batched_ffn_input_scale(scale_exp):
+    """x scaled by 2^-8 (h about 2^-16 of its usual size) and by 2^6: the
+    batched down projection normalises h s per wave before splitting it into
+    fp16 parts, so the error stays within tolerance at any magnitude."""
+    ld = W.make_layer(410, 0, 512, 900, 32, 3, rhos=(0.5, 0.95, 0.9, 0.7, 0.6, 0.8, 0.95, 0.5),
+                      zipf_bias=True)
+    ld.x = (ld.x.astype(np.float32) * np.float32(2.0 ** scale_exp)).astype(np.float16)
+    k = 150
+    n16, n8 = _counts(k, (1, 5), (3, 10))
+    worst, _ = _run_steps(ld, 2, k, n16, n8, C=k, batch=8, label=f"batched x*2^{scale_exp}")
+    say(f"batched x*2^{scale_exp} worst FFN error {worst:.2e}")
 
 
 def test_batched_all_fp16_equals_single_token():
