@@ -278,10 +278,11 @@ m2c_status m2c_cache_fill(m2c_layer* layer, const void* plan, void* stream);
  * stream); zero y first for the plain FFN output.
  *   x dev fp16 [batch][d_model];  y dev fp32 [batch][d_model], in/out.
  * `batch` (1..max_batch) must equal the batch given to the plan. Batch 1 is a
- * gather-dequant GEMV; larger batches run the gate / up contraction on the
- * matrix cores (fp16 operands: the codes, exact, and x; fp32 accumulation,
- * group scales applied in fp32) and are never bit-deterministic (the
- * deterministic flag applies to batch 1). */
+ * gather-dequant GEMV; larger batches run both contractions on the matrix
+ * cores with fp32 accumulation: gate / up with the codes (exact as fp16) and
+ * x, group scales applied in fp32; down with the codes and h times the group
+ * scale, the latter split into an fp16 high and low part. They are never
+ * bit-deterministic (the deterministic flag applies to batch 1). */
 m2c_status m2c_sparse_ffn(m2c_layer* layer, const uint16_t* x, int32_t batch, const void* plan,
                           float* y, void* stream);
 
