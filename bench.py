@@ -68,6 +68,9 @@ def parse_args():
     p.add_argument("--batch-sweep", action="store_true",
                    help="only the batched-decode workload (7B-shaped layer, batch 8): LRU capacity "
                         "10/30/60%% x tiers 10/40/50 or all FP16, one JSON line")
+    p.add_argument("--sweep-point", default="", metavar="CAP:MIX",
+                   help="with --batch-sweep: only this point, e.g. 0.3:10/40/50 or 0.1:fp16 (for "
+                        "counter runs that need one configuration)")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MB",
                    help="only copy a buffer of this many MB device to device, 5 times "
                         "(a plain copy kernel of known size, to scale HBM counters)")
@@ -287,13 +290,14 @@ def ffn_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
             "frac_of_peak": nbytes / avg / 1e9 / PEAK_HBM_GBPS, "host_hidden": bool(covered)}
 
 
-def batched_sweep(steps, warmup, torch, m2c, W):
+def batched_sweep(steps, warmup, torch, m2c, W, only=None):
     """The batched-decode workload: one 7B-shaped layer, batch 8 (rows with
     rho 0.5 and 0.95, log-Zipf neuron popularity), predict -> plan -> fill ->
     batched FFN per step on one stream, for LRU capacity 10 / 30 / 60 % of
     d_ff and tiers 10/40/50 or all FP16. Per point: step time, tokens/s
     (batch rows per second), the union's size and hit rate, fill traffic and
-    the FFN's algorithmic bytes over its time."""
+    the FFN's algorithmic bytes over its time. `only` = (capacity fraction,
+    tier mix) restricts the sweep to that point."""
     wl = W.WORKLOADS["llama2-7b-b8"]
     B = wl.batch
     k, n16_m, n8_m = wl.counts()
@@ -306,6 +310,8 @@ def batched_sweep(steps, warmup, torch, m2c, W):
     owner, points = None, []
     for cap in (F(1, 10), F(3, 10), F(3, 5)):
         for mix in ("10/40/50", "fp16"):
+            if only is not None and (cap, mix) != only:
+                continue
             n16, n8 = (n16_m, n8_m) if mix != "fp16" else (k, 0)
             C = int(d_ff * cap // 1)
             desc = m2c.make_desc(d, d_ff, wl.pred_rank, k, C, max_batch=B)
@@ -386,8 +392,12 @@ def main():
         return
     ffn_flags = m2c.FLAG_DETERMINISTIC_FFN if args.deterministic_ffn else 0
     if args.batch_sweep:
+        only = None
+        if args.sweep_point:
+            cap_s, mix = args.sweep_point.split(":")
+            only = (F(cap_s), mix)
         print(json.dumps({"batched_sweep": batched_sweep(min(args.steps, 56), args.warmup, torch,
-                                                          m2c, W)}), flush=True)
+                                                          m2c, W, only)}), flush=True)
         return
     if args.only_ffn:
         wl_f = W.WORKLOADS[args.only_ffn]

@@ -540,7 +540,15 @@ __global__ __launch_bounds__(kDMThreads) void ffn_bdm_kernel(
   // time (LDS float atomics are slow)
   __shared__ float s_y[kDMRegions][16 * NT][kRow];
   const int G = d >> 7;
-  const int grp = blockIdx.x % G;
+  int grp = blockIdx.x % G;
+  // Groups 2i and 2i + 1 of a run go to workgroup ids 8 apart: one XCD (ids
+  // are dealt to the 8 XCDs in turn) and about the same start, so that a
+  // 128-byte line of INT4 codes, which holds both groups of a neuron, is
+  // fetched into that XCD's L2 once.
+  if ((G & 15) == 0) {
+    const int p = grp & 15;
+    grp = (grp & ~15) + 2 * (p & 7) + (p >> 3);
+  }
   int n3, n2, n1;
   work_counts(counts, cap, n3, n2, n1);
   int tier, lo, hi;

@@ -7,6 +7,9 @@ profiles/, and read the counter figures back for bench.py.
         --copy-fetch ... --copy-write ... --copy-bytes B --out profiles/NAME.md
     python -m paper_2410_14740_amd.rocprof_summary stats --name NAME --command CMD \
         --stats DIR/PREFIX_kernel_stats.csv --out profiles/NAME.md
+    python -m paper_2410_14740_amd.rocprof_summary kernels --name NAME --command CMD \
+        --kernel NAME1 --kernel NAME2 --trace ... --fetch ... --write ... \
+        --copy-fetch ... --copy-write ... --copy-bytes B --algorithmic-bytes A --out profiles/NAME.md
 
 The FFN summary holds the average duration of each sparse-FFN kernel over the
 last N back-to-back calls of the trace, the HBM bytes per call from the
@@ -96,6 +99,42 @@ def ffn_summary(a) -> str:
     return "\n".join(lines)
 
 
+def kernels_summary(a) -> str:
+    """Average duration and HBM-side bytes per dispatch of the named kernels
+    (one dispatch of each per step), against the step's algorithmic bytes."""
+    names = a.kernel
+    dur = collections.defaultdict(list)
+    for r in csv.DictReader(open(a.trace)):
+        for k in names:
+            if k in r["Kernel_Name"]:
+                dur[k].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    fetch = _per_kernel_counter(a.fetch, names)
+    write = _per_kernel_counter(a.write, names)
+    cf = a.copy_bytes / 1024.0 / _copy_counter(a.copy_fetch)
+    cw = a.copy_bytes / 1024.0 / _copy_counter(a.copy_write)
+    lines = [f"# {a.name}", "", a.description, "",
+             "Commands (from the repository root, on one MI355X):", ""]
+    lines += [f"    {c}" for c in a.command]
+    lines += ["", "| Kernel | Dispatches | Avg duration (us) | FETCH_SIZE (KiB/dispatch) | WRITE_SIZE (KiB/dispatch) "
+              "| HBM-side MB/dispatch |", "|---|---|---|---|---|---|"]
+    total, total_us = 0.0, 0.0
+    for k in names:
+        mb = (fetch.get(k, 0.0) * cf + write.get(k, 0.0) * cw) * 1024 / 1e6
+        us = sum(dur[k]) / len(dur[k]) if dur[k] else 0.0
+        total += mb
+        total_us += us
+        lines.append(f"| `{k}` | {len(dur[k])} | {us:.2f} | {fetch.get(k, 0.0):.1f} | {write.get(k, 0.0):.1f} "
+                     f"| {mb:.2f} |")
+    alg = a.algorithmic_bytes / 1e6
+    lines += ["",
+              f"* Counter scale from a {a.copy_bytes / 2**20:.0f} MiB device copy: FETCH_SIZE x{cf:.3f}, "
+              f"WRITE_SIZE x{cw:.3f}.",
+              f"* Per step: {total:.2f} MB HBM-side against {alg:.2f} MB algorithmic ({total / alg:.3f}x), "
+              f"{total_us:.1f} us in these kernels: {a.algorithmic_bytes / (total_us * 1e3):.0f} GB/s "
+              f"algorithmic.", ""]
+    return "\n".join(lines)
+
+
 def stats_summary(a) -> str:
     rows = list(csv.DictReader(open(a.stats)))
     lines = [f"# {a.name}", "", a.description, "", "Command (from the repository root, on one MI355X):", ""]
@@ -134,13 +173,21 @@ def main():
     f.add_argument("--algorithmic-bytes", type=int, required=True)
     f.add_argument("--command", action="append", required=True)
     f.add_argument("--description", default="")
+    kp = sub.add_parser("kernels")
+    for n in ("--name", "--trace", "--fetch", "--write", "--copy-fetch", "--copy-write", "--out"):
+        kp.add_argument(n, required=True)
+    kp.add_argument("--kernel", action="append", required=True)
+    kp.add_argument("--copy-bytes", type=int, required=True)
+    kp.add_argument("--algorithmic-bytes", type=int, required=True)
+    kp.add_argument("--command", action="append", required=True)
+    kp.add_argument("--description", default="")
     s = sub.add_parser("stats")
     for n in ("--stats", "--out", "--name"):
         s.add_argument(n, required=True)
     s.add_argument("--command", action="append", required=True)
     s.add_argument("--description", default="")
     a = p.parse_args()
-    text = ffn_summary(a) if a.mode == "ffn" else stats_summary(a)
+    text = {"ffn": ffn_summary, "kernels": kernels_summary, "stats": stats_summary}[a.mode](a)
     with open(a.out, "w") as fh:
         fh.write(text)
     print(text)
