@@ -285,10 +285,11 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
 // keeps the products at fp32-level precision whatever the magnitudes.
 //
 // Workgroup: one group by a run of one tier; its 8 waves take consecutive
-// parts of the run, in steps of 16 neurons. In a step lane (x, j) (x = lane % 16, j = lane / 16) loads the 8
-// codes at columns 8x .. 8x + 7 of the group from neurons 4j .. 4j + 3; MFMA e
-// (e = 0..7) takes code e of each, so that its 16 result columns are 8x + e,
-// and the lane's A operand is h s of batch row x for the same four neurons.
+// parts of the run, in steps of 16 neurons. In a step lane (x, j)
+// (x = lane % 16, j = lane / 16) loads the 8 codes at columns 8x .. 8x + 7 of
+// the group from neurons 4j .. 4j + 3; MFMA e (e = 0..7) takes code e of
+// each, so that its 16 result columns are 8x + e, and the lane's A operand is
+// h s of batch row x for the same four neurons.
 
 constexpr int kDMThreads = 512;
 constexpr int kDMWaves = kDMThreads / 64;
