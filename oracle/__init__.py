@@ -39,7 +39,7 @@ def build(force: bool = False) -> str:
         tmp = _LIB + f".tmp{os.getpid()}"
         subprocess.run(
             ["gcc", "-O2", "-std=c99", "-Wall", "-ffp-contract=off", "-fno-fast-math",
-             "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"],
+             "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"],
             check=True,
         )
         os.replace(tmp, _LIB)
@@ -62,9 +62,11 @@ def _load():
             "orc_dequant_record": (I, [I, I, P, P, P, P]),
             "orc_predict": (I, [I, I, I, P, P, P, P, P, P]),
             "orc_select_tiers": (I, [I, P, I, I, I, P, P]),
-            "orc_lru_plan": (I, [I, I, I, I, P, I] + [P] * 4 + [P] * 13),
+            "orc_lru_plan": (I, [I, I, I, I, P, I, I] + [P] * 4 + [P] * 11),
             "orc_sparse_ffn": (I, [I, I, I, P, P, P, P, I64, P, I64, P, I64, P, P]),
             "orc_dense_ffn": (I, [I, I, P, P, P, P, P]),
+            "orc_set_threads": (None, [I]),
+            "orc_get_threads": (I, []),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -72,6 +74,16 @@ def _load():
             fn.argtypes = args
         _lib = lib
     return _lib
+
+
+def set_threads(n: int):
+    """Threads the oracle's loops may use (1 = the serial program). Results
+    do not depend on it: threads only split independent sums."""
+    _load().orc_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(_load().orc_get_threads())
 
 
 def _p(a):
@@ -156,11 +168,17 @@ def select_tiers(s, k: int, n16: int, n8: int):
     return tier, ranked[:k]
 
 
-class LRUCache:
-    """Step-atomic LRU slot cache of one layer (C resident + S staging slots)."""
+POLICY_EXACT = 0      # a hit needs the resident tier to equal the requested one
+POLICY_DOMINANCE = 1  # a resident tier at or above the requested one is a hit
 
-    def __init__(self, d_ff: int, C: int, S: int):
-        self.d_ff, self.C, self.S = d_ff, C, S
+
+class LRUCache:
+    """Step-atomic LRU slot cache of one layer (C resident + S staging slots).
+    policy: POLICY_EXACT or POLICY_DOMINANCE (how a resident neuron at
+    another tier than the requested one is treated)."""
+
+    def __init__(self, d_ff: int, C: int, S: int, policy: int = POLICY_EXACT):
+        self.d_ff, self.C, self.S, self.policy = d_ff, C, S, policy
         self.slot_of = np.full(d_ff, -1, np.int32)
         self.slot_key = np.full(max(C, 1), -1, np.int32)
         self.slot_tier = np.zeros(max(C, 1), np.uint8)
@@ -179,23 +197,20 @@ class LRUCache:
             req_hit=np.zeros(n, np.uint8), req_slot=np.zeros(n, np.int32),
             req_mask=np.zeros(n, np.uint32), fill_ids=np.zeros(n, np.int32),
             fill_tier=np.zeros(n, np.uint8), fill_slot=np.zeros(n, np.int32),
-            fill_from=np.zeros(n, np.uint8),
-            evicted_ids=np.zeros(n, np.int32), work_slot=np.zeros(n, np.int32),
-            work_mask=np.zeros(n, np.uint32),
+            fill_from=np.zeros(n, np.uint8), evicted_ids=np.zeros(n, np.int32),
         )
         rc = _load().orc_lru_plan(
-            d_ff, self.C, self.S, B, _p(tm), int(step),
+            d_ff, self.C, self.S, B, _p(tm), int(step), int(self.policy),
             _p(self.slot_of), _p(self.slot_key), _p(self.slot_tier), _p(self.slot_last),
             _p(counts), _p(out["req_ids"]), _p(out["req_tier"]), _p(out["req_hit"]),
             _p(out["req_slot"]), _p(out["req_mask"]), _p(out["fill_ids"]), _p(out["fill_tier"]),
             _p(out["fill_slot"]), _p(out["fill_from"]), _p(out["evicted_ids"]),
-            _p(out["work_slot"]), _p(out["work_mask"]),
         )
         if rc != 0:
             raise RuntimeError(f"orc_lru_plan failed ({rc})")
         nreq, nfill, nev = int(counts[0]), int(counts[6]), int(counts[5])
         res = {"counts": counts}
-        for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "work_slot", "work_mask"):
+        for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask"):
             res[key] = out[key][:nreq].copy()
         for key in ("fill_ids", "fill_tier", "fill_slot", "fill_from"):
             res[key] = out[key][:nfill].copy()

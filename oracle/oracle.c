@@ -9,14 +9,37 @@
  * It shares no code with the HIP library: every step below is written out
  * from its definition, in loops, in the order the definition gives.
  *
- * Build: gcc -O2 -std=c99 -ffp-contract=off -fPIC -shared oracle.c -lm
+ * Build: gcc -O2 -std=c99 -ffp-contract=off -fopenmp -fPIC -shared oracle.c -lm
  * (no fast-math and no FMA contraction: every fused multiply-add below is an
- * explicit fmaf call).
+ * explicit fmaf call). OpenMP only splits independent results over threads:
+ * every dot product and every output element is still one sum taken in the
+ * order its definition gives, so the results do not depend on the thread
+ * count.
  */
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Threads the oracle may use (1 = the serial program). */
+void orc_set_threads(int n) {
+#ifdef _OPENMP
+  omp_set_num_threads(n > 0 ? n : 1);
+#else
+  (void)n;
+#endif
+}
+
+int orc_get_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
 
 /* ------------------------------------------------------------------------ */
 /* IEEE binary16 <-> binary32, written from the format definition.           */
@@ -107,8 +130,11 @@ int orc_build_records(int d, int d_ff, const uint16_t* w_gate, const uint16_t* w
   if (d <= 0 || d % 128 != 0 || d_ff <= 0 || tier < 1 || tier > 3) return -1;
   if (stride < orc_record_bytes(d, tier)) return -1;
   int G = d / 128;
+#pragma omp parallel
+  {
   float* vec = (float*)malloc(sizeof(float) * d);
   int* q = (int*)malloc(sizeof(int) * d);
+#pragma omp for schedule(dynamic, 16)
   for (int i = 0; i < d_ff; i++) {
     uint8_t* rec = out + (int64_t)i * stride;
     memset(rec, 0, (size_t)stride);
@@ -149,38 +175,44 @@ int orc_build_records(int d, int d_ff, const uint16_t* w_gate, const uint16_t* w
   }
   free(vec);
   free(q);
+  }
   return 0;
+}
+
+/* Exact dequantized values of elements [j0, j0 + n) of vector v (0 gate,
+ * 1 up, 2 down) of one record. */
+static void dequant_part(int d, int tier, const uint8_t* rec, int v, int j0, int n, double* out) {
+  int G = d / 128;
+  for (int j = j0; j < j0 + n; j++) {
+    double val;
+    if (tier == 3) {
+      const uint8_t* p = rec + (int64_t)v * 2 * d + 2 * j;
+      val = orc_f16_to_f32((uint16_t)(p[0] | (p[1] << 8)));
+    } else {
+      int64_t codes_bytes = (tier == 2) ? d : d / 2;
+      const uint8_t* codes = rec + v * codes_bytes;
+      const uint8_t* sc = rec + 3 * codes_bytes + (int64_t)v * 2 * G + 2 * (j / 128);
+      double sv = orc_f16_to_f32((uint16_t)(sc[0] | (sc[1] << 8)));
+      int q;
+      if (tier == 2) {
+        q = (int8_t)codes[j];
+      } else {
+        int nib = (j % 2 == 0) ? (codes[j / 2] & 0xf) : (codes[j / 2] >> 4);
+        q = (nib >= 8) ? nib - 16 : nib;
+      }
+      val = q * sv;
+    }
+    out[j - j0] = val;
+  }
 }
 
 /* Exact dequantized values (q * s, or the fp16 value) of one record. */
 int orc_dequant_record(int d, int tier, const uint8_t* rec, double* gate, double* up,
                        double* down) {
   if (d <= 0 || d % 128 != 0 || tier < 1 || tier > 3) return -1;
-  int G = d / 128;
-  double* outs[3] = {gate, up, down};
-  for (int v = 0; v < 3; v++) {
-    for (int j = 0; j < d; j++) {
-      double val;
-      if (tier == 3) {
-        const uint8_t* p = rec + (int64_t)v * 2 * d + 2 * j;
-        val = orc_f16_to_f32((uint16_t)(p[0] | (p[1] << 8)));
-      } else {
-        int64_t codes_bytes = (tier == 2) ? d : d / 2;
-        const uint8_t* codes = rec + v * codes_bytes;
-        const uint8_t* sc = rec + 3 * codes_bytes + (int64_t)v * 2 * G + 2 * (j / 128);
-        double s = orc_f16_to_f32((uint16_t)(sc[0] | (sc[1] << 8)));
-        int q;
-        if (tier == 2) {
-          q = (int8_t)codes[j];
-        } else {
-          int nib = (j % 2 == 0) ? (codes[j / 2] & 0xf) : (codes[j / 2] >> 4);
-          q = (nib >= 8) ? nib - 16 : nib;
-        }
-        val = q * s;
-      }
-      outs[v][j] = val;
-    }
-  }
+  dequant_part(d, tier, rec, 0, 0, d, gate);
+  dequant_part(d, tier, rec, 1, 0, d, up);
+  dequant_part(d, tier, rec, 2, 0, d, down);
   return 0;
 }
 
@@ -231,7 +263,9 @@ static float canon_dot_h_f(const uint16_t* a, const float* b, int n) {
 int orc_predict(int d, int d_ff, int r, const uint16_t* A, const uint16_t* B, const float* bias,
                 const uint16_t* x, float* z, float* s) {
   if (d <= 0 || d % 8 != 0 || r <= 0 || r % 8 != 0 || d_ff <= 0) return -1;
+#pragma omp parallel for schedule(static)
   for (int j = 0; j < r; j++) z[j] = canon_dot_h_h(A + (int64_t)j * d, x, d);
+#pragma omp parallel for schedule(static)
   for (int i = 0; i < d_ff; i++) {
     float v = canon_dot_h_f(B + (int64_t)i * r, z, r);
     if (bias) v = v + bias[i];
@@ -284,31 +318,31 @@ int orc_select_tiers(int d_ff, const float* s, int k, int n16, int n8, uint8_t* 
  * Sec. 1 and Sec. 6.4: LRU replacement of neurons in HBM). One step is
  * atomic: hits are decided against the cache before any eviction.
  *   tier of neuron i for the step = max over batch rows; R = {i : tier > 0}.
- *   For i in R, ascending: resident at the same tier -> HIT; resident at
- *   another tier -> REFILL in place; not resident -> NEW.
- *   Each NEW (ascending id) takes the untouched slot with the smallest
- *   (last_use, slot) found by a linear scan, evicting its neuron; when no
- *   untouched slot is left it is a BYPASS into staging slot C + j'.
- *   Every slot used by R gets last_use = step.
+ *   For i in R, ascending, when i is resident at tier r and requested at t:
+ *     policy 0 (exact tier): r == t -> HIT; otherwise REFILL in place at t.
+ *     policy 1 (dominance): r >= t -> HIT, and the step uses i at tier r
+ *       (the bytes in the slot are the record at tier r); r < t -> REFILL in
+ *       place at t.
+ *   Not resident -> NEW. Each NEW (ascending id) takes the untouched slot
+ *   with the smallest (last_use, slot) found by a linear scan, evicting its
+ *   neuron; when no untouched slot is left it is a BYPASS into staging slot
+ *   C + j'. Every slot used by R gets last_use = step.
  * State arrays (in/out): slot_of [d_ff], slot_key/slot_tier/slot_last [C];
  * an empty slot has key -1 and last_use -1.
- * Outputs: counts [16] (same order as the library's plan counts), the
- * required list (ids, tier, hit code 0 NEW 1 HIT 2 REFILL 3 BYPASS, slot,
- * row mask), the fill list, evicted ids, and the FFN work order
- * (tier-major FP16, INT8, INT4; ascending id inside a tier).
- * fill_from[f]: for a REFILL, the tier of the record the slot held for the
- * same neuron before the step, else 0. counts[13] counts the fills whose
- * slot held the neuron's FP16 record and that need INT8 or INT4: the record
- * they need is a function of bytes already in the slot (every tier record is
- * quantized from the same fp16 weights), so no host copy is needed.        */
+ * Outputs: counts [16]: 0 |R|, 1 HIT, 2 REFILL, 3 NEW, 4 BYPASS, 5 evictions,
+ * 6 fills, 7..9 |R| at the step tier FP16 / INT8 / INT4, 10..12 fills by
+ * tier FP16 / INT8 / INT4, the rest 0; the required list (ids, step tier,
+ * hit code 0 NEW 1 HIT 2 REFILL 3 BYPASS, slot, row mask), the fill list
+ * (every non-HIT in ascending id: id, tier, slot, and for a REFILL the tier
+ * the slot held before the step, else 0) and the evicted ids in victim
+ * order. Returns 0, -1 on bad arguments, -2 if the staging slots overflow. */
 
-int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int step,
+int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int step, int policy,
                  int32_t* slot_of, int32_t* slot_key, uint8_t* slot_tier, int32_t* slot_last,
                  int32_t* counts, int32_t* req_ids, uint8_t* req_tier, uint8_t* req_hit,
                  int32_t* req_slot, uint32_t* req_mask, int32_t* fill_ids, uint8_t* fill_tier,
-                 int32_t* fill_slot, uint8_t* fill_from, int32_t* evicted_ids,
-                 int32_t* work_slot, uint32_t* work_mask) {
-  if (d_ff <= 0 || C < 0 || S < 0 || B < 1 || B > 32) return -1;
+                 int32_t* fill_slot, uint8_t* fill_from, int32_t* evicted_ids) {
+  if (d_ff <= 0 || C < 0 || S < 0 || B < 1 || B > 32 || policy < 0 || policy > 1) return -1;
   for (int c = 0; c < 16; c++) counts[c] = 0;
   uint8_t* touched = (uint8_t*)calloc((size_t)(C > 0 ? C : 1), 1);
   uint8_t* before = (uint8_t*)calloc((size_t)(d_ff > 0 ? d_ff : 1), 1); /* by position */
@@ -332,10 +366,18 @@ int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int ste
   for (int p = 0; p < n; p++) {
     int i = req_ids[p], s = slot_of[i];
     if (s >= 0) {
+      int r = slot_tier[s], t = req_tier[p];
       touched[s] = 1;
-      before[p] = slot_tier[s];
-      if (slot_tier[s] == req_tier[p]) { req_hit[p] = 1; counts[1]++; }
-      else { req_hit[p] = 2; counts[2]++; slot_tier[s] = req_tier[p]; }
+      before[p] = (uint8_t)r;
+      if (r == t || (policy == 1 && r > t)) {
+        req_hit[p] = 1;
+        req_tier[p] = (uint8_t)r; /* the step uses the resident record */
+        counts[1]++;
+      } else {
+        req_hit[p] = 2;
+        counts[2]++;
+        slot_tier[s] = (uint8_t)t;
+      }
       req_slot[p] = s;
     } else {
       req_hit[p] = 0;
@@ -376,27 +418,16 @@ int orc_lru_plan(int d_ff, int C, int S, int B, const uint8_t* tier_map, int ste
     if (req_hit[p] != 3) slot_last[req_slot[p]] = step;
   int nf = 0;
   for (int p = 0; p < n; p++) {
+    counts[7 + (3 - req_tier[p])]++;
     if (req_hit[p] == 1) continue;
     fill_ids[nf] = req_ids[p];
     fill_tier[nf] = req_tier[p];
     fill_slot[nf] = req_slot[p];
     fill_from[nf] = req_hit[p] == 2 ? before[p] : 0;
     counts[10 + (3 - req_tier[p])]++;
-    if (fill_from[nf] == 3 && req_tier[p] < 3) counts[13]++;
     nf++;
   }
   counts[6] = nf;
-  int w = 0;
-  for (int t = 3; t >= 1; t--) {
-    for (int p = 0; p < n; p++) {
-      if (req_tier[p] != t) continue;
-      work_slot[w] = req_slot[p];
-      work_mask[w] = req_mask[p];
-      w++;
-    }
-    counts[7 + (3 - t)] = 0;
-    for (int p = 0; p < n; p++) counts[7 + (3 - t)] += (req_tier[p] == t);
-  }
   free(touched);
   free(before);
   return 0;
@@ -417,31 +448,68 @@ int orc_sparse_ffn(int d, int B, int n, const int32_t* ids, const uint8_t* tiers
                    const uint8_t* rec_int8, int64_t stride_int8, const uint8_t* rec_int4,
                    int64_t stride_int4, const uint16_t* x, double* y) {
   if (d <= 0 || d % 128 != 0 || B < 1 || n < 0) return -1;
-  double* g = (double*)malloc(sizeof(double) * d);
-  double* u = (double*)malloc(sizeof(double) * d);
-  double* dn = (double*)malloc(sizeof(double) * d);
-  double* xd = (double*)malloc(sizeof(double) * d);
-  for (int64_t j = 0; j < (int64_t)B * d; j++) y[j] = 0.0;
-  int rc = 0;
+  const uint8_t** recs = (const uint8_t**)malloc(sizeof(uint8_t*) * (n > 0 ? n : 1));
   for (int p = 0; p < n; p++) {
-    const uint8_t* rec;
     int t = tiers[p];
-    if (t == 3) rec = rec_fp16 + (int64_t)ids[p] * stride_fp16;
-    else if (t == 2) rec = rec_int8 + (int64_t)ids[p] * stride_int8;
-    else if (t == 1) rec = rec_int4 + (int64_t)ids[p] * stride_int4;
-    else { rc = -1; break; }
-    orc_dequant_record(d, t, rec, g, u, dn);
-    for (int b = 0; b < B; b++) {
-      if (masks && !((masks[p] >> b) & 1u)) continue;
-      for (int j = 0; j < d; j++) xd[j] = orc_f16_to_f32(x[(int64_t)b * d + j]);
-      double a = 0.0, c = 0.0;
-      for (int j = 0; j < d; j++) { a += g[j] * xd[j]; c += u[j] * xd[j]; }
-      double h = a / (1.0 + exp(-a)) * c;
-      for (int j = 0; j < d; j++) y[(int64_t)b * d + j] += h * dn[j];
+    if (t == 3) recs[p] = rec_fp16 + (int64_t)ids[p] * stride_fp16;
+    else if (t == 2) recs[p] = rec_int8 + (int64_t)ids[p] * stride_int8;
+    else if (t == 1) recs[p] = rec_int4 + (int64_t)ids[p] * stride_int4;
+    else { free(recs); return -1; }
+  }
+  double* xd = (double*)malloc(sizeof(double) * (size_t)B * d);
+  for (int64_t j = 0; j < (int64_t)B * d; j++) xd[j] = orc_f16_to_f32(x[j]);
+  /* h[p][b] = silu(<g_p, x_b>) * <u_p, x_b>, each dot product summed in
+     ascending element order; 0 where row b does not select neuron p */
+  double* h = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * B);
+#pragma omp parallel
+  {
+    double* g = (double*)malloc(sizeof(double) * d);
+    double* u = (double*)malloc(sizeof(double) * d);
+#pragma omp for schedule(dynamic, 4)
+    for (int p = 0; p < n; p++) {
+      dequant_part(d, tiers[p], recs[p], 0, 0, d, g);
+      dequant_part(d, tiers[p], recs[p], 1, 0, d, u);
+      for (int b = 0; b < B; b++) {
+        double hv = 0.0;
+        if (!masks || ((masks[p] >> b) & 1u)) {
+          double a = 0.0, c = 0.0;
+          for (int j = 0; j < d; j++) {
+            a += g[j] * xd[(int64_t)b * d + j];
+            c += u[j] * xd[(int64_t)b * d + j];
+          }
+          hv = a / (1.0 + exp(-a)) * c;
+        }
+        h[(int64_t)p * B + b] = hv;
+      }
+    }
+    free(g);
+    free(u);
+  }
+  /* y_b[j] = sum over selected p, in ascending p, of h[p][b] * d_p[j], one
+     quantization group of 128 output elements per task */
+  int G = d / 128;
+#pragma omp parallel
+  {
+    double dn[128];
+#pragma omp for schedule(dynamic, 1)
+    for (int gj = 0; gj < G; gj++) {
+      for (int b = 0; b < B; b++)
+        for (int j = 0; j < 128; j++) y[(int64_t)b * d + gj * 128 + j] = 0.0;
+      for (int p = 0; p < n; p++) {
+        dequant_part(d, tiers[p], recs[p], 2, gj * 128, 128, dn);
+        for (int b = 0; b < B; b++) {
+          if (masks && !((masks[p] >> b) & 1u)) continue;
+          double hv = h[(int64_t)p * B + b];
+          double* yb = y + (int64_t)b * d + gj * 128;
+          for (int j = 0; j < 128; j++) yb[j] += hv * dn[j];
+        }
+      }
     }
   }
-  free(g); free(u); free(dn); free(xd);
-  return rc;
+  free(h);
+  free(xd);
+  free(recs);
+  return 0;
 }
 
 /* Dense SwiGLU FFN in fp64 (every neuron at fp16): the reference point the

@@ -25,6 +25,21 @@ def r8_errors(y, y_ref):
 FFN_TOL = 2e-3
 
 
+def work_order(plan):
+    """The library's FFN work list of a plan, from the oracle's required
+    list: slots and row masks tier-major (FP16, INT8, INT4), ascending id
+    inside a tier (the layout the plan's work_slot / work_mask document)."""
+    order = [p for t in (3, 2, 1) for p in range(len(plan["req_ids"])) if plan["req_tier"][p] == t]
+    return (np.asarray([plan["req_slot"][p] for p in order], np.int32),
+            np.asarray([plan["req_mask"][p] for p in order], np.uint32))
+
+
+def derived_fills(plan):
+    """Fills to INT8 / INT4 of a neuron whose slot held its FP16 record
+    (fill_from == 3): the library makes them on the GPU from that record."""
+    return int(np.count_nonzero((plan["fill_from"] == 3) & (plan["fill_tier"] < 3)))
+
+
 def subset_records(ld, ids):
     """Oracle records (all three tiers) for the neurons `ids` only, indexed by
     position in `ids`; returns ({tier: records}, {neuron id: row})."""

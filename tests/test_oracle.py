@@ -236,9 +236,11 @@ def test_select_all_equal_and_signed_zero():
 # --------------------------------------------------------------------------
 # LRU slot cache
 
-def _brute_lru_step(state, tiers, step, C):
+def _brute_lru_step(state, tiers, step, C, dominance=False):
     """Brute force of one atomic step: sort every untouched slot by
-    (last use, slot) and hand them out in that order."""
+    (last use, slot) and hand them out in that order. dominance: a neuron
+    resident at a tier at or above the requested one is a hit at its resident
+    tier (tiers[i] is updated to the tier the step uses)."""
     slot_of, key, stier, last = state
     req = [i for i in sorted(tiers) if tiers[i] > 0]
     touched = set()
@@ -247,7 +249,10 @@ def _brute_lru_step(state, tiers, step, C):
         if i in slot_of:
             s = slot_of[i]
             touched.add(s)
-            res[i] = ("HIT" if stier[s] == tiers[i] else "REFILL", s, stier[s])
+            hit = stier[s] == tiers[i] or (dominance and stier[s] > tiers[i])
+            res[i] = ("HIT" if hit else "REFILL", s, stier[s])
+            if hit:
+                tiers[i] = stier[s]
             stier[s] = tiers[i]
     free = sorted((last[s], s) for s in range(C) if s not in touched)
     new = [i for i in req if i not in slot_of]
@@ -269,14 +274,16 @@ def _brute_lru_step(state, tiers, step, C):
     return req, res, evicted
 
 
+@pytest.mark.parametrize("policy", [oracle.POLICY_EXACT, oracle.POLICY_DOMINANCE])
 @pytest.mark.parametrize("d_ff,C,B", [(40, 7, 1), (40, 12, 3), (25, 25, 2), (30, 0, 1)])
-def test_lru_matches_brute_force(d_ff, C, B):
+def test_lru_matches_brute_force(d_ff, C, B, policy):
     rng = np.random.default_rng(d_ff * 100 + C)
     S = d_ff
-    cache = oracle.LRUCache(d_ff, C, S)
+    dom = policy == oracle.POLICY_DOMINANCE
+    cache = oracle.LRUCache(d_ff, C, S, policy)
     st = ({}, [None] * C, [0] * C, [-1] * C)
     code = {"NEW": 0, "HIT": 1, "REFILL": 2, "BYPASS": 3}
-    derived = 0
+    derived = tier_hits = 0
     for step in range(30):
         tm = np.zeros((B, d_ff), np.uint8)
         for b in range(B):
@@ -284,26 +291,28 @@ def test_lru_matches_brute_force(d_ff, C, B):
             tm[b, ids] = rng.integers(1, 4, size=ids.size)
         p = cache.plan(tm, step)
         tiers = {i: int(tm[:, i].max()) for i in range(d_ff)}
-        req, res, ev = _brute_lru_step(st, tiers, step, C)
+        asked = dict(tiers)
+        req, res, ev = _brute_lru_step(st, tiers, step, C, dominance=dom)
         assert list(p["req_ids"]) == req
         assert [code[res[i][0]] for i in req] == list(p["req_hit"])
         assert [res[i][1] for i in req] == list(p["req_slot"])
+        assert list(p["req_tier"]) == [tiers[i] for i in req]
         assert list(p["evicted_ids"]) == ev
         assert list(p["fill_ids"]) == [i for i in req if res[i][0] != "HIT"]
         # the tier a REFILL's slot held before the step (0 for NEW / BYPASS)
         frm = [res[i][2] if res[i][0] == "REFILL" else 0 for i in req if res[i][0] != "HIT"]
         assert list(p["fill_from"]) == frm
+        # an FP16 record refilled to INT8 / INT4 happens only under exact tiers
+        derived += sum(1 for f, i in zip(frm, p["fill_ids"]) if f == 3 and tiers[i] < 3)
+        tier_hits += sum(1 for i in req if res[i][0] == "HIT" and tiers[i] != asked[i])
         c = p["counts"]
-        assert c[13] == sum(1 for f, i in zip(frm, p["fill_ids"]) if f == 3 and tiers[i] < 3)
-        derived += int(c[13])
         assert c[0] == c[1] + c[2] + c[3] + c[4] == len(req)
         assert c[6] == c[2] + c[3] + c[4] == c[10] + c[11] + c[12]
+        assert [c[7], c[8], c[9]] == [sum(1 for i in req if tiers[i] == t) for t in (3, 2, 1)]
+        assert not c[13:].any()
         # masks: bit b set iff row b selected the neuron
         for n_, i in enumerate(req):
             assert p["req_mask"][n_] == sum(1 << b for b in range(B) if tm[b, i] > 0)
-        # FFN work order: tier-major, ascending id inside a tier
-        ws = [res[i][1] for t in (3, 2, 1) for i in req if tiers[i] == t]
-        assert list(p["work_slot"]) == ws
         # tables: the same as the brute force's, and inverse maps of each other
         assert {i: int(cache.slot_of[i]) for i in range(d_ff) if cache.slot_of[i] >= 0} == st[0]
         for s_ in range(C):
@@ -312,7 +321,49 @@ def test_lru_matches_brute_force(d_ff, C, B):
             assert cache.slot_last[s_] == st[3][s_]
             if k_ >= 0:
                 assert cache.slot_of[k_] == s_ and cache.slot_tier[s_] == st[2][s_]
-    assert C == 0 or derived > 0  # the FP16 -> lower-tier refill case was exercised
+    if dom:
+        assert derived == 0 and (C == 0 or tier_hits > 0)  # hits above the requested tier
+    else:
+        assert tier_hits == 0 and (C == 0 or derived > 0)  # FP16 -> lower-tier refills
+
+
+def test_lru_dominance_closed_form_when_everything_fits():
+    """Dominance hits with C >= d_ff: nothing is ever evicted, a resident
+    tier only rises, so neuron i is resident at the highest tier requested so
+    far; a request at tier t is a hit iff i was requested before at some
+    tier >= t, and the step then uses that highest tier."""
+    d_ff = 50
+    cache = oracle.LRUCache(d_ff, d_ff, 0, oracle.POLICY_DOMINANCE)
+    rng = np.random.default_rng(5)
+    best = np.zeros(d_ff, np.int64)
+    for t in range(40):
+        tm = np.zeros(d_ff, np.uint8)
+        ids = rng.choice(d_ff, 12, replace=False)
+        tm[ids] = rng.integers(1, 4, size=ids.size)
+        p = cache.plan(tm, t)
+        req = np.nonzero(tm)[0]
+        hit = best[req] >= tm[req]
+        assert list(p["req_ids"]) == list(req)
+        assert list(p["req_hit"] == 1) == list(hit)
+        assert list(p["req_tier"]) == list(np.where(hit, best[req], tm[req]))
+        assert int(p["counts"][1]) == int(hit.sum()) and int(p["counts"][5]) == 0
+        best[req] = np.maximum(best[req], tm[req])
+
+
+def test_lru_dominance_equals_exact_with_one_tier():
+    """With every active neuron at one tier the two policies are the same
+    cache (no resident tier differs from a requested one)."""
+    d_ff, C = 120, 30
+    a = oracle.LRUCache(d_ff, C, d_ff, oracle.POLICY_EXACT)
+    b = oracle.LRUCache(d_ff, C, d_ff, oracle.POLICY_DOMINANCE)
+    rng = np.random.default_rng(8)
+    for t in range(30):
+        tm = np.zeros((2, d_ff), np.uint8)
+        for r in range(2):
+            tm[r, rng.choice(d_ff, 20, replace=False)] = 2
+        pa, pb = a.plan(tm, t), b.plan(tm, t)
+        for key in pa:
+            assert np.array_equal(pa[key], pb[key]), key
 
 
 def test_lru_atu_closed_form():
@@ -437,3 +488,24 @@ def test_inputs_are_ar1_with_unit_marginals():
     assert abs(x.std() - 1.0) < 0.05
     c = np.mean([np.corrcoef(x[t], x[t + 1])[0, 1] for t in range(63)])
     assert abs(c - 0.9) < 0.02
+
+
+def test_oracle_results_do_not_depend_on_threads():
+    """Threads only split independent sums: records, scores and the FFN are
+    the same bits at one thread and at several."""
+    lw = W.make_layer(31, 0, 512, 300, 32, 2, rhos=(0.9, 0.5, 0.7))
+    ids = np.arange(0, 300, 3, dtype=np.int32)
+    tiers = (ids % 3 + 1).astype(np.uint8)
+    masks = (ids % 7 + 1).astype(np.uint32)
+    outs = []
+    for n in (1, 4):
+        oracle.set_threads(n)
+        recs = {t: oracle.build_records(lw.w_gate, lw.w_up, lw.w_down, t) for t in (1, 2, 3)}
+        _, sc = oracle.predict(lw.pred_a, lw.pred_b, None, lw.x[1, 0])
+        y = oracle.sparse_ffn(lw.x[0], ids, tiers, recs, masks)
+        outs.append((recs, sc, y))
+    oracle.set_threads(1)
+    (r1, s1, y1), (r4, s4, y4) = outs
+    assert all(np.array_equal(r1[t], r4[t]) for t in (1, 2, 3))
+    assert np.array_equal(s1.view(np.uint32), s4.view(np.uint32))
+    assert np.array_equal(y1.view(np.uint64), y4.view(np.uint64))
