@@ -4,15 +4,19 @@
 One step = one decode token through every FFN layer of the stack: for each
 layer, predictor scores -> top-k and tiers -> cache plan -> cache fill from
 the pinned host store -> gather-dequant sparse FFN, all through the C ABI.
+The default workload is the 70B-shaped stack (80 layers, d 8192, d_ff 28672,
+k 2867 with tiers 286/860/1721, C = k), the configuration the roofline target
+is quoted on.
 
-Streams: predict+plan run on an aux stream, fills on a copy stream, the FFN on
-the main stream. Layer l's predict may start once the FFN of layer l-2 is
-done (the one-layer look-ahead of the paper's preloader, Sec. 5.4), so the
-fill of layer l overlaps the FFN of layer l-1 (Sec. 1: asynchronous loading
-overlapped with computation).
+Streams (paper_2410_14740_amd.pipeline): predict + plan on an aux stream,
+fills on a copy stream, the FFN on the main stream; layer l's predict may
+start once the FFN of layer l-2 is done, so the fill of layer l overlaps the
+FFN of layer l-1 (Sec. 1: asynchronous loading overlapped with computation;
+Sec. 6.1: dedicated streams).
 
 Prints one JSON line (the benchmark contract), including the HBM roofline of
-the sparse FFN and the oracle timed on the host cores.
+the sparse FFN on the workload's layer shape and the oracle timed on the host
+cores at one thread and at every core this process may use.
 """
 from __future__ import annotations
 
@@ -40,20 +44,30 @@ def parse_args():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=120, help="timed decode steps")
     p.add_argument("--warmup", type=int, default=8, help="untimed decode steps first")
-    p.add_argument("--workload", default="llama2-7b")
-    p.add_argument("--weight-sets", type=int, default=0,
-                   help="draw only this many distinct weight sets and let layers share them "
-                        "(0 = every layer its own weights)")
+    p.add_argument("--workload", default="llama2-70b")
+    p.add_argument("--weight-sets", type=int, default=-1,
+                   help="draw only this many distinct weight sets and let layers share their "
+                        "pinned neuron stores (0 = every layer its own weights; -1 = 8 for the "
+                        "70B stack, whose 80 stores would take 199 GB of pinned host memory, "
+                        "else 0). Every layer keeps its own predictor, inputs and slot cache.")
+    p.add_argument("--policy", choices=("exact", "dominance"), default="exact",
+                   help="cache hits: exact tier (default) or a resident tier at or above the "
+                        "requested one")
+    p.add_argument("--policy-sweep", action="store_true",
+                   help="only the cache-policy measurement: hit rates of exact-tier and "
+                        "dominance hits, LRU at C = 30%% and at C = k (the ATU regime), against "
+                        "the AR(1) correlation rho of the inputs, plus the 7B stack's tokens/s "
+                        "under both policies")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle baseline sample (0 = skip)")
     p.add_argument("--layers", type=int, default=0, help="override the layer count (0 = workload's)")
-    p.add_argument("--ffn-layers", type=int, default=16,
+    p.add_argument("--ffn-layers", type=int, default=8,
                    help="layers cycled by the isolated sparse-FFN measurement on the workload's "
                         "layer shape (their active records exceed the 256 MB Infinity Cache)")
     p.add_argument("--ffn-reps", type=int, default=10, help="passes over those layers")
-    p.add_argument("--target-workload", default="llama2-70b",
+    p.add_argument("--extra-workload", default="llama2-7b",
                    help="second isolated sparse-FFN measurement on this layer shape ('' = skip)")
-    p.add_argument("--target-layers", type=int, default=8)
+    p.add_argument("--extra-layers", type=int, default=16)
     p.add_argument("--overlap-steps", type=int, default=4,
                    help="untimed steps after the timed ones with events around every stage, "
                         "to measure how much of the fill time overlaps compute")
@@ -113,48 +127,73 @@ def build_stack(wl, n_layers, steps_total, weight_sets, torch, m2c, W, flags=0):
     return layers, x_dev, keep
 
 
-def cpu_baseline(wl, ld, n_layers, budget_s, oracle):
-    """The oracle (plain C, one thread) on a bounded sample of the same work:
-    layer 0 of the stack, consecutive decode steps until about `budget_s`
-    seconds of predict + select + plan + FFN have run. Record building is
-    set-up, not timed. Returns the contract's cpu_baseline object."""
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy):
+    """The oracle on a bounded sample of the same work: layer 0 of the stack,
+    consecutive decode steps of predict + select + LRU plan + fp64 sparse FFN
+    until about `budget_s` seconds have run, timed twice: at one thread (the
+    paper's one-core setting) and at every core this process may use (OpenMP
+    over independent sums; the results are the same bits). Building the
+    records of the neurons the sample touches is set-up, not timed. Returns
+    the contract's cpu_baseline object (the all-core leg) with the one-thread
+    leg inside."""
     k, n16, n8 = wl.counts()
     C = wl.cache_slots()
     cap = min(wl.d_ff, k)
-    cache = oracle.LRUCache(wl.d_ff, C, max(0, cap - C))
-    # records for the neurons the sample will touch (found by a first pass)
+    n_cores = len(os.sched_getaffinity(0))
+    oracle.set_threads(n_cores)
+    # records for the neurons the sample can touch (found by a first pass)
     steps_avail = ld.x.shape[0]
     tiers_by_step = []
-    t0 = time.perf_counter()
-    for t in range(min(steps_avail, 64)):
+    for t in range(steps_avail):
         _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
         tiers_by_step.append(oracle.select_tiers(s, k, n16, n8)[0])
-        if time.perf_counter() - t0 > budget_s / 3:
-            break
     used = np.nonzero(np.any(np.stack(tiers_by_step) > 0, axis=0))[0]
     row = np.full(wl.d_ff, -1, np.int64)
     row[used] = np.arange(used.size)
     recs = {q: oracle.build_records(ld.w_gate[used], ld.w_up[used],
                                     np.ascontiguousarray(ld.w_down[:, used]), q) for q in (1, 2, 3)}
-    n_steps = len(tiers_by_step)
-    t_start = time.perf_counter()
-    done = 0
-    for t in range(n_steps):
-        _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
-        tm, _ = oracle.select_tiers(s, k, n16, n8)
-        plan = cache.plan(tm, t)
-        ids = row[plan["req_ids"]].astype(np.int32)
-        oracle.sparse_ffn(ld.x[t], ids, plan["req_tier"], recs)
-        done += 1
-        if time.perf_counter() - t_start > budget_s:
-            break
-    el = time.perf_counter() - t_start
-    per = el / done
-    return {"value": 1.0 / (per * n_layers), "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"layer 0 of {wl.name}, {done} consecutive decode steps of predict + "
-                      f"select + LRU plan + fp64 sparse FFN, single thread; "
-                      f"{per * 1e3:.1f} ms per layer-step, scaled to {n_layers} layers",
-            "ms_per_layer_step": per * 1e3}
+
+    def leg(threads, budget):
+        oracle.set_threads(threads)
+        cache = oracle.LRUCache(wl.d_ff, C, max(0, cap - C), policy)
+        t_start = time.perf_counter()
+        done = 0
+        for t in range(steps_avail):
+            _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
+            tm, _ = oracle.select_tiers(s, k, n16, n8)
+            plan = cache.plan(tm, t)
+            ids = row[plan["req_ids"]].astype(np.int32)
+            oracle.sparse_ffn(ld.x[t], ids, plan["req_tier"], recs)
+            done += 1
+            if time.perf_counter() - t_start > budget:
+                break
+        per = (time.perf_counter() - t_start) / done
+        return per, done, oracle.get_threads()
+
+    per1, done1, _ = leg(1, budget_s / 2)
+    perN, doneN, used_threads = leg(n_cores, budget_s / 2)
+    oracle.set_threads(1)
+    return {"value": 1.0 / (perN * n_layers), "unit": "tokens/s", "cores": used_threads,
+            "kind": "oracle",
+            "sample": f"layer 0 of the {wl.name} stack, {doneN} consecutive decode steps of "
+                      f"predict + select + LRU plan + fp64 sparse FFN on {used_threads} threads "
+                      f"(OpenMP over independent sums); {perN * 1e3:.1f} ms per layer-step, "
+                      f"scaled to {n_layers} layers",
+            "ms_per_layer_step": perN * 1e3,
+            "cpu_model": _cpu_model(), "sched_getaffinity": n_cores,
+            "one_thread": {"value": 1.0 / (per1 * n_layers), "unit": "tokens/s", "cores": 1,
+                           "ms_per_layer_step": per1 * 1e3, "steps": done1}}
 
 
 def hold_stream(torch, s, host_seconds):
@@ -365,6 +404,192 @@ def batched_sweep(steps, warmup, torch, m2c, W, only=None):
     return {"workload": wl.name, "batch": B, "steps": steps, "warmup": warmup, "points": points}
 
 
+class _StageEvents:
+    """Hooks of the schedule that record HIP events around the stages:
+    `timed` keeps (FFN start, FFN end, fill start, fill end) per layer-step,
+    `spans` keeps (aux start, aux end, fill start, fill end, FFN start, FFN
+    end) for the overlap measurement."""
+
+    def __init__(self, torch, timed, spans):
+        self.torch = torch
+        self.timed, self.spans = timed, spans
+        self.cur = None
+
+    def _ev(self, s, i):
+        self.cur[i].record(s)
+
+    def before_predict(self, l, t, s):
+        self.cur = [self.torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        self._ev(s, 0)
+
+    def after_plan(self, l, t, s):
+        self._ev(s, 1)
+
+    def before_fill(self, l, t, s):
+        self._ev(s, 2)
+
+    def after_fill(self, l, t, s):
+        self._ev(s, 3)
+
+    def before_ffn(self, l, t, s):
+        self._ev(s, 4)
+
+    def after_ffn(self, l, t, s):
+        self._ev(s, 5)
+        (self.spans if self.spans is not None else self.timed).append(self.cur)
+
+
+def run_stack(wl, n_layers, steps, warmup, weight_sets, flags, overlap_steps, stage_events,
+              torch, m2c, W):
+    """The decode pipeline over the whole stack: `warmup` untimed steps,
+    `steps` timed ones between a synchronization on each side, then
+    `overlap_steps` untimed steps with events around every stage."""
+    from paper_2410_14740_amd import pipeline
+    k, n16, n8 = wl.counts()
+    steps_total = warmup + steps
+    t_setup = time.perf_counter()
+    layers, x_dev, ld0 = build_stack(wl, n_layers, steps_total + overlap_steps, weight_sets, torch,
+                                     m2c, W, flags=flags)
+    log(f"setup {time.perf_counter() - t_setup:.1f} s")
+    d, d_ff = wl.d_model, wl.d_ff
+    tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
+    # m2c_sparse_ffn adds into y (a residual stream): one zeroed row per
+    # layer-step, so every output is the plain FFN of its token
+    y = torch.zeros((steps_total + overlap_steps, n_layers, d), dtype=torch.float32, device="cuda")
+    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=2)
+    timing = []
+    ev_hooks = _StageEvents(torch, timing, None) if stage_events else None
+
+    def step(t, hooks=None):
+        sched.step(t, lambda l: x_dev[l, t], lambda l: y[t, l], hooks=hooks)
+
+    for t in range(warmup):
+        step(t)
+    torch.cuda.synchronize()
+    st0 = [L.stats() for L in layers]
+    t0 = time.perf_counter()
+    for t in range(warmup, steps_total):
+        step(t, ev_hooks)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st1 = [L.stats() for L in layers]
+    # A few more steps, untimed, with events around every stage: how much of
+    # the fills' time runs while predict / plan or the FFN runs on another
+    # stream (the events themselves delay the cross-stream waits a little, so
+    # they stay out of the timed steps). The aux stream (and through the
+    # events the other two) is held by a spin kernel while the host enqueues,
+    # so the extra calls do not space the stages out.
+    spans = []
+    if overlap_steps:
+        hold_stream(torch, sched.aux, 0.002 * n_layers * overlap_steps)
+        sp_hooks = _StageEvents(torch, None, spans)
+        for t in range(steps_total, steps_total + overlap_steps):
+            step(t, sp_hooks)
+    torch.cuda.synchronize()
+    overlap = stage_overlap(spans) if spans else None
+    ffn_ms = np.array([e[4].elapsed_time(e[5]) for e in timing]) if timing else None
+    fill_ms = np.array([e[2].elapsed_time(e[3]) for e in timing]) if timing else None
+    diff = lambda f: sum(getattr(b, f) - getattr(a, f) for a, b in zip(st0, st1))
+    reqs = diff("req")
+    # bytes the fills read over the host link (fills derived on the GPU from a
+    # resident FP16 record read none)
+    fill_bytes = diff("host_bytes")
+    derived_bytes = diff("fill_bytes") - fill_bytes
+    n_ls = steps * n_layers
+    # host-link rate of the fills: from the stage events if recorded, else the
+    # fill bytes over the wall time (a lower bound: fills run back to back only
+    # when nothing else is on the critical path)
+    fill_avg_s = float(fill_ms.mean()) * 1e-3 if fill_ms is not None else wall / n_ls
+    info = layers[0].info
+    for L in layers:
+        L.close()
+    return {
+        "wall": wall, "n_layer_steps": n_ls, "ld0": ld0, "info": info,
+        "tokens_per_s": steps / wall, "us_per_layer_step": wall / n_ls * 1e6,
+        "pipeline": {
+            "stage_events": bool(stage_events),
+            "ffn_us_avg": float(ffn_ms.mean()) * 1e3 if ffn_ms is not None else None,
+            "fill_us_avg": fill_avg_s * 1e6 if fill_ms is not None else None,
+            "fill_MB_per_layer_step": fill_bytes / n_ls / 1e6,
+            "derived_MB_per_layer_step": derived_bytes / n_ls / 1e6,
+            "ffn_MB_per_layer_step": diff("req_bytes") / n_ls / 1e6,
+            "cache": {"hit_rate": diff("hit") / max(reqs, 1),
+                      "refill_rate": diff("refill") / max(reqs, 1),
+                      "new_rate": diff("new_") / max(reqs, 1),
+                      "bypass_rate": diff("bypass") / max(reqs, 1)},
+            "overlap": overlap,
+        },
+        "host_link": {"kernel": "fill_kernel (device gather from pinned host memory)",
+                      "achieved": fill_bytes / n_ls / fill_avg_s / 1e9,
+                      "peak": PEAK_HOST_LINK_GBPS, "unit": "GB/s",
+                      "frac": fill_bytes / n_ls / fill_avg_s / 1e9 / PEAK_HOST_LINK_GBPS,
+                      "measured_over": "fill kernels" if fill_ms is not None else "wall time"},
+    }
+
+
+def policy_sweep(steps, torch, m2c, W):
+    """Cache behaviour against the inter-token correlation of the inputs (the
+    paper's Fig. 6 reports about 80% overlap between consecutive tokens' active
+    sets): on two 7B-shaped layers, for rho in {0.5, 0.7, 0.8, 0.9, 0.95},
+    the consecutive-step overlap |S_t & S_t-1| / k measured from the plans and
+    the hit rates of exact-tier and dominance hits with LRU at C = 30% of d_ff
+    and at C = k (where LRU is the paper's Adjacent Token Update policy);
+    then the 7B stack's tokens/s and host-link bytes under both policies."""
+    wl0 = W.WORKLOADS["llama2-7b"]
+    k, n16, n8 = wl0.counts()
+    d, d_ff = wl0.d_model, wl0.d_ff
+    rows = []
+    owner = None
+    tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream()
+    for rho in (0.5, 0.7, 0.8, 0.9, 0.95):
+        for C, cname in ((wl0.cache_slots(), "lru_30pct"), (k, "atu_c_eq_k")):
+            for pol, flag in (("exact", 0), ("dominance", m2c.FLAG_DOMINANT_HITS)):
+                hits = reqs = host = ovl = 0
+                for l in range(2):
+                    ld = W.make_layer(wl0.seed + 100, l, d, d_ff, wl0.pred_rank, steps, (rho,),
+                                      wl0.sigma_w, wl0.sigma_p, draw_weights=owner is None)
+                    L = m2c.Layer(m2c.make_desc(d, d_ff, wl0.pred_rank, k, C, flags=flag), ld,
+                                  weights_of=owner)
+                    if owner is None:
+                        owner = L
+                    x = torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16).cuda()
+                    prev = None
+                    for t in range(steps):
+                        L.predict_rank(x[t], 1, k, n16, n8, None, tiers, stream=s)
+                        L.cache_plan(tiers, 1, t, stream=s)
+                        L.cache_fill(stream=s)
+                        if t >= 4:  # steady state: the cache has warmed up
+                            if t == 4:
+                                torch.cuda.synchronize()
+                                st0 = L.stats()
+                        cur = set(L.read_plan()["req_ids"].tolist())
+                        if prev is not None and t >= 4:
+                            ovl += len(cur & prev)
+                        prev = cur
+                    torch.cuda.synchronize()
+                    st1 = L.stats()
+                    hits += st1.hit - st0.hit
+                    reqs += st1.req - st0.req
+                    host += st1.host_bytes - st0.host_bytes
+                    if L is not owner:
+                        L.close()
+                n = 2 * (steps - 4)
+                rows.append({"rho": rho, "cache": cname, "cache_slots": C, "policy": pol,
+                             "overlap": ovl / (n * k), "hit_rate": hits / max(reqs, 1),
+                             "host_MB_per_layer_step": host / n / 1e6})
+                log(f"policy sweep rho {rho} {cname} {pol}: hit {rows[-1]['hit_rate']:.3f}")
+    owner.close()
+    stacks = {}
+    for pol, flag in (("exact", 0), ("dominance", m2c.FLAG_DOMINANT_HITS)):
+        r = run_stack(wl0, wl0.n_layers, 24, 8, 0, flag, 0, False, torch, m2c, W)
+        stacks[pol] = {"tokens_per_s": r["tokens_per_s"], "us_per_layer_step": r["us_per_layer_step"],
+                       "host_MB_per_layer_step": r["pipeline"]["fill_MB_per_layer_step"],
+                       "cache": r["pipeline"]["cache"]}
+        log(f"7B stack, {pol}: {r['tokens_per_s']:.1f} tokens/s")
+    return {"workload": wl0.name, "steps_per_point": steps, "points": rows, "stack_7b": stacks}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -399,154 +624,69 @@ def main():
         print(json.dumps({"batched_sweep": batched_sweep(min(args.steps, 56), args.warmup, torch,
                                                           m2c, W, only)}), flush=True)
         return
+    if args.policy_sweep:
+        print(json.dumps({"policy_sweep": policy_sweep(min(args.steps, 36), torch, m2c, W)}),
+              flush=True)
+        return
     if args.only_ffn:
         wl_f = W.WORKLOADS[args.only_ffn]
-        g = ffn_isolated(wl_f, args.ffn_layers if args.only_ffn == args.workload else args.target_layers,
-                         args.ffn_reps, torch, m2c, W, flags=ffn_flags)
+        g = ffn_isolated(wl_f, args.ffn_layers if args.only_ffn == args.workload
+                         else args.extra_layers, args.ffn_reps, torch, m2c, W, flags=ffn_flags)
         print(json.dumps({"ffn_isolated": g}), flush=True)
         return
     wl = W.WORKLOADS[args.workload]
     n_layers = args.layers or wl.n_layers
     k, n16, n8 = wl.counts()
     n4 = k - n16 - n8
-    steps_total = args.warmup + args.steps
-    t_setup = time.perf_counter()
-    layers, x_dev, ld0 = build_stack(wl, n_layers, steps_total, args.weight_sets, torch, m2c, W,
-                                     flags=ffn_flags)
-    log(f"setup {time.perf_counter() - t_setup:.1f} s")
-    d, d_ff = wl.d_model, wl.d_ff
-    info = layers[0].info
-    rb = info.record_bytes
-    ffn_bytes = n16 * rb[3] + n8 * rb[2] + n4 * rb[1] + 2 * d + 4 * d
-
-    main_s, aux_s, copy_s = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
-    ev_plan = [torch.cuda.Event() for _ in range(n_layers)]
-    ev_fill = [torch.cuda.Event() for _ in range(n_layers)]
-    ev_ffn = [torch.cuda.Event() for _ in range(n_layers)]
-    tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
-    # m2c_sparse_ffn adds into y (a residual stream): one zeroed row per
-    # layer-step, so every output is the plain FFN of its token
-    y = torch.zeros((steps_total, n_layers, d), dtype=torch.float32, device="cuda")
-    lag = min(2, n_layers)
-    timing = []  # (ffn_start, ffn_end, fill_start, fill_end) per timed layer-step
-
-    overlap_ev = []  # (aux start, aux end, fill start, fill end, ffn start, ffn end)
-
-    def step(t, timed, spans=False):
-        for l in range(n_layers):
-            f = t * n_layers + l
-            L = layers[l]
-            if f - lag >= 0:
-                aux_s.wait_event(ev_ffn[(f - lag) % n_layers])
-            x = x_dev[l, t % steps_total]
-            if spans:
-                sp = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
-                sp[0].record(aux_s)
-            L.predict_rank(x, 1, k, n16, n8, None, tiers[l], stream=aux_s)
-            L.cache_plan(tiers[l], 1, t, stream=aux_s)
-            if spans:
-                sp[1].record(aux_s)
-            ev_plan[l].record(aux_s)
-            copy_s.wait_event(ev_plan[l])
-            if timed:
-                ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-                ev[2].record(copy_s)
-            if spans:
-                sp[2].record(copy_s)
-            L.cache_fill(stream=copy_s)
-            if timed:
-                ev[3].record(copy_s)
-            if spans:
-                sp[3].record(copy_s)
-            ev_fill[l].record(copy_s)
-            main_s.wait_event(ev_fill[l])
-            if timed:
-                ev[0].record(main_s)
-            if spans:
-                sp[4].record(main_s)
-            L.sparse_ffn(x, 1, y[t % steps_total, l], stream=main_s)
-            if timed:
-                ev[1].record(main_s)
-                timing.append(ev)
-            if spans:
-                sp[5].record(main_s)
-                overlap_ev.append(sp)
-            ev_ffn[l].record(main_s)
-
-    for t in range(args.warmup):
-        step(t, False)
-    torch.cuda.synchronize()
-    st0 = [L.stats() for L in layers]
-    t0 = time.perf_counter()
-    for t in range(args.warmup, steps_total):
-        step(t, args.stage_events)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    st1 = [L.stats() for L in layers]
-    # A few more steps, untimed, with events around every stage: how much of
-    # the fills' time runs while predict / plan or the FFN runs on another
-    # stream (the events themselves delay the cross-stream waits a little, so
-    # they stay out of the timed steps).
-    # The aux stream (and through the events the other two) is held by a spin
-    # kernel while the host enqueues, so the extra calls do not space the
-    # stages out.
-    if args.overlap_steps:
-        hold_stream(torch, aux_s, 0.03 * args.overlap_steps)
-    for t in range(steps_total, steps_total + args.overlap_steps):
-        step(t, False, spans=True)
-    torch.cuda.synchronize()
-    overlap = stage_overlap(overlap_ev) if overlap_ev else None
-
-    ffn_ms = np.array([e[0].elapsed_time(e[1]) for e in timing]) if timing else None
-    fill_ms = np.array([e[2].elapsed_time(e[3]) for e in timing]) if timing else None
-    reqs = sum(b.req - a.req for a, b in zip(st0, st1))
-    hits = sum(b.hit - a.hit for a, b in zip(st0, st1))
-    refills = sum(b.refill - a.refill for a, b in zip(st0, st1))
-    bypass = sum(b.bypass - a.bypass for a, b in zip(st0, st1))
-    # bytes the fills read over the host link (fills derived on the GPU from a
-    # resident FP16 record read none)
-    fill_bytes = sum(b.host_bytes - a.host_bytes for a, b in zip(st0, st1))
-    derived_bytes = sum(b.fill_bytes - a.fill_bytes for a, b in zip(st0, st1)) - fill_bytes
-    n_ls = args.steps * n_layers
-    # host-link rate of the fills: from the stage events if recorded, else
-    # the fill bytes over the wall time (a lower bound: fills run back to
-    # back only when nothing else is on the critical path)
-    fill_avg_s = float(fill_ms.mean()) * 1e-3 if fill_ms is not None else wall / n_ls
-    fill_Bps = fill_bytes / n_ls / fill_avg_s
-    tokens_per_s = args.steps / wall
-
-    for L in layers:
-        L.close()
-    layers = []
+    weight_sets = args.weight_sets if args.weight_sets >= 0 else (
+        8 if wl.name == "llama2-70b" else 0)
+    flags = ffn_flags | (m2c.FLAG_DOMINANT_HITS if args.policy == "dominance" else 0)
+    r = run_stack(wl, n_layers, args.steps, args.warmup, weight_sets, flags, args.overlap_steps,
+                  args.stage_events, torch, m2c, W)
+    log(f"stack: {r['tokens_per_s']:.2f} tokens/s")
     log(f"isolated sparse FFN on {args.ffn_layers} {wl.name}-shaped layers")
     iso = ffn_isolated(wl, args.ffn_layers, args.ffn_reps, torch, m2c, W, flags=ffn_flags)
-    target = None
-    if args.target_workload:
-        log(f"isolated sparse FFN on {args.target_layers} {args.target_workload}-shaped layers")
-        target = ffn_isolated(W.WORKLOADS[args.target_workload], args.target_layers,
-                              args.ffn_reps, torch, m2c, W, flags=ffn_flags)
+    extra = None
+    if args.extra_workload and args.extra_workload != wl.name:
+        log(f"isolated sparse FFN on {args.extra_layers} {args.extra_workload}-shaped layers")
+        extra = ffn_isolated(W.WORKLOADS[args.extra_workload], args.extra_layers, args.ffn_reps,
+                             torch, m2c, W, flags=ffn_flags)
 
     cpu = None
     if args.cpu_seconds > 0:
         import oracle
         log("timing the oracle on the host")
-        cpu = cpu_baseline(wl, ld0, n_layers, args.cpu_seconds, oracle)
+        cpu = cpu_baseline(wl, r["ld0"], n_layers, args.cpu_seconds, oracle,
+                           oracle.POLICY_DOMINANCE if args.policy == "dominance"
+                           else oracle.POLICY_EXACT)
 
     # HBM bytes per call from the committed counter summary of this layer
     # shape, or None when the FFN kernels have changed since it was taken
     from paper_2410_14740_amd import rocprof_summary
-    ffn_traffic = None if args.deterministic_ffn else rocprof_summary.read_ffn_traffic(
-        os.path.join(ROOT, "profiles", f"sparse_ffn_{wl.name}_layer.md"))
+
+    def traffic(name):
+        return None if args.deterministic_ffn else rocprof_summary.read_ffn_traffic(
+            os.path.join(ROOT, "profiles", f"sparse_ffn_{name}_layer.md"))
+
     ffn_kind = ("three kernels (up, down, ordered reduce), deterministic" if args.deterministic_ffn
                 else "one launch (h tasks, then down tasks that wait on the h words)")
+    d, d_ff = wl.d_model, wl.d_ff
+
+    def roof(g, name, layers_cycled):
+        return {"bound": "hbm", "achieved": g["achieved_GBps"], "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s", "frac": g["achieved_GBps"] / PEAK_HBM_GBPS,
+                "traffic": traffic(name), "kernel": "m2c_sparse_ffn (ffn_fused_kernel)",
+                "workload": f"{name} layer shape, {layers_cycled} layers cycled",
+                "bytes_per_launch": g["bytes_per_launch"], "us_per_launch": g["us_avg"]}
+
     out = {
         "metric": METRIC,
-        "value": tokens_per_s,
+        "value": r["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": wall / args.steps * 1e3,
+        "ms_per_step": r["wall"] / args.steps * 1e3,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -555,40 +695,25 @@ def main():
         "config": {
             "workload": wl.name, "layers": n_layers, "d_model": d, "d_ff": d_ff,
             "pred_rank": wl.pred_rank, "k": k, "tiers_fp16_int8_int4": [n16, n8, n4],
-            "cache_slots": wl.cache_slots(), "batch": 1, "decode_steps": steps_total,
+            "cache_slots": wl.cache_slots(), "batch": 1,
+            "decode_steps": args.warmup + args.steps,
             "weights": "fp16 records with int8/int4 copies (group 128, fp16 scales), "
                        "pinned host store",
-            "distinct_weight_sets": args.weight_sets or n_layers,
+            "distinct_weight_sets": weight_sets or n_layers,
+            "cache_policy": "LRU, " + ("dominance hits" if args.policy == "dominance"
+                                       else "exact-tier hits"),
             "ffn": ffn_kind,
         },
-        "us_per_layer_step": wall / n_ls * 1e6,
-        "pipeline": {
-            "stage_events": bool(args.stage_events),
-            "ffn_us_avg": float(ffn_ms.mean()) * 1e3 if ffn_ms is not None else None,
-            "fill_us_avg": fill_avg_s * 1e6 if fill_ms is not None else None,
-            "fill_MB_per_layer_step": fill_bytes / n_ls / 1e6,
-            "derived_MB_per_layer_step": derived_bytes / n_ls / 1e6,
-            "cache": {"hit_rate": hits / max(reqs, 1), "refill_rate": refills / max(reqs, 1),
-                      "bypass_rate": bypass / max(reqs, 1)},
-            "overlap": overlap,
-        },
-        # the step's gather-GEMV (m2c_sparse_ffn: ffn_fused_kernel),
-        # algorithmic bytes per call over the per-call time of back-to-back calls
-        "roofline": {"bound": "hbm", "achieved": iso["achieved_GBps"], "peak": PEAK_HBM_GBPS,
-                     "unit": "GB/s", "frac": iso["achieved_GBps"] / PEAK_HBM_GBPS,
-                     "traffic": ffn_traffic, "kernel": "m2c_sparse_ffn (ffn_fused_kernel)",
-                     "workload": f"{wl.name} layer shape, {args.ffn_layers} layers cycled",
-                     "bytes_per_launch": iso["bytes_per_launch"], "us_per_launch": iso["us_avg"]},
-        "roofline_target_layer": None if target is None else {
-            "bound": "hbm", "achieved": target["achieved_GBps"], "peak": PEAK_HBM_GBPS,
-            "unit": "GB/s", "frac": target["achieved_GBps"] / PEAK_HBM_GBPS,
-            "workload": f"{target['workload']} layer shape, {args.target_layers} layers cycled",
-            "bytes_per_launch": target["bytes_per_launch"], "us_per_launch": target["us_avg"]},
+        "us_per_layer_step": r["us_per_layer_step"],
+        "pipeline": r["pipeline"],
+        # the step's gather-GEMV (m2c_sparse_ffn: ffn_fused_kernel) on this
+        # workload's layer shape: algorithmic bytes per call over the per-call
+        # time of back-to-back calls between one pair of HIP events
+        "roofline": roof(iso, wl.name, args.ffn_layers),
+        "roofline_extra_layer": None if extra is None else roof(extra, extra["workload"],
+                                                                 args.extra_layers),
         # the fills are bound by the host link, not by HBM
-        "host_link": {"kernel": "fill_kernel (device gather from pinned host memory)",
-                      "achieved": fill_Bps / 1e9, "peak": PEAK_HOST_LINK_GBPS, "unit": "GB/s",
-                      "frac": fill_Bps / 1e9 / PEAK_HOST_LINK_GBPS,
-                      "measured_over": "fill kernels" if fill_ms is not None else "wall time"},
+        "host_link": r["host_link"],
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

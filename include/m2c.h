@@ -85,8 +85,11 @@
  * slot_bytes = 6d bytes (an FP16 record). The required set R of a step is
  * every neuron with tier > 0 in some batch row, taken at the highest tier any
  * row asks for. The step is atomic: for i in R (ascending id)
- *   HIT     i is resident at the requested tier;
- *   REFILL  i is resident at another tier: it is refilled in its own slot;
+ *   HIT     i is resident at the requested tier (with M2C_FLAG_DOMINANT_HITS:
+ *           at the requested tier or above; the step then uses the resident
+ *           tier);
+ *   REFILL  i is resident at another tier (with M2C_FLAG_DOMINANT_HITS: a
+ *           lower one): it is refilled in its own slot;
  *   NEW     i is not resident.
  * Victims are the slots holding no neuron of R, ordered by (last use
  * ascending, slot ascending); never-used slots count as last use -1. The j-th
@@ -142,7 +145,14 @@ enum {
      kernels (h of every neuron, then the down projection by column slice and
      neuron group) whose neuron groups are added into y with fp32 atomics,
      so the summation order, and the last bits of y, vary from run to run. */
-  M2C_FLAG_DETERMINISTIC_FFN = 1
+  M2C_FLAG_DETERMINISTIC_FFN = 1,
+  /* Cache policy variant (Sec. 5.3 "Cache Policy"): a neuron resident at a
+     tier at or above the requested one is a HIT and the step uses it at its
+     resident tier (req_tier and the FFN then carry the resident tier); only
+     a resident tier below the requested one is a REFILL. The default is the
+     exact-tier policy: any other resident tier is a REFILL. With dominance
+     hits the output depends on the cache history, not only on the step. */
+  M2C_FLAG_DOMINANT_HITS = 2
 };
 
 /* Sizes that follow from a descriptor. */
@@ -311,8 +321,32 @@ m2c_status m2c_debug_read_slot(const m2c_layer* layer, int32_t slot, void* out, 
 m2c_status m2c_debug_read_tables(const m2c_layer* layer, int32_t* slot_of, int32_t* slot_key,
                                  uint8_t* slot_tier, int32_t* slot_last);
 
+/* Test support. Enqueues on `stream` a kernel that overwrites with 0xFF
+ * bytes every slot the fill of `plan` writes (slot_bytes each), except the
+ * slots whose INT8 / INT4 record the fill may make from the FP16 bytes
+ * already there (fill_from == 3). Enqueued right before m2c_cache_fill on the
+ * same stream, it makes ordering mistakes visible: an FFN that reads a slot
+ * before its fill completes reads 0xFF bytes (NaN as fp16, code -1 as
+ * INT8 / INT4 with a NaN scale), and a fill that starts while an earlier FFN
+ * still reads the slot corrupts that FFN's output. */
+m2c_status m2c_debug_poison_fill_slots(m2c_layer* layer, const void* plan, void* stream);
+
+/* Test support. polls > 0: the layer's one-launch batch-1 sparse FFN (d_model
+ * <= 8192, not deterministic) stops publishing its h values and its down
+ * tasks give up after `polls` polls, so that every later call takes the
+ * bounded-wait give-up path (h = 0, status word set, M2C_ERR_STATE from the
+ * next m2c_layer_stats) while every kernel still exits normally. polls == 0
+ * restores the normal behaviour. Host-side setting; affects launches made
+ * after the call. */
+m2c_status m2c_debug_ffn_withhold_h(m2c_layer* layer, int32_t polls);
+
 /* Message of the last error on this thread ("" if none). */
 const char* m2c_last_error(void);
+
+/* Identifier of the sources the library was built from (16 hex digits of a
+ * SHA-256 over the kernel sources and this header), so that a loader can
+ * refuse a library built from other sources. Static string, never NULL. */
+const char* m2c_build_id(void);
 
 #ifdef __cplusplus
 }

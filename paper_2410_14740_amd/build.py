@@ -6,6 +6,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import glob
+import hashlib
 import os
 import subprocess
 import sys
@@ -34,14 +35,31 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+def source_id() -> str:
+    """SHA-256 (first 16 hex digits) over every file the library is built
+    from: the kernels, their headers and the public header. The build bakes
+    it into the library (m2c_build_id), so a loader can tell a library built
+    from other sources."""
+    files = sorted(glob.glob(os.path.join(CSRC, "*")) +
+                   glob.glob(os.path.join(ROOT, "include", "*.h")))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     srcs = sources()
     objs = [os.path.join(BUILD_DIR, os.path.basename(s) + ".o") for s in srcs]
 
+    sid = source_id()
+
     def compile_one(pair):
         src, obj = pair
-        cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+        cmd = [HIPCC, *FLAGS, f'-DM2C_SOURCE_ID="{sid}"', "-c", src, "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"hipcc failed on {os.path.basename(src)}:\n{r.stdout}{r.stderr}")

@@ -458,7 +458,8 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
     const uint16_t* __restrict__ x, int d, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ work_slot, const uint8_t* __restrict__ slots, uint32_t sb,
     int cap, int n_slots, unsigned long long* __restrict__ gen,
-    unsigned long long* __restrict__ hw, int32_t* __restrict__ status, float* __restrict__ y) {
+    unsigned long long* __restrict__ hw, int32_t* __restrict__ status, float* __restrict__ y,
+    int withhold) {
   extern __shared__ uint4 xlds[];  // fused_lds_bytes(d)
   __shared__ FShared sh;
   const int tid = threadIdx.x;
@@ -526,16 +527,18 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
       const float h = sl >= 0 && sl < n_slots ? silu_mul(sa, sbv) : 0.0f;
       const unsigned long long word =
           ((unsigned long long)epoch << 32) | (unsigned long long)__float_as_uint(h);
-      __hip_atomic_store(hw + kc.lo + tid, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (withhold == 0)  // test support withholds the word to drive the give-up path
+        __hip_atomic_store(hw + kc.lo + tid, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   } else {
     // the h words of the run, polled after every data load has been issued
     float h = 0.0f;
     if (tid < n_items) {
       unsigned long long hv = load_word(hw + kc.lo + tid);
+      const int limit = withhold > 0 ? withhold : kFSpin;
       int spins = 0;
       while ((uint32_t)(hv >> 32) != epoch) {
-        if (++spins > kFSpin) {
+        if (++spins > limit) {
           atomicOr(status, M2C_STATUS_FFN_WAIT);
           hv = 0;
           break;
@@ -590,7 +593,8 @@ hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* counts,
   const size_t lds = fused_lds_bytes(d);
   hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, d, counts,
                      work_slot, L->slots, (uint32_t)L->info.slot_bytes, L->cap,
-                     L->desc.cache_slots + L->S, L->st.ffn_gen, L->st.ffn_hw, L->st.status, y);
+                     L->desc.cache_slots + L->S, L->st.ffn_gen, L->st.ffn_hw, L->st.status, y,
+                     L->ffn_withhold);
   return hipGetLastError();
 }
 

@@ -128,4 +128,34 @@ hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stre
   return hipGetLastError();
 }
 
+// Test support: 0xFF over every slot the fill of a plan writes, except the
+// slots a fill may derive from (fill_from == 3, INT8 / INT4), whose FP16
+// bytes the fill reads.
+__global__ __launch_bounds__(kFillThreads) void poison_kernel(const int32_t* __restrict__ counts,
+                                                              const uint8_t* __restrict__ fill_tier,
+                                                              const int32_t* __restrict__ fill_slot,
+                                                              const uint8_t* __restrict__ fill_from,
+                                                              uint8_t* __restrict__ slots,
+                                                              int64_t slot_bytes, int cap,
+                                                              int n_slots) {
+  int n = counts[M2C_CNT_FILL];
+  n = n < 0 ? 0 : n > cap ? cap : n;
+  const u32x4 ones = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+  for (int e = blockIdx.x; e < n; e += gridDim.x) {
+    const int t = fill_tier[e], slot = fill_slot[e];
+    if (slot < 0 || slot >= n_slots || (fill_from[e] == 3 && t < 3)) continue;
+    u32x4* dst = reinterpret_cast<u32x4*>(slots + (int64_t)slot * slot_bytes);
+    for (int v = threadIdx.x; v < (int)(slot_bytes >> 4); v += kFillThreads) dst[v] = ones;
+  }
+}
+
+hipError_t launch_poison_fill_slots(const m2c_layer* L, const uint8_t* plan, hipStream_t stream) {
+  const m2c_plan_layout& lay = L->layout;
+  hipLaunchKernelGGL(poison_kernel, dim3(kFillBlocks), dim3(kFillThreads), 0, stream,
+                     reinterpret_cast<const int32_t*>(plan + lay.counts), plan + lay.fill_tier,
+                     reinterpret_cast<const int32_t*>(plan + lay.fill_slot), plan + lay.fill_from,
+                     L->slots, (int64_t)L->info.slot_bytes, L->cap, L->desc.cache_slots + L->S);
+  return hipGetLastError();
+}
+
 }  // namespace m2c

@@ -49,7 +49,8 @@ __device__ __forceinline__ void thread_range(int n, int& lo, int& hi) {
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __restrict__ tier_map,
                                                             int B, int d_ff, int C, int cap,
-                                                            int step, DeviceState st, PlanPtrs P) {
+                                                            int step, int dom, DeviceState st,
+                                                            PlanPtrs P) {
   __shared__ unsigned long long scan64[kPlanThreads / 64 + 1];
   __shared__ uint32_t scan32[kPlanThreads / 64 + 1];
   __shared__ int sh_hit, sh_refill, sh_empty, sh_der[2];
@@ -73,9 +74,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
     }
     t = t > 3 ? 3 : t;  // codes above FP16 read as FP16
     if (t) {
+      const int s = st.slot_of[i];
+      if (dom && s >= 0 && st.slot_tier[s] > t) t = st.slot_tier[s];  // hit at the resident tier
       ++nreq;
       tiers += 1ull << (21 * (3 - t));
-      if (st.slot_of[i] < 0) ++nnew;
+      if (s < 0) ++nnew;
     }
   }
   unsigned long long tot;
@@ -112,11 +115,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(const uint8_t* __res
       }
       t = t > 3 ? 3 : t;
       if (!t) continue;
+      const int s = st.slot_of[i];
+      // the first sweep took the same step tier (slot_tier of a neuron's slot
+      // changes only below, by the thread that owns the neuron)
+      if (dom && s >= 0 && st.slot_tier[s] > t) t = st.slot_tier[s];
       P.req_ids[pos] = i;
       P.req_tier[pos] = (uint8_t)t;
       P.req_mask[pos] = m;
       st.work_pos[pos] = t == 3 ? r3++ : t == 2 ? r2++ : r1++;
-      const int s = st.slot_of[i];
       if (s >= 0) {
         const bool same = st.slot_tier[s] == t;
         P.req_hit[pos] = same ? 1 : 2;
@@ -332,7 +338,7 @@ __device__ __forceinline__ void neuron_tiers(const uint8_t* __restrict__ tm, int
 }
 
 __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
-    const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step,
+    const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step, int dom,
     DeviceState st, PlanPtrs P) {
   __shared__ uint8_t s_info[kPJ * kPlanThreads];  // tier | code << 2 (1 hit, 2 refill, 0 new)
   __shared__ uint32_t s_touch[kPJ * kPlanThreads / 32];  // slots touched this step
@@ -372,7 +378,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
       const bool valid = j < NJ && i < d_ff;
       const bool req = valid && t[g] > 0;
       const bool res = req && sl[g] >= 0;
-      const bool hit = res && old[g] == t[g];
+      const bool hit = res && (old[g] == t[g] || (dom && old[g] > t[g]));
+      if (hit) t[g] = old[g];  // the step tier of a hit is the resident tier
       if (valid) s_info[i] = req ? (uint8_t)(t[g] | ((hit ? 1 : res ? 2 : 0) << 2)) : 0;
       if (res) atomicOr(&s_touch[sl[g] >> 5], 1u << (sl[g] & 31));
       const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
@@ -632,12 +639,13 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
   P.evicted_ids = reinterpret_cast<int32_t*>(plan + lay.evicted_ids);
   P.work_slot = reinterpret_cast<int32_t*>(plan + lay.work_slot);
   P.work_mask = reinterpret_cast<uint32_t*>(plan + lay.work_mask);
+  const int dom = (L->desc.flags & M2C_FLAG_DOMINANT_HITS) ? 1 : 0;
   if (L->desc.d_ff <= kPJ * kPlanThreads)
     hipLaunchKernelGGL(plan_fast_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
-                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, L->st, P);
+                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, dom, L->st, P);
   else
     hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
-                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, L->st, P);
+                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, dom, L->st, P);
   return hipGetLastError();
 }
 

@@ -85,7 +85,7 @@ m2c_status check_desc(const m2c_layer_desc* D, int* S_out, int* cap_out) {
   if (S < need)
     return fail(M2C_ERR_INVALID_ARG, "staging_slots %d: at least %d are needed (or -1)",
                 D->staging_slots, need);
-  if (D->flags & ~M2C_FLAG_DETERMINISTIC_FFN)
+  if (D->flags & ~(M2C_FLAG_DETERMINISTIC_FFN | M2C_FLAG_DOMINANT_HITS))
     return fail(M2C_ERR_INVALID_ARG, "flags 0x%x: unknown bits", D->flags);
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || D->device < 0 || D->device >= ndev)
@@ -355,6 +355,11 @@ int64_t m2c_record_bytes(int32_t d_model, int32_t tier) {
 
 const char* m2c_last_error(void) { return g_err; }
 
+#ifndef M2C_SOURCE_ID
+#define M2C_SOURCE_ID "unknown"
+#endif
+const char* m2c_build_id(void) { return M2C_SOURCE_ID; }
+
 m2c_status m2c_layer_create(const m2c_layer_desc* desc, const uint16_t* w_gate,
                             const uint16_t* w_up, const uint16_t* w_down, const uint16_t* pred_a,
                             const uint16_t* pred_b, const float* score_bias, m2c_layer** out) {
@@ -565,6 +570,21 @@ m2c_status m2c_debug_read_slot(const m2c_layer* L, int32_t slot, void* out, size
   HIPOK(hipMemcpy(out, L->slots + (int64_t)slot * L->info.slot_bytes, bytes,
                   hipMemcpyDeviceToHost),
         "read slot");
+  return M2C_OK;
+}
+
+m2c_status m2c_debug_poison_fill_slots(m2c_layer* L, const void* plan, void* stream) {
+  if (!L || !plan) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  DeviceGuard g(L->desc.device);
+  HIPOK(m2c::launch_poison_fill_slots(L, (const uint8_t*)plan, (hipStream_t)stream),
+        "poison launch");
+  return M2C_OK;
+}
+
+m2c_status m2c_debug_ffn_withhold_h(m2c_layer* L, int32_t polls) {
+  if (!L) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (polls < 0) return fail(M2C_ERR_INVALID_ARG, "polls %d: need >= 0", polls);
+  L->ffn_withhold = polls;
   return M2C_OK;
 }
 

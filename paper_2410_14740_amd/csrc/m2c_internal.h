@@ -79,6 +79,7 @@ struct m2c_layer {
   int ffn_grid = 0;  // workgroups of the one-launch FFN
   m2c::DeviceState st;
   int64_t last_step = -1;
+  int ffn_withhold = 0;  // test support: > 0 = h words withheld, polls before giving up
 };
 
 namespace m2c {
@@ -100,6 +101,7 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
                        hipStream_t stream);
 hipError_t launch_reset(m2c_layer* L, hipStream_t stream);
 hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
+hipError_t launch_poison_fill_slots(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
 hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
                       hipStream_t stream);
 hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan,

@@ -36,6 +36,7 @@ class M2CError(RuntimeError):
 
 
 FLAG_DETERMINISTIC_FFN = 1
+FLAG_DOMINANT_HITS = 2
 
 
 class LayerDesc(ctypes.Structure):
@@ -75,7 +76,8 @@ _lib = None
 
 
 def load(path: str = LIB_PATH):
-    """Load libm2c.so. There is no fallback: a missing library is an error."""
+    """Load libm2c.so. There is no fallback: a missing library, or one built
+    from other sources than the ones in the tree, is an error."""
     global _lib
     if _lib is not None:
         return _lib
@@ -103,14 +105,32 @@ def load(path: str = LIB_PATH):
         "m2c_debug_read_record": (I32, [P, I32, I32, P, S]),
         "m2c_debug_read_slot": (I32, [P, I32, P, S]),
         "m2c_debug_read_tables": (I32, [P, P, P, P, P]),
+        "m2c_debug_poison_fill_slots": (I32, [P, P, P]),
+        "m2c_debug_ffn_withhold_h": (I32, [P, I32]),
         "m2c_last_error": (ctypes.c_char_p, []),
+        "m2c_build_id": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
+    from . import build as _build
+    want, got = _build.source_id(), lib.m2c_build_id().decode()
+    if got != want:
+        raise ImportError(f"{path} was built from other sources (build id {got}, sources {want}); "
+                          "run `python -m paper_2410_14740_amd.build`")
     _lib = lib
     return lib
+
+
+def is_current(path: str = LIB_PATH) -> bool:
+    """True when the library exists and was built from the sources in the tree
+    (checked without loading it: the build id string is in the file)."""
+    if not os.path.exists(path):
+        return False
+    from . import build as _build
+    with open(path, "rb") as f:
+        return _build.source_id().encode() in f.read()
 
 
 def _check(status: int):
@@ -237,6 +257,18 @@ def m2c_debug_read_tables(layer, d_ff: int, C: int):
     _check(load().m2c_debug_read_tables(layer, slot_of.ctypes.data, key.ctypes.data,
                                         tier.ctypes.data, last.ctypes.data))
     return slot_of, key[:C], tier[:C], last[:C]
+
+
+def m2c_debug_poison_fill_slots(layer, plan, stream=None):
+    _check(load().m2c_debug_poison_fill_slots(layer, _ptr(plan), _stream(stream)))
+
+
+def m2c_debug_ffn_withhold_h(layer, polls: int):
+    _check(load().m2c_debug_ffn_withhold_h(layer, polls))
+
+
+def m2c_build_id() -> str:
+    return load().m2c_build_id().decode()
 
 
 def m2c_last_error() -> str:

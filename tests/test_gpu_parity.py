@@ -11,7 +11,8 @@ import oracle
 from paper_2410_14740_amd import m2c
 from paper_2410_14740_amd import workloads as W
 
-from helpers import FFN_TOL, oracle_ffn, r8_errors, say, subset_records
+from helpers import (FFN_TOL, derived_fills, oracle_ffn, r8_errors, say, subset_records,
+                     work_order)
 
 pytestmark = pytest.mark.gpu
 
@@ -81,10 +82,17 @@ def test_predict_and_tiers_bit_exact(name, d, d_ff, r, seed, batch):
 
 
 def _compare_plan(g, o, step):
+    """Every field of the library's plan against the oracle's: the method's
+    lists and counts, plus the FFN work order and the derived-fill count the
+    library adds (both follow from the oracle's lists)."""
     for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "fill_ids",
-                "fill_tier", "fill_slot", "fill_from", "evicted_ids", "work_slot", "work_mask"):
+                "fill_tier", "fill_slot", "fill_from", "evicted_ids"):
         assert np.array_equal(g[key], o[key]), f"step {step}: plan field {key} differs"
-    assert np.array_equal(g["counts"][:14], o["counts"][:14]), f"step {step}: counts differ"
+    assert np.array_equal(g["counts"][:13], o["counts"][:13]), f"step {step}: counts differ"
+    ws, wm = work_order(o)
+    assert np.array_equal(g["work_slot"], ws), f"step {step}: FFN work order differs"
+    assert np.array_equal(g["work_mask"], wm), f"step {step}: FFN work masks differ"
+    assert g["counts"][m2c.CNT_FILL_DERIVED] == derived_fills(o), f"step {step}: derived count"
 
 
 def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flags=0):
@@ -92,7 +100,9 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flag
     step, comparing every stage."""
     d_ff = ld.d_ff
     L = _layer(ld, k, C, max_batch=batch, flags=flags)
-    cache = oracle.LRUCache(d_ff, C, L.info.staging_slots)
+    policy = (oracle.POLICY_DOMINANCE if flags & m2c.FLAG_DOMINANT_HITS
+              else oracle.POLICY_EXACT)
+    cache = oracle.LRUCache(d_ff, C, L.info.staging_slots, policy)
     tiers = torch.empty((batch, d_ff), dtype=torch.uint8, device="cuda")
     y = torch.empty((batch, ld.d_model), dtype=torch.float32, device="cuda")
     stats = np.zeros(16, np.int64)
@@ -115,6 +125,7 @@ def _run_steps(ld, steps, k, n16, n8, C, batch=1, check_ffn=True, label="", flag
         g = L.read_plan()
         _compare_plan(g, o, t)
         stats += o["counts"]
+        stats[13] += derived_fills(o)
         slot_of, key, stier, last = m2c.m2c_debug_read_tables(L.handle, d_ff, C)
         assert np.array_equal(slot_of, cache.slot_of)
         assert np.array_equal(key, cache.slot_key[:C])
@@ -387,31 +398,146 @@ def test_shared_store_layers():
     L1.close()
 
 
+@pytest.mark.timeout(900)
 def test_llama70b_layer_shape():
     """One layer at the 70B shape (d 8192, d_ff 28672, rank 512, k 2867,
     tiers 286/860/1721, C = k): scores, tiers, plans and tables bit-exact,
-    every FFN output within tolerance, over three steps."""
+    every FFN output within tolerance, over eight steps (C = k: every step
+    evicts what the previous token used and the new one does not)."""
     wl = W.WORKLOADS["llama2-70b"]
     say("70B layer: drawing weights")
-    ld = W.workload_layer(wl, 0, steps=3)
+    ld = W.workload_layer(wl, 0, steps=8)
     k, n16, n8 = wl.counts()
-    worst, _ = _run_steps(ld, 3, k, n16, n8, wl.cache_slots(), label="70B layer")
+    worst, _ = _run_steps(ld, 8, k, n16, n8, wl.cache_slots(), label="70B layer")
     say(f"70B layer worst FFN error {worst:.2e}")
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["llama2-7b", "llama2-13b"])
 def test_llama7b_13b_layer_shapes(name):
     """One layer at the 7B shape (d 4096, d_ff 11008, rank 256, k 2201 =
     220/880/1101, C 3302) and at the 13B shape (d 5120 -- not a power of two:
     padded lanes in every gate/up unit -- d_ff 13824, k 2073 = 414/622/1037,
-    C 2764), batch 1, over four steps: scores, tiers, plans, slot tables and
-    derived records bit-exact, every FFN output within tolerance."""
+    C 2764), batch 1, over sixteen steps (the LRU reaches steady-state
+    eviction): scores, tiers, plans, slot tables and derived records
+    bit-exact, every FFN output within tolerance."""
     wl = W.WORKLOADS[name]
     say(f"{name} layer: drawing weights")
-    ld = W.workload_layer(wl, 0, steps=4)
+    ld = W.workload_layer(wl, 0, steps=16)
     k, n16, n8 = wl.counts()
-    worst, _ = _run_steps(ld, 4, k, n16, n8, wl.cache_slots(), label=f"{name} layer")
+    worst, _ = _run_steps(ld, 16, k, n16, n8, wl.cache_slots(), label=f"{name} layer")
     say(f"{name} layer worst FFN error {worst:.2e}")
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("cap,mix", [((1, 10), "10/40/50"), ((1, 10), "fp16"), ((3, 5), "fp16")])
+def test_batched_llama7b_b8_sweep_points(cap, mix):
+    """More points of the batch-8 sweep at full shape: C = 10% of d_ff (most
+    of the union bypasses through staging slots) with mixed tiers and all
+    FP16, and C = 60% all FP16; two steps each."""
+    wl = W.WORKLOADS["llama2-7b-b8"]
+    say(f"7B batch-8 C={cap} {mix}: drawing weights")
+    ld = W.workload_layer(wl, 0, steps=2)
+    k, n16, n8 = wl.counts()
+    if mix == "fp16":
+        n16, n8 = k, 0
+    C = wl.d_ff * cap[0] // cap[1]
+    worst, _ = _run_steps(ld, 2, k, n16, n8, C, batch=wl.batch, label=f"7B b8 C={C} {mix}")
+    say(f"7B batch-8 C={C} {mix} worst FFN error {worst:.2e}")
+
+
+@pytest.mark.parametrize("batch", [1, 4])
+def test_no_cache_slots_everything_bypasses(batch):
+    """C = 0: every active neuron is a BYPASS filled into a staging slot each
+    step, nothing is retained."""
+    ld = W.make_layer(71, 0, 512, 900, 32, 4, rhos=(0.8, 0.5, 0.95, 0.7)[:batch])
+    k = 150
+    n16, n8 = _counts(k, (1, 5), (3, 10))
+    worst, _ = _run_steps(ld, 4, k, n16, n8, C=0, batch=batch, label=f"C=0 B={batch}")
+    say(f"C=0 batch {batch} worst FFN error {worst:.2e}")
+
+
+def test_wide_d_ff_general_kernels():
+    """d_ff above 32768 runs the general select and plan kernels (the
+    register select and the ballot plan take d_ff <= 32768): tiers, plans and
+    tables bit-exact, FFN within tolerance, over four steps with evictions."""
+    ld = W.make_layer(83, 0, 256, 40000, 16, 4, rhos=(0.7,))
+    k = 3000
+    n16, n8 = _counts(k, (1, 10), (3, 10))
+    worst, _ = _run_steps(ld, 4, k, n16, n8, C=2500, label="d_ff=40000")
+    say(f"d_ff=40000 worst FFN error {worst:.2e}")
+
+
+def test_wide_d_ff_general_kernels_batched_dominance():
+    ld = W.make_layer(84, 0, 256, 36000, 16, 3, rhos=(0.7, 0.9))
+    k = 1200
+    n16, n8 = _counts(k, (1, 5), (3, 10))
+    _run_steps(ld, 3, k, n16, n8, C=1500, batch=2, flags=m2c.FLAG_DOMINANT_HITS,
+               label="d_ff=36000 B=2 dominance")
+
+
+@pytest.mark.parametrize("batch,C", [(1, 200), (4, 200), (1, 2752)])
+def test_dominant_hits_policy(batch, C):
+    """Dominance hits (a neuron resident at a tier at or above the requested
+    one is a hit at its resident tier): plans, step tiers, tables and the FFN
+    over the resident records against the oracle's dominance policy, with
+    evictions and bypasses (C = 200) and with everything resident."""
+    ld = W.make_layer(W.WORKLOADS["tiny"].seed, 5, 1024, 2752, 128, 10,
+                      rhos=(0.8, 0.5, 0.95, 0.7)[:batch])
+    k = 688
+    n16, n8 = _counts(k)
+    worst, _ = _run_steps(ld, 10, k, n16, n8, C=C, batch=batch, flags=m2c.FLAG_DOMINANT_HITS,
+                          label=f"dominance B={batch} C={C}")
+    say(f"dominance B={batch} C={C} worst FFN error {worst:.2e}")
+
+
+@pytest.mark.timeout(900)
+def test_dominant_hits_llama7b_layer():
+    """Dominance hits on the 7B-shaped layer (C = 30%) over eight steps."""
+    wl = W.WORKLOADS["llama2-7b"]
+    say("7B layer, dominance: drawing weights")
+    ld = W.workload_layer(wl, 1, steps=8)
+    k, n16, n8 = wl.counts()
+    worst, _ = _run_steps(ld, 8, k, n16, n8, wl.cache_slots(), flags=m2c.FLAG_DOMINANT_HITS,
+                          label="7B layer dominance")
+    say(f"7B dominance worst FFN error {worst:.2e}")
+
+
+def test_ffn_wait_give_up_is_reported():
+    """The one-launch FFN's bounded wait: with its h values withheld (test
+    support), every down task gives up after a few polls and exits, the call's
+    output misses the down projection, m2c_layer_stats reports M2C_ERR_STATE
+    once and clears it, and the next normal call is correct again."""
+    ld = W.make_layer(44, 0, 1024, 2752, 128, 3)
+    k = 688
+    n16, n8 = _counts(k)
+    L = _layer(ld, k, 1376)
+    tiers = torch.empty((1, ld.d_ff), dtype=torch.uint8, device="cuda")
+    x = _x16(ld, 0)
+    L.predict_rank(x, 1, k, n16, n8, None, tiers)
+    L.cache_plan(tiers, 1, 0)
+    L.cache_fill()
+    y = torch.zeros((1, ld.d_model), dtype=torch.float32, device="cuda")
+    say("give-up: withheld h values")
+    m2c.m2c_debug_ffn_withhold_h(L.handle, 16)
+    L.sparse_ffn(x, 1, y)
+    torch.cuda.synchronize()
+    assert not y.cpu().numpy().any()  # every down task took h = 0
+    with pytest.raises(m2c.M2CError) as e:
+        L.stats()
+    assert e.value.status == m2c.M2C_ERR_STATE
+    L.stats()  # reported once, then cleared
+    m2c.m2c_debug_ffn_withhold_h(L.handle, 0)
+    plan = L.read_plan()
+    y_ref = oracle_ffn(ld, ld.x[0], plan["req_ids"], plan["req_tier"])[0]
+    for t in range(2):
+        say(f"give-up: normal call {t}")
+        y.zero_()
+        L.sparse_ffn(x, 1, y)
+        torch.cuda.synchronize()
+        assert r8_errors(y.cpu().numpy()[0], y_ref).max() <= FFN_TOL
+    L.stats()
+    L.close()
 
 
 @pytest.mark.parametrize("d,d_ff", [(1024, 2752), (4096, 3000), (8192, 3000)])

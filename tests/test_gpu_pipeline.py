@@ -1,0 +1,131 @@
+"""The decode schedule the benchmark times (paper_2410_14740_amd.pipeline:
+predict + plan on an aux stream, fills on a copy stream, the FFN on the main
+stream, cross-stream events with a look-ahead lag) against the oracle.
+
+Every layer-step's plan (as the FFN saw it: copied on the main stream right
+after the FFN), FFN output, the final slot tables and the layer counters are
+compared with the oracle. The race variants make ordering mistakes visible:
+
+  * each stream is held by a spin kernel of a seeded random length before its
+    stage, so the stages of different layer-steps are pushed against each
+    other in many orders;
+  * every slot a fill writes is overwritten with 0xFF bytes on the copy
+    stream right before the fill: an FFN that read a slot before its fill
+    completed would read NaN, and a fill (or its poison) that started while
+    an earlier FFN still read the slot would corrupt that FFN's output.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2410_14740_amd import m2c
+from paper_2410_14740_amd import pipeline
+from paper_2410_14740_amd import workloads as W
+
+from helpers import FFN_TOL, derived_fills, oracle_ffn, r8_errors, say, work_order
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+class _Hooks:
+    """Held streams, poisoned fill slots and the plan archive."""
+
+    def __init__(self, layers, archive, hold, poison, seed):
+        self.layers = layers
+        self.archive = archive
+        self.hold = hold
+        self.poison = poison
+        self.rng = np.random.default_rng(seed)
+
+    def _spin(self, s):
+        if self.hold:
+            cycles = int(self.rng.integers(20_000, 400_000))  # about 10 to 200 us
+            with torch.cuda.stream(s):
+                torch.cuda._sleep(cycles)
+
+    def before_predict(self, l, t, s):
+        self._spin(s)
+
+    def before_fill(self, l, t, s):
+        self._spin(s)
+        if self.poison:
+            L = self.layers[l]
+            m2c.m2c_debug_poison_fill_slots(L.handle, L.plan, s)
+
+    def before_ffn(self, l, t, s):
+        self._spin(s)
+
+    def after_ffn(self, l, t, s):
+        with torch.cuda.stream(s):
+            self.archive[t, l].copy_(self.layers[l].plan)
+
+
+def _check_plan(L, raw, o, where):
+    g = L.read_plan(plan=raw)
+    for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "fill_ids", "fill_tier",
+                "fill_slot", "fill_from", "evicted_ids"):
+        assert np.array_equal(g[key], o[key]), f"{where}: plan field {key} differs"
+    assert np.array_equal(g["counts"][:13], o["counts"][:13]), f"{where}: counts differ"
+    ws, wm = work_order(o)
+    assert np.array_equal(g["work_slot"], ws) and np.array_equal(g["work_mask"], wm), \
+        f"{where}: FFN work order differs"
+    assert g["counts"][m2c.CNT_FILL_DERIVED] == derived_fills(o), f"{where}: derived count"
+
+
+@pytest.mark.parametrize("n_layers,lag,hold,poison,flags", [
+    (4, 2, False, False, 0),
+    (4, 2, True, True, 0),
+    (2, 1, True, True, 0),
+    (3, 2, True, True, m2c.FLAG_DOMINANT_HITS),
+])
+def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
+    d, d_ff, r, steps = 512, 1400, 32, 12
+    k = 350
+    n16, n8 = k // 10, (k // 2) - k // 10
+    C = 250  # below k: evictions and bypasses through staging slots every step
+    desc = m2c.make_desc(d, d_ff, r, k, C, flags=flags)
+    policy = oracle.POLICY_DOMINANCE if flags & m2c.FLAG_DOMINANT_HITS else oracle.POLICY_EXACT
+    lds = [W.make_layer(900 + n_layers, l, d, d_ff, r, steps, rhos=(0.8,)) for l in range(n_layers)]
+    layers = [m2c.Layer(desc, ld) for ld in lds]
+    x = torch.stack([torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16)
+                     for ld in lds]).cuda()  # [layer][step][d]
+    y = torch.zeros((steps, n_layers, d), dtype=torch.float32, device="cuda")
+    tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
+    archive = torch.empty((steps, n_layers, layers[0].info.plan_bytes), dtype=torch.uint8,
+                          device="cuda")
+    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=lag)
+    hooks = _Hooks(layers, archive, hold, poison, seed=n_layers * 10 + lag)
+    torch.cuda.synchronize()
+    say(f"pipeline layers={n_layers} lag={lag} hold={hold} poison={poison} flags={flags}: enqueue")
+    for t in range(steps):
+        sched.step(t, lambda l: x[l, t], lambda l: y[t, l], hooks=hooks)
+    torch.cuda.synchronize()
+    say("pipeline: compare with the oracle")
+    yg = y.cpu().numpy()
+    arch = archive.cpu()
+    worst = 0.0
+    for l, (L, ld) in enumerate(zip(layers, lds)):
+        cache = oracle.LRUCache(d_ff, C, L.info.staging_slots, policy)
+        tot = np.zeros(16, np.int64)
+        for t in range(steps):
+            _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
+            tm, _ = oracle.select_tiers(s, k, n16, n8)
+            o = cache.plan(tm, t)
+            tot += o["counts"]
+            _check_plan(L, arch[t, l], o, f"layer {l} step {t}")
+            y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"])[0]
+            err = r8_errors(yg[t, l], y_ref).max()
+            worst = max(worst, err)
+            assert err <= FFN_TOL, f"layer {l} step {t}: FFN error {err:.3e}"
+        slot_of, key, stier, last = m2c.m2c_debug_read_tables(L.handle, d_ff, C)
+        assert np.array_equal(slot_of, cache.slot_of) and np.array_equal(key, cache.slot_key[:C])
+        assert np.array_equal(stier, cache.slot_tier[:C]) and np.array_equal(last, cache.slot_last[:C])
+        st = L.stats()  # raises if a plan overflowed or an FFN gave up waiting
+        assert (st.plans, st.req, st.hit, st.refill, st.new_, st.bypass) == (
+            steps, tot[0], tot[1], tot[2], tot[3], tot[4])
+        assert st.bypass > 0 and st.evict > 0
+    say(f"pipeline worst FFN error {worst:.2e}")
+    for L in layers:
+        L.close()
