@@ -79,6 +79,19 @@ def parse_args():
     p.add_argument("--only-ffn", default="", metavar="WORKLOAD",
                    help="run only the isolated sparse-FFN measurement on this layer shape "
                         "(for profiling)")
+    p.add_argument("--only-predict", default="", metavar="WORKLOAD",
+                   help="run only the isolated predictor + top-k measurement on this layer shape")
+    p.add_argument("--fill-sweep", action="store_true",
+                   help="only the host-to-HBM transfer sweep: gather kernel vs per-record "
+                        "hipMemcpyAsync vs one bulk copy, against the number of records")
+    p.add_argument("--ssd-tier", action="store_true",
+                   help="only the SSD -> DRAM tier measurement on the 7B-shaped stack")
+    p.add_argument("--ssd-dir", default=os.environ.get("TMPDIR", "/tmp"),
+                   help="directory of the layer store file")
+    p.add_argument("--ssd-sets", type=int, default=4)
+    p.add_argument("--ssd-fixed", type=int, default=4)
+    p.add_argument("--ssd-slots", type=int, default=8)
+    p.add_argument("--ssd-lookahead", type=int, default=2)
     p.add_argument("--batch-sweep", action="store_true",
                    help="only the batched-decode workload (7B-shaped layer, batch 8): LRU capacity "
                         "10/30/60%% x tiers 10/40/50 or all FP16, one JSON line")
@@ -327,6 +340,111 @@ def ffn_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
     return {"workload": wl.name, "layers_cycled": n_layers, "launches": len(calls),
             "us_avg": avg * 1e6, "bytes_per_launch": nbytes, "achieved_GBps": nbytes / avg / 1e9,
             "frac_of_peak": nbytes / avg / 1e9 / PEAK_HBM_GBPS, "host_hidden": bool(covered)}
+
+
+def predict_isolated(wl, n_layers, reps, torch, m2c, W):
+    """m2c_predict_rank (predictor z and s kernels, then the top-k select)
+    alone on `n_layers` layers of workload `wl`'s shape (their predictors
+    exceed the Infinity Cache for the 70B shape), back to back on one stream.
+    Algorithmic bytes per call: 2 (r d + d_ff r) of predictor weights, 2 d of x,
+    4 d_ff of scores written and read by the select, d_ff of tier map."""
+    k, n16, n8 = wl.counts()
+    d, d_ff, r = wl.d_model, wl.d_ff, wl.pred_rank
+    desc = m2c.make_desc(d, d_ff, r, k, 0)
+    layers = []
+    for l in range(n_layers):
+        ld = W.workload_layer(wl, l, steps=1, draw_weights=(l == 0))
+        layers.append((m2c.Layer(desc, ld, weights_of=layers[0][0] if l else None),
+                       torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16).cuda()))
+    tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream()
+    calls = [(lambda L=L, x=x: L.predict_rank(x[0], 1, k, n16, n8, None, tiers, stream=s))
+             for _ in range(reps) for L, x in layers]
+    for fn in calls[:n_layers]:
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for fn in calls[:n_layers]:
+        fn()
+    torch.cuda.synchronize()
+    per_call = (time.perf_counter() - t0) / n_layers
+    ms, covered = timed_back_to_back(torch, s, calls, per_call * len(calls) * 10 + 0.05)
+    nbytes = 2 * (r * d + d_ff * r) + 2 * d + 4 * d_ff * 2 + d_ff
+    for L, _ in layers:
+        L.close()
+    return {"workload": wl.name, "layers_cycled": n_layers, "launches": len(calls),
+            "us_avg": ms * 1e3, "bytes_per_call": nbytes,
+            "achieved_GBps": nbytes / (ms * 1e-3) / 1e9, "host_hidden": bool(covered)}
+
+
+def fill_sweep(torch, m2c, W):
+    """Host-to-HBM transfer rate against the size of a transfer (the analog of
+    the paper's Fig. 5, transfer time and bandwidth against tensor size), on
+    the 70B record sizes: for n records of one tier, n in 1 .. 2048,
+      gather  m2c_cache_fill of a plan with n NEW neurons (one launch of the
+              device gather kernel over the pinned host store);
+      memcpy  n hipMemcpyAsync calls of one record each, pinned host to
+              scattered slots of a device arena (the neuron-level copies the
+              paper issues on its streams);
+      bulk    one hipMemcpyAsync of the same n records' bytes, contiguous
+              (the copy engine's rate on large transfers).
+    Each is timed with HIP events on one stream, averaged over repetitions."""
+    wl = W.WORKLOADS["llama2-70b"]
+    d, d_ff, r = wl.d_model, 4096, 8
+    ld = W.make_layer(wl.seed + 7, 0, d, d_ff, r, 1, sigma_w=wl.sigma_w)
+    desc = m2c.make_desc(d, d_ff, r, 2048, 2048)
+    L = m2c.Layer(desc, ld)
+    s = torch.cuda.current_stream()
+    rows = []
+    host = torch.empty(2048 * 6 * d, dtype=torch.uint8, pin_memory=True)
+    arena = torch.empty(4096 * 6 * d, dtype=torch.uint8, device="cuda")
+    perm = np.random.default_rng(3).permutation(4096)
+    for tier in (3, 2, 1):
+        rb = L.info.record_bytes[tier]
+        for n in (1, 4, 16, 64, 256, 1024, 2048):
+            reps = max(2, min(50, 4096 // n))
+            tm = np.zeros((1, d_ff), np.uint8)
+            tm[0, :n] = tier
+            tmd = torch.from_numpy(tm).cuda()
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            tot = 0.0
+            for q in range(reps):
+                L.reset_cache(stream=s)
+                L.cache_plan(tmd, 1, 0, stream=s)
+                ev[0].record(s)
+                L.cache_fill(stream=s)
+                ev[1].record(s)
+                torch.cuda.synchronize()
+                tot += ev[0].elapsed_time(ev[1])
+            g_ms = tot / reps
+            # per-record copies into scattered slots of the arena
+            tot = 0.0
+            for q in range(reps):
+                ev[0].record(s)
+                for j in range(n):
+                    dst = int(perm[j]) * 6 * d
+                    arena[dst:dst + rb].copy_(host[j * rb:(j + 1) * rb], non_blocking=True)
+                ev[1].record(s)
+                torch.cuda.synchronize()
+                tot += ev[0].elapsed_time(ev[1])
+            m_ms = tot / reps
+            tot = 0.0
+            for q in range(reps):
+                ev[0].record(s)
+                arena[:n * rb].copy_(host[:n * rb], non_blocking=True)
+                ev[1].record(s)
+                torch.cuda.synchronize()
+                tot += ev[0].elapsed_time(ev[1])
+            b_ms = tot / reps
+            nb = n * rb
+            rows.append({"tier": tier, "record_bytes": rb, "records": n, "bytes": nb,
+                         "gather_us": g_ms * 1e3, "gather_GBps": nb / g_ms / 1e6,
+                         "memcpy_us": m_ms * 1e3, "memcpy_GBps": nb / m_ms / 1e6,
+                         "bulk_us": b_ms * 1e3, "bulk_GBps": nb / b_ms / 1e6})
+            log(f"fill sweep tier {tier} n {n}: gather {rows[-1]['gather_GBps']:.1f} GB/s, "
+                f"memcpy {rows[-1]['memcpy_GBps']:.1f}, bulk {rows[-1]['bulk_GBps']:.1f}")
+    L.close()
+    return {"d_model": d, "rows": rows}
 
 
 def batched_sweep(steps, warmup, torch, m2c, W, only=None):
@@ -590,6 +708,80 @@ def policy_sweep(steps, torch, m2c, W):
     return {"workload": wl0.name, "steps_per_point": steps, "points": rows, "stack_7b": stacks}
 
 
+def ssd_tier(args, torch, m2c, W):
+    """The SSD -> DRAM tier (Sec. 5.4) on the 7B-shaped stack: the layers'
+    neuron stores in a file (`--ssd-sets` distinct weight sets, layer l reads
+    set l mod sets, so every load is a real read of a whole layer), a pinned
+    two-level DRAM cache (`--ssd-fixed` layers in the fixed area,
+    `--ssd-slots` dynamic slots, look-ahead `--ssd-lookahead`, direct I/O),
+    and the decode pipeline reading every fill through the cache. Reports
+    tokens/s, the file read rate, how long fills waited for their layer, and
+    the DRAM the cache holds against all layers in DRAM."""
+    from paper_2410_14740_amd import pipeline
+    wl = W.WORKLOADS["llama2-7b"]
+    n_layers = args.layers or wl.n_layers
+    k, n16, n8 = wl.counts()
+    C = wl.cache_slots()
+    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C)
+    sets = args.ssd_sets
+    steps = args.warmup + args.steps
+    path = os.path.join(args.ssd_dir, f"m2c_stores_{os.getpid()}.bin")
+    offs, off = [], 0
+    t0 = time.perf_counter()
+    for q in range(sets):
+        ld = W.workload_layer(wl, q, steps=1)
+        o = m2c.Layer(desc, ld)
+        offs.append(off)
+        off += m2c.m2c_layer_write_store(o.handle, path, off)
+        o.close()
+        log(f"wrote store {q + 1}/{sets} ({off / 1e9:.2f} GB)")
+    os.sync()
+    log(f"store file {off / 1e9:.2f} GB in {time.perf_counter() - t0:.1f} s")
+    layer_bytes = sum(wl.d_ff * ((m2c.m2c_record_bytes(wl.d_model, t) + 15) // 16 * 16)
+                      for t in (1, 2, 3))
+    dd = m2c.DramDesc(n_layers, args.ssd_fixed, args.ssd_slots, args.ssd_lookahead, layer_bytes,
+                      m2c.DRAM_DIRECT_IO, 0)
+    dram = m2c.m2c_dram_create(dd, path, [offs[l % sets] for l in range(n_layers)])
+    layers = []
+    x_dev = torch.empty((n_layers, steps, wl.d_model), dtype=torch.float16, device="cuda")
+    for l in range(n_layers):
+        ld = W.workload_layer(wl, l, steps=steps, draw_weights=False)
+        x_dev[l].copy_(torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16))
+        layers.append(m2c.Layer(desc, ld, dram=dram, dram_index=l))
+    tiers = torch.empty((n_layers, wl.d_ff), dtype=torch.uint8, device="cuda")
+    y = torch.zeros((steps, n_layers, wl.d_model), dtype=torch.float32, device="cuda")
+    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=2)
+    for t in range(args.warmup):
+        sched.step(t, lambda l: x_dev[l, t], lambda l: y[t, l])
+        log(f"ssd tier: warm-up token {t}")
+    torch.cuda.synchronize()
+    s0 = m2c.m2c_dram_get_stats(dram)
+    t0 = time.perf_counter()
+    for t in range(args.warmup, steps):
+        sched.step(t, lambda l: x_dev[l, t], lambda l: y[t, l])
+        log(f"ssd tier: token {t}")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    s1 = m2c.m2c_dram_get_stats(dram)
+    for L in layers:
+        L.close()
+    m2c.m2c_dram_destroy(dram)
+    os.remove(path)
+    loads = s1.loads - s0.loads
+    rd = s1.bytes_read - s0.bytes_read
+    return {"workload": wl.name, "layers": n_layers, "tokens": args.steps, "tokens_per_s":
+            args.steps / wall, "ms_per_token": wall / args.steps * 1e3,
+            "fixed_layers": args.ssd_fixed, "dynamic_slots": args.ssd_slots,
+            "lookahead": args.ssd_lookahead, "distinct_weight_sets_in_file": sets,
+            "layer_MB": layer_bytes / 1e6, "loads_per_token": loads / args.steps,
+            "file_read_GBps": rd / max(s1.read_seconds - s0.read_seconds, 1e-9) / 1e9,
+            "file_GB_per_token": rd / args.steps / 1e9,
+            "fill_wait_s_per_token": (s1.wait_seconds - s0.wait_seconds) / args.steps,
+            "direct_io": bool(s1.direct_io),
+            "dram_GB_cache": (args.ssd_fixed + args.ssd_slots) * layer_bytes / 1e9,
+            "dram_GB_all_layers": n_layers * layer_bytes / 1e9}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -627,6 +819,17 @@ def main():
     if args.policy_sweep:
         print(json.dumps({"policy_sweep": policy_sweep(min(args.steps, 36), torch, m2c, W)}),
               flush=True)
+        return
+    if args.only_predict:
+        wl_p = W.WORKLOADS[args.only_predict]
+        print(json.dumps({"predict_isolated": predict_isolated(wl_p, 8, args.ffn_reps, torch, m2c,
+                                                               W)}), flush=True)
+        return
+    if args.ssd_tier:
+        print(json.dumps({"ssd_tier": ssd_tier(args, torch, m2c, W)}), flush=True)
+        return
+    if args.fill_sweep:
+        print(json.dumps({"fill_sweep": fill_sweep(torch, m2c, W)}), flush=True)
         return
     if args.only_ffn:
         wl_f = W.WORKLOADS[args.only_ffn]

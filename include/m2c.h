@@ -310,6 +310,89 @@ m2c_status m2c_layer_reset_cache(m2c_layer* layer, void* stream);
  * GPU for a long time); that call's output is wrong. */
 m2c_status m2c_layer_stats(const m2c_layer* layer, m2c_stats* out);
 
+/* ------------------------------------------------------------------------
+ * SSD -> DRAM tier (Sec. 5.4 "Pattern-Aware Preloading for SSD", Fig. 8)
+ * ------------------------------------------------------------------------
+ * Every layer's neuron records live in a file (the SSD). A two-level DRAM
+ * cache holds the first `fixed_layers` layers in a fixed area, read once at
+ * creation and never evicted (a new token does not reload them), and the
+ * other layers in a dynamic area of `dynamic_slots` layer-sized buffers. A
+ * loader thread reads whole layers ahead of use. When layer l is acquired,
+ * the window l, l+1, ..., l+lookahead (mod n_layers) is made resident in
+ * that order (the caller waits only for l); a missing layer takes the lowest
+ * empty slot, else the slot of the loaded, unheld layer outside the window
+ * whose next use in the cyclic layer order is furthest away (largest
+ * (layer - l) mod n_layers); a look-ahead load with no slot to give up is
+ * skipped. These decisions depend only on the order of acquires.
+ *
+ * File layout of one layer (what m2c_layer_write_store writes): the FP16,
+ * INT8 and INT4 record arrays back to back (d_ff * record_stride[t] bytes
+ * each), zero-padded to a multiple of 4096 bytes; layer_bytes is the
+ * unpadded size. Layer offsets in the file are multiples of 4096. */
+enum {
+  M2C_DRAM_HOST_MEMORY = 1, /* plain host memory (no HIP calls; CPU-side use
+                               and tests); default: pinned (hipHostMalloc) so
+                               that the GPU fill reads it over the host link */
+  M2C_DRAM_DIRECT_IO = 2    /* read with O_DIRECT (bypass the page cache);
+                               falls back to buffered reads if the file system
+                               refuses it (m2c_dram_stats.direct_io says) */
+};
+typedef struct {
+  int32_t n_layers;      /* layers in the file                                 */
+  int32_t fixed_layers;  /* fixed area: layers 0 .. fixed_layers-1             */
+  int32_t dynamic_slots; /* dynamic area: >= lookahead + 1 unless every layer
+                            is fixed                                          */
+  int32_t lookahead;     /* layers loaded ahead of the one in use, >= 1        */
+  int64_t layer_bytes;   /* bytes of one layer's records (unpadded)            */
+  int32_t flags;         /* M2C_DRAM_*                                         */
+  int32_t device;        /* device whose fills read the pinned buffers         */
+} m2c_dram_desc;
+typedef struct {
+  int64_t acquires, hits;  /* hits: the layer was already in DRAM             */
+  int64_t loads, evictions;
+  int64_t bytes_read;      /* layer_bytes per load from the file              */
+  int64_t fixed_bytes;     /* bytes of the fixed area                         */
+  double read_seconds;     /* time the loader spent reading                   */
+  double wait_seconds;     /* time acquires spent waiting for their layer     */
+  int32_t direct_io;       /* 1 if reads bypass the page cache                */
+} m2c_dram_stats;
+typedef struct m2c_dram m2c_dram; /* opaque */
+
+/* Write the layer's host store into `path` (created if missing) at `offset`
+ * (a multiple of 4096), in the file layout above; *padded_bytes gets the
+ * bytes written (layer_bytes rounded up to 4096). Synchronous. */
+m2c_status m2c_layer_write_store(const m2c_layer* layer, const char* path, int64_t offset,
+                                 int64_t* padded_bytes);
+
+/* Open the cache over `path`; offsets[l] is layer l's offset. Reads the fixed
+ * area before returning and starts the loader thread. */
+m2c_status m2c_dram_create(const m2c_dram_desc* desc, const char* path, const int64_t* offsets,
+                           m2c_dram** out);
+/* Stops the loader, waits for the GPU readers of the buffers, frees them.
+ * M2C_ERR_STATE while layers created on the cache still exist. */
+m2c_status m2c_dram_destroy(m2c_dram* dram);
+/* Host-side use: wait until `layer` is in DRAM, hold it, return its bytes. */
+m2c_status m2c_dram_acquire(m2c_dram* dram, int32_t layer, const uint8_t** data);
+/* Give up a hold taken by m2c_dram_acquire. */
+m2c_status m2c_dram_release(m2c_dram* dram, int32_t layer);
+m2c_status m2c_dram_get_stats(m2c_dram* dram, m2c_dram_stats* out);
+/* Test support: the loads decided so far, in order (layer loaded, layer
+ * evicted or -1); *count gets the total, at most `capacity` are copied. */
+m2c_status m2c_dram_get_log(m2c_dram* dram, int32_t* loaded, int32_t* evicted, int32_t capacity,
+                            int32_t* count);
+
+/* Create a layer whose neuron records are layer `index` of a pinned DRAM
+ * cache (same d_model / d_ff and device; dram layer_bytes must equal the
+ * layer's record arrays). Its own predictor, slot cache and tables; each
+ * m2c_cache_fill acquires the layer from the cache (waiting for the loader
+ * if needed), enqueues the gather from those buffers and releases them
+ * behind a HIP event, so the loader never overwrites bytes a fill still
+ * reads. Fills of layers of one cache should be issued in layer order (the
+ * cyclic order the look-ahead assumes). The cache must outlive the layer. */
+m2c_status m2c_layer_create_from_dram(const m2c_layer_desc* desc, m2c_dram* dram, int32_t index,
+                                      const uint16_t* pred_a, const uint16_t* pred_b,
+                                      const float* score_bias, m2c_layer** out);
+
 /* Test support. Copies one record of the host store (no device work). */
 m2c_status m2c_debug_read_record(const m2c_layer* layer, int32_t tier, int32_t neuron, void* out,
                                  size_t bytes);

@@ -105,12 +105,13 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
   }
 }
 
-hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stream) {
+hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, const uint8_t* const host[4],
+                       hipStream_t stream) {
   const m2c_plan_layout& lay = L->layout;
   FillSrc src;
   for (int t = 0; t < 4; ++t) {
-    src.host[t] = L->store->host[t];
-    src.stride[t] = L->store->stride[t];
+    src.host[t] = host[t];
+    src.stride[t] = t ? L->info.record_stride[t] : 0;
   }
   // The host link, not the CUs, bounds a fill: 64 workgroups keep about
   // 1 MB of reads in flight, enough to cover its latency, while leaving the

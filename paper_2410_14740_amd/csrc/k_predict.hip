@@ -143,8 +143,8 @@ static void launch_z(int blocks, size_t lds, hipStream_t stream, const uint16_t*
                      z);
 }
 
-hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, float* scores,
-                          hipStream_t stream) {
+hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, float* z,
+                          float* scores, hipStream_t stream) {
   const int d = L->desc.d_model, r = L->desc.pred_rank, d_ff = L->desc.d_ff;
   const int Lz = canon_lanes(d), Ls = canon_lanes(r);
   const int nch = ((d >> 3) + Lz - 1) / Lz;  // chunks per lane of the z kernel
@@ -159,7 +159,7 @@ hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, floa
     const int bz = (waves_z + 3) / 4;
     const size_t lz = (size_t)nb * d * 2;
     const uint16_t* xb = x + (int64_t)b0 * d;
-    float* zb = L->z + (int64_t)b0 * r;
+    float* zb = z + (int64_t)b0 * r;
     if (nch <= 1)
       launch_z<1>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
     else if (nch <= 2)

@@ -1,8 +1,11 @@
 // Host side of the m2c C ABI: argument checking, the layer object, the
 // pinned host neuron store, create-time quantization and the entry points.
+#include <errno.h>
+#include <fcntl.h>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
+#include <unistd.h>
 
 #include <new>
 
@@ -149,6 +152,7 @@ void free_layer(m2c_layer* L) {
       (void)hipFree(L->dev_base);
     }
     release_store(L->store);
+    if (L->dram) m2c::dram_ref(L->dram, -1);
   }
   delete L;
 }
@@ -346,6 +350,30 @@ m2c_status new_layer(const m2c_layer_desc* desc, m2c_layer** out, m2c_layer** ma
 
 }  // namespace
 
+namespace m2c {
+
+m2c_status api_fail(m2c_status code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+m2c_status check_predict_args(const m2c_layer* L, const uint16_t* x, int batch, int k, int n_fp16,
+                              int n_int8, const uint8_t* tier_map) {
+  if (!L || !x || !tier_map) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (batch < 1 || batch > L->desc.max_batch)
+    return fail(M2C_ERR_CAPACITY, "batch %d outside [1, max_batch=%d]", batch, L->desc.max_batch);
+  if (k < 0 || k > L->desc.k_max)
+    return fail(M2C_ERR_CAPACITY, "k %d outside [0, k_max=%d]", k, L->desc.k_max);
+  if (n_fp16 < 0 || n_int8 < 0 || (int64_t)n_fp16 + n_int8 > k)
+    return fail(M2C_ERR_INVALID_ARG, "tier counts %d + %d exceed k %d", n_fp16, n_int8, k);
+  return M2C_OK;
+}
+
+}  // namespace m2c
+
 extern "C" {
 
 int64_t m2c_record_bytes(int32_t d_model, int32_t tier) {
@@ -402,6 +430,9 @@ m2c_status m2c_layer_create_shared(const m2c_layer_desc* desc, const m2c_layer* 
                                    const float* score_bias, m2c_layer** out) {
   if (!weights_of || !pred_a || !pred_b)
     return fail(M2C_ERR_INVALID_ARG, "weights_of or a predictor pointer is NULL");
+  if (!weights_of->store)
+    return fail(M2C_ERR_INVALID_ARG, "weights_of reads its records from a DRAM cache: create the "
+                "layer with m2c_layer_create_from_dram instead");
   if (!desc || desc->d_model != weights_of->desc.d_model || desc->d_ff != weights_of->desc.d_ff ||
       desc->device != weights_of->desc.device)
     return fail(M2C_ERR_INVALID_ARG, "d_model, d_ff and device must match weights_of");
@@ -429,6 +460,88 @@ m2c_status m2c_layer_create_shared(const m2c_layer_desc* desc, const m2c_layer* 
   return M2C_OK;
 }
 
+m2c_status m2c_layer_create_from_dram(const m2c_layer_desc* desc, m2c_dram* dram, int32_t index,
+                                      const uint16_t* pred_a, const uint16_t* pred_b,
+                                      const float* score_bias, m2c_layer** out) {
+  if (!dram || !pred_a || !pred_b)
+    return fail(M2C_ERR_INVALID_ARG, "dram or a predictor pointer is NULL");
+  if (!m2c::dram_pinned(dram))
+    return fail(M2C_ERR_INVALID_ARG, "the DRAM cache uses plain host memory; GPU fills need a "
+                "pinned one (no M2C_DRAM_HOST_MEMORY)");
+  if (index < 0 || index >= m2c::dram_layers(dram))
+    return fail(M2C_ERR_INVALID_ARG, "index %d outside [0, %d)", index, m2c::dram_layers(dram));
+  m2c_layer* L = nullptr;
+  m2c_status rc = new_layer(desc, out, &L);
+  if (rc != M2C_OK) return rc;
+  int64_t want = 0;
+  for (int t = 1; t <= 3; ++t) want += (int64_t)desc->d_ff * L->info.record_stride[t];
+  if (want != m2c::dram_layer_bytes(dram) || desc->device != m2c::dram_device(dram)) {
+    const long long have = (long long)m2c::dram_layer_bytes(dram);
+    delete L;
+    return fail(M2C_ERR_INVALID_ARG, "the DRAM cache holds %lld-byte layers on device %d; this "
+                "layer needs %lld bytes on device %d", have, m2c::dram_device(dram),
+                (long long)want, desc->device);
+  }
+  DeviceGuard g(desc->device);
+  if (!g.ok) {
+    delete L;
+    return fail(M2C_ERR_HIP, "hipSetDevice(%d) failed", desc->device);
+  }
+  L->dram = dram;
+  L->dram_index = index;
+  m2c::dram_ref(dram, 1);
+  rc = alloc_device(L, score_bias != nullptr);
+  if (rc == M2C_OK) rc = upload_predictor(L, pred_a, pred_b, score_bias);
+  if (rc != M2C_OK) {
+    char keep[sizeof(g_err)];
+    memcpy(keep, g_err, sizeof(keep));
+    free_layer(L);
+    memcpy(g_err, keep, sizeof(keep));
+    return rc;
+  }
+  L->info.host_store_bytes = 0;
+  *out = L;
+  return M2C_OK;
+}
+
+m2c_status m2c_layer_write_store(const m2c_layer* L, const char* path, int64_t offset,
+                                 int64_t* padded_bytes) {
+  if (!L || !path) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (!L->store) return fail(M2C_ERR_INVALID_ARG, "the layer has no host store of its own");
+  if (offset < 0 || offset % 4096)
+    return fail(M2C_ERR_INVALID_ARG, "offset %lld: need a multiple of 4096", (long long)offset);
+  const int fd = open(path, O_WRONLY | O_CREAT, 0644);
+  if (fd < 0) return fail(M2C_ERR_INVALID_ARG, "open(%s): %s", path, strerror(errno));
+  int64_t pos = offset;
+  m2c_status rc = M2C_OK;
+  for (int t = 3; t >= 1 && rc == M2C_OK; --t) {
+    const uint8_t* p = L->store->host[t];
+    int64_t left = (int64_t)L->desc.d_ff * L->store->stride[t];
+    while (left > 0) {
+      const ssize_t w = pwrite(fd, p, (size_t)(left < (1 << 30) ? left : (1 << 30)), pos);
+      if (w < 0 && errno == EINTR) continue;
+      if (w <= 0) {
+        rc = fail(M2C_ERR_INVALID_ARG, "write(%s): %s", path, strerror(errno));
+        break;
+      }
+      p += w;
+      pos += w;
+      left -= w;
+    }
+  }
+  const int64_t pad = (4096 - (pos - offset) % 4096) % 4096;
+  if (rc == M2C_OK && pad) {
+    static const uint8_t zeros[4096] = {0};
+    if (pwrite(fd, zeros, (size_t)pad, pos) != (ssize_t)pad)
+      rc = fail(M2C_ERR_INVALID_ARG, "write(%s): %s", path, strerror(errno));
+    pos += pad;
+  }
+  if (close(fd) != 0 && rc == M2C_OK)
+    rc = fail(M2C_ERR_INVALID_ARG, "close(%s): %s", path, strerror(errno));
+  if (rc == M2C_OK && padded_bytes) *padded_bytes = pos - offset;
+  return rc;
+}
+
 m2c_status m2c_layer_destroy(m2c_layer* layer) {
   free_layer(layer);
   return M2C_OK;
@@ -449,17 +562,12 @@ m2c_status m2c_plan_get_layout(const m2c_layer* layer, m2c_plan_layout* out) {
 m2c_status m2c_predict_rank(m2c_layer* L, const uint16_t* x, int32_t batch, int32_t k,
                             int32_t n_fp16, int32_t n_int8, float* scores, uint8_t* tier_map,
                             void* stream) {
-  if (!L || !x || !tier_map) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
-  if (batch < 1 || batch > L->desc.max_batch)
-    return fail(M2C_ERR_CAPACITY, "batch %d outside [1, max_batch=%d]", batch, L->desc.max_batch);
-  if (k < 0 || k > L->desc.k_max)
-    return fail(M2C_ERR_CAPACITY, "k %d outside [0, k_max=%d]", k, L->desc.k_max);
-  if (n_fp16 < 0 || n_int8 < 0 || (int64_t)n_fp16 + n_int8 > k)
-    return fail(M2C_ERR_INVALID_ARG, "tier counts %d + %d exceed k %d", n_fp16, n_int8, k);
+  m2c_status rc = m2c::check_predict_args(L, x, batch, k, n_fp16, n_int8, tier_map);
+  if (rc != M2C_OK) return rc;
   DeviceGuard g(L->desc.device);
   hipStream_t s = (hipStream_t)stream;
   float* sc = scores ? scores : L->scores;
-  HIPOK(m2c::launch_predict(L, x, batch, sc, s), "predictor launch");
+  HIPOK(m2c::launch_predict(L, x, batch, L->z, sc, s), "predictor launch");
   HIPOK(m2c::launch_select(sc, batch, L->desc.d_ff, k, n_fp16, n_int8, tier_map, s),
         "select launch");
   return M2C_OK;
@@ -486,7 +594,38 @@ m2c_status m2c_cache_plan(m2c_layer* L, const uint8_t* tier_map, int32_t batch, 
 m2c_status m2c_cache_fill(m2c_layer* L, const void* plan, void* stream) {
   if (!L || !plan) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
   DeviceGuard g(L->desc.device);
-  HIPOK(m2c::launch_fill(L, (const uint8_t*)plan, (hipStream_t)stream), "fill launch");
+  if (!L->dram) {
+    HIPOK(m2c::launch_fill(L, (const uint8_t*)plan, L->store->host, (hipStream_t)stream),
+          "fill launch");
+    return M2C_OK;
+  }
+  // records in a DRAM cache: hold the layer's buffer while the fill is
+  // enqueued, release it behind an event after the fill
+  const uint8_t* base = nullptr;
+  int slot = -1;
+  m2c_status rc = m2c::dram_acquire(L->dram, L->dram_index, &base, &slot);
+  if (rc != M2C_OK) return rc;
+  const uint8_t* host[4] = {nullptr, nullptr, nullptr, nullptr};
+  int64_t off = 0;
+  for (int t = 3; t >= 1; --t) {
+    host[t] = base + off;
+    off += (int64_t)L->desc.d_ff * L->info.record_stride[t];
+  }
+  hipError_t e = m2c::launch_fill(L, (const uint8_t*)plan, host, (hipStream_t)stream);
+  hipEvent_t ev = nullptr;
+  if (e == hipSuccess && slot >= 0) {
+    ev = m2c::dram_event(L->dram);
+    e = ev ? hipEventRecord(ev, (hipStream_t)stream) : hipErrorOutOfMemory;
+  }
+  if (e != hipSuccess) {
+    // nothing can be known about the fill: wait for the device before the
+    // buffer may be reused
+    (void)hipGetLastError();
+    (void)hipDeviceSynchronize();
+    m2c::dram_release(L->dram, slot, nullptr);
+    return hip_fail(e, "fill launch");
+  }
+  m2c::dram_release(L->dram, slot, ev);
   return M2C_OK;
 }
 
@@ -554,10 +693,22 @@ m2c_status m2c_debug_read_record(const m2c_layer* L, int32_t tier, int32_t neuro
   if (!L || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
   if (tier < 1 || tier > 3 || neuron < 0 || neuron >= L->desc.d_ff)
     return fail(M2C_ERR_INVALID_ARG, "tier %d / neuron %d out of range", tier, neuron);
-  if ((int64_t)bytes > L->store->stride[tier])
+  const int64_t stride = L->info.record_stride[tier];
+  if ((int64_t)bytes > stride)
     return fail(M2C_ERR_INVALID_ARG, "%zu bytes exceed the record stride %lld", bytes,
-                (long long)L->store->stride[tier]);
-  memcpy(out, L->store->host[tier] + (int64_t)neuron * L->store->stride[tier], bytes);
+                (long long)stride);
+  if (L->store) {
+    memcpy(out, L->store->host[tier] + (int64_t)neuron * stride, bytes);
+    return M2C_OK;
+  }
+  const uint8_t* base = nullptr;
+  int slot = -1;
+  m2c_status rc = m2c::dram_acquire(L->dram, L->dram_index, &base, &slot);
+  if (rc != M2C_OK) return rc;
+  int64_t off = 0;
+  for (int t = 3; t > tier; --t) off += (int64_t)L->desc.d_ff * L->info.record_stride[t];
+  memcpy(out, base + off + (int64_t)neuron * stride, bytes);
+  m2c::dram_release(L->dram, slot, nullptr);
   return M2C_OK;
 }
 

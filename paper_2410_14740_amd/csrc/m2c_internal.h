@@ -80,9 +80,30 @@ struct m2c_layer {
   m2c::DeviceState st;
   int64_t last_step = -1;
   int ffn_withhold = 0;  // test support: > 0 = h words withheld, polls before giving up
+  m2c_dram* dram = nullptr;  // records come from this DRAM cache (store is null)
+  int dram_index = -1;
 };
 
 namespace m2c {
+
+// ---------------------------------------------------------------------------
+// Host-side helpers of the entry points (m2c_api.hip)
+
+// Sets the thread's error message (m2c_last_error) and returns `code`.
+m2c_status api_fail(m2c_status code, const char* fmt, ...);
+// The host-side argument checks of m2c_predict_rank.
+m2c_status check_predict_args(const m2c_layer* L, const uint16_t* x, int batch, int k, int n_fp16,
+                              int n_int8, const uint8_t* tier_map);
+
+// SSD -> DRAM tier (dram_cache.hip)
+m2c_status dram_acquire(m2c_dram* D, int layer, const uint8_t** data, int* slot);
+void dram_release(m2c_dram* D, int slot, hipEvent_t reader);
+hipEvent_t dram_event(m2c_dram* D);
+int64_t dram_layer_bytes(const m2c_dram* D);
+int dram_layers(const m2c_dram* D);
+int dram_device(const m2c_dram* D);
+bool dram_pinned(const m2c_dram* D);
+void dram_ref(m2c_dram* D, int delta);
 
 // ---------------------------------------------------------------------------
 // Launchers (one per kernel file). All enqueue on `stream` and return the
@@ -93,14 +114,15 @@ hipError_t launch_transpose_u16(const uint16_t* in, uint16_t* out, int rows, int
 hipError_t launch_quantize_records(const uint16_t* wg, const uint16_t* wu, const uint16_t* wdT,
                                    int d, int i0, int n, uint8_t* r16, int64_t st16, uint8_t* r8,
                                    int64_t st8, uint8_t* r4, int64_t st4, hipStream_t stream);
-hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, float* scores,
-                          hipStream_t stream);
+hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, float* z,
+                          float* scores, hipStream_t stream);
 hipError_t launch_select(const float* scores, int batch, int d_ff, int k, int n16, int n8,
                          uint8_t* tier_map, hipStream_t stream);
 hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int step, uint8_t* plan,
                        hipStream_t stream);
 hipError_t launch_reset(m2c_layer* L, hipStream_t stream);
-hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
+hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, const uint8_t* const host[4],
+                       hipStream_t stream);
 hipError_t launch_poison_fill_slots(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
 hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
                       hipStream_t stream);

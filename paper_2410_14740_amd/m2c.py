@@ -63,6 +63,24 @@ class PlanLayout(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in PLAN_FIELDS]
 
 
+DRAM_HOST_MEMORY = 1
+DRAM_DIRECT_IO = 2
+
+
+class DramDesc(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("fixed_layers", ctypes.c_int32),
+                ("dynamic_slots", ctypes.c_int32), ("lookahead", ctypes.c_int32),
+                ("layer_bytes", ctypes.c_int64), ("flags", ctypes.c_int32),
+                ("device", ctypes.c_int32)]
+
+
+class DramStats(ctypes.Structure):
+    _fields_ = [("acquires", ctypes.c_int64), ("hits", ctypes.c_int64), ("loads", ctypes.c_int64),
+                ("evictions", ctypes.c_int64), ("bytes_read", ctypes.c_int64),
+                ("fixed_bytes", ctypes.c_int64), ("read_seconds", ctypes.c_double),
+                ("wait_seconds", ctypes.c_double), ("direct_io", ctypes.c_int32)]
+
+
 class Stats(ctypes.Structure):
     _fields_ = [("plans", ctypes.c_int64), ("req", ctypes.c_int64), ("hit", ctypes.c_int64),
                 ("refill", ctypes.c_int64), ("new_", ctypes.c_int64), ("bypass", ctypes.c_int64),
@@ -107,6 +125,15 @@ def load(path: str = LIB_PATH):
         "m2c_debug_read_tables": (I32, [P, P, P, P, P]),
         "m2c_debug_poison_fill_slots": (I32, [P, P, P]),
         "m2c_debug_ffn_withhold_h": (I32, [P, I32]),
+        "m2c_layer_write_store": (I32, [P, ctypes.c_char_p, I64, ctypes.POINTER(I64)]),
+        "m2c_dram_create": (I32, [ctypes.POINTER(DramDesc), ctypes.c_char_p, P, ctypes.POINTER(P)]),
+        "m2c_dram_destroy": (I32, [P]),
+        "m2c_dram_acquire": (I32, [P, I32, ctypes.POINTER(P)]),
+        "m2c_dram_release": (I32, [P, I32]),
+        "m2c_dram_get_stats": (I32, [P, ctypes.POINTER(DramStats)]),
+        "m2c_dram_get_log": (I32, [P, P, P, I32, ctypes.POINTER(I32)]),
+        "m2c_layer_create_from_dram": (I32, [ctypes.POINTER(LayerDesc), P, I32, P, P, P,
+                                             ctypes.POINTER(P)]),
         "m2c_last_error": (ctypes.c_char_p, []),
         "m2c_build_id": (ctypes.c_char_p, []),
     }
@@ -271,6 +298,61 @@ def m2c_build_id() -> str:
     return load().m2c_build_id().decode()
 
 
+def m2c_layer_write_store(layer, path: str, offset: int) -> int:
+    n = ctypes.c_int64()
+    _check(load().m2c_layer_write_store(layer, path.encode(), offset, ctypes.byref(n)))
+    return n.value
+
+
+def m2c_dram_create(desc: DramDesc, path: str, offsets):
+    offs = np.ascontiguousarray(offsets, dtype=np.int64)
+    out = ctypes.c_void_p()
+    _check(load().m2c_dram_create(ctypes.byref(desc), path.encode(), offs.ctypes.data,
+                                  ctypes.byref(out)))
+    return out.value
+
+
+def m2c_dram_destroy(dram):
+    _check(load().m2c_dram_destroy(dram))
+
+
+def m2c_dram_acquire(dram, layer: int, nbytes: int) -> np.ndarray:
+    """Hold `layer` and return a copy of its first `nbytes` bytes."""
+    p = ctypes.c_void_p()
+    _check(load().m2c_dram_acquire(dram, layer, ctypes.byref(p)))
+    return np.ctypeslib.as_array((ctypes.c_uint8 * nbytes).from_address(p.value)).copy()
+
+
+def m2c_dram_release(dram, layer: int):
+    _check(load().m2c_dram_release(dram, layer))
+
+
+def m2c_dram_get_stats(dram) -> DramStats:
+    st = DramStats()
+    _check(load().m2c_dram_get_stats(dram, ctypes.byref(st)))
+    return st
+
+
+def m2c_dram_get_log(dram):
+    """[(loaded layer, evicted layer or -1)] in decision order."""
+    n = ctypes.c_int32()
+    _check(load().m2c_dram_get_log(dram, None, None, 0, ctypes.byref(n)))
+    a = np.empty(max(n.value, 1), np.int32)
+    b = np.empty(max(n.value, 1), np.int32)
+    _check(load().m2c_dram_get_log(dram, a.ctypes.data, b.ctypes.data, n.value, ctypes.byref(n)))
+    return list(zip(a[:n.value].tolist(), b[:n.value].tolist()))
+
+
+def m2c_layer_create_from_dram(desc: LayerDesc, dram, index: int, pred_a, pred_b, score_bias=None):
+    pred_a, pred_b = _host16(pred_a), _host16(pred_b)
+    if score_bias is not None:
+        score_bias = np.ascontiguousarray(score_bias, dtype=np.float32)
+    out = ctypes.c_void_p()
+    _check(load().m2c_layer_create_from_dram(ctypes.byref(desc), dram, index, _ptr(pred_a),
+                                             _ptr(pred_b), _ptr(score_bias), ctypes.byref(out)))
+    return out.value
+
+
 def m2c_last_error() -> str:
     return load().m2c_last_error().decode()
 
@@ -281,10 +363,14 @@ def m2c_last_error() -> str:
 class Layer:
     """Owns a layer handle and one plan buffer; methods map 1:1 onto the ABI."""
 
-    def __init__(self, desc: LayerDesc, data=None, weights_of: "Layer | None" = None):
+    def __init__(self, desc: LayerDesc, data=None, weights_of: "Layer | None" = None,
+                 dram=None, dram_index: int = -1):
         import torch
         self.desc = desc
-        if weights_of is None:
+        if dram is not None:
+            self.handle = m2c_layer_create_from_dram(desc, dram, dram_index, data.pred_a,
+                                                     data.pred_b, data.bias)
+        elif weights_of is None:
             self.handle = m2c_layer_create(desc, data.w_gate, data.w_up, data.w_down, data.pred_a,
                                            data.pred_b, data.bias)
         else:

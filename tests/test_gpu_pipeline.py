@@ -129,3 +129,74 @@ def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
     say(f"pipeline worst FFN error {worst:.2e}")
     for L in layers:
         L.close()
+
+
+def test_schedule_with_layers_read_from_dram_cache(tmp_path):
+    """The SSD -> DRAM tier under the same schedule: four layers' stores
+    written to a file, a pinned two-level DRAM cache with one fixed layer and
+    two dynamic slots (look-ahead 1), so every token reloads layers while the
+    GPU fills still read others; held streams and poisoned slots as above.
+    Outputs and plans match the oracle, every fill read the right bytes (the
+    FFN would be wrong otherwise), and the cache's load decisions are the
+    preloader oracle's."""
+    from oracle.preload import TwoLevelDram
+    n_layers, d, d_ff, r, steps = 4, 512, 1400, 32, 8
+    k = 350
+    n16, n8 = k // 10, (k // 2) - k // 10
+    C = 250
+    desc = m2c.make_desc(d, d_ff, r, k, C)
+    lds = [W.make_layer(950, l, d, d_ff, r, steps, rhos=(0.8,)) for l in range(n_layers)]
+    path = str(tmp_path / "stores.bin")
+    offs, off = [], 0
+    owners = []
+    for ld in lds:
+        o = m2c.Layer(desc, ld)
+        offs.append(off)
+        off += m2c.m2c_layer_write_store(o.handle, path, off)
+        owners.append(o)
+    layer_bytes = sum(d_ff * owners[0].info.record_stride[t] for t in (1, 2, 3))
+    for o in owners:
+        o.close()
+    dram = m2c.m2c_dram_create(m2c.DramDesc(n_layers, 1, 2, 1, layer_bytes, 0, 0), path, offs)
+    layers = [m2c.Layer(desc, ld, dram=dram, dram_index=l) for l, ld in enumerate(lds)]
+    # a record read through the cache is the oracle's record
+    rec = m2c.m2c_debug_read_record(layers[2].handle, 1, 17, layers[2].info.record_stride[1])
+    ref = oracle.build_records(lds[2].w_gate[17:18], lds[2].w_up[17:18],
+                               np.ascontiguousarray(lds[2].w_down[:, 17:18]), 1)[0]
+    assert np.array_equal(rec, ref)
+    x = torch.stack([torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16)
+                     for ld in lds]).cuda()
+    y = torch.zeros((steps, n_layers, d), dtype=torch.float32, device="cuda")
+    tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
+    archive = torch.empty((steps, n_layers, layers[0].info.plan_bytes), dtype=torch.uint8,
+                          device="cuda")
+    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=2)
+    hooks = _Hooks(layers, archive, True, True, seed=77)
+    say("pipeline from the DRAM cache: enqueue")
+    for t in range(steps):
+        sched.step(t, lambda l: x[l, t], lambda l: y[t, l], hooks=hooks)
+    torch.cuda.synchronize()
+    yg = y.cpu().numpy()
+    arch = archive.cpu()
+    for l, (L, ld) in enumerate(zip(layers, lds)):
+        cache = oracle.LRUCache(d_ff, C, L.info.staging_slots)
+        for t in range(steps):
+            _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
+            tm, _ = oracle.select_tiers(s, k, n16, n8)
+            o = cache.plan(tm, t)
+            _check_plan(L, arch[t, l], o, f"layer {l} step {t}")
+            y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"])[0]
+            err = r8_errors(yg[t, l], y_ref).max()
+            assert err <= FFN_TOL, f"layer {l} step {t}: FFN error {err:.3e}"
+        L.stats()
+    ref = TwoLevelDram(n_layers, 1, 2, 1)
+    ref.use(2)  # the record read above acquired layer 2 first
+    for t in range(steps):
+        for l in range(n_layers):
+            ref.use(l)
+    assert m2c.m2c_dram_get_log(dram) == [(m, old) for (_, m, _, old) in ref.log]
+    st = m2c.m2c_dram_get_stats(dram)
+    assert st.loads == len(ref.log) > n_layers  # layers were reloaded while fills ran
+    for L in layers:
+        L.close()
+    m2c.m2c_dram_destroy(dram)
