@@ -263,6 +263,28 @@ m2c_status m2c_predict_rank(m2c_layer* layer, const uint16_t* x, int32_t batch, 
                             int32_t n_fp16, int32_t n_int8, float* scores, uint8_t* tier_map,
                             void* stream);
 
+/* Bytes of the fixed device scratch array of m2c_predict_rank_noalloc. */
+#define M2C_NOALLOC_SCRATCH_BYTES (4u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * scores and tier map as m2c_predict_rank, bit for bit, with the call's
+ * scratch -- z [batch][pred_rank] fp32 and, when `scores` is NULL, the scores
+ * [batch][d_ff] fp32 -- in one fixed device array of M2C_NOALLOC_SCRATCH_BYTES
+ * that the library keeps on every GPU it runs on until the process ends,
+ * instead of the layer's own buffers. Allocates nothing: no hipMalloc, no
+ * hipFree, no allocating library call.
+ * Limit: round_up(4 * batch * pred_rank, 256) + (scores ? 0 : 4 * batch *
+ * d_ff) <= M2C_NOALLOC_SCRATCH_BYTES, else M2C_ERR_CAPACITY with nothing
+ * enqueued. Every call on one GPU, from any layer, shares that GPU's array:
+ * calls that can run at the same time on one GPU (streams not ordered with
+ * each other, or other threads) race and give wrong results; calls ordered
+ * on one stream are safe. The array is fully written before it is read, so
+ * what an earlier call left in it never matters. */
+m2c_status m2c_predict_rank_noalloc(m2c_layer* layer, const uint16_t* x, int32_t batch, int32_t k,
+                                    int32_t n_fp16, int32_t n_int8, float* scores,
+                                    uint8_t* tier_map, void* stream);
+
 /* Resolve tier_map (dev uint8 [batch][d_ff]) against the slot cache for
  * decode step `step`, write the plan into `plan` (dev, plan_bytes) and update
  * the slot tables. `step` must be >= 0, < 2^31 and strictly greater than the

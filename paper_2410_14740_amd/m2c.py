@@ -115,6 +115,7 @@ def load(path: str = LIB_PATH):
         "m2c_layer_get_info": (I32, [P, ctypes.POINTER(LayerInfo)]),
         "m2c_plan_get_layout": (I32, [P, ctypes.POINTER(PlanLayout)]),
         "m2c_predict_rank": (I32, [P, P, I32, I32, I32, I32, P, P, P]),
+        "m2c_predict_rank_noalloc": (I32, [P, P, I32, I32, I32, I32, P, P, P]),
         "m2c_cache_plan": (I32, [P, P, I32, I64, P, P]),
         "m2c_cache_fill": (I32, [P, P, P]),
         "m2c_sparse_ffn": (I32, [P, P, I32, P, P, P]),
@@ -240,6 +241,11 @@ def m2c_plan_get_layout(layer: int) -> PlanLayout:
 def m2c_predict_rank(layer, x, batch, k, n_fp16, n_int8, scores, tier_map, stream=None):
     _check(load().m2c_predict_rank(layer, _ptr(x), batch, k, n_fp16, n_int8, _ptr(scores),
                                    _ptr(tier_map), _stream(stream)))
+
+
+def m2c_predict_rank_noalloc(layer, x, batch, k, n_fp16, n_int8, scores, tier_map, stream=None):
+    _check(load().m2c_predict_rank_noalloc(layer, _ptr(x), batch, k, n_fp16, n_int8, _ptr(scores),
+                                           _ptr(tier_map), _stream(stream)))
 
 
 def m2c_cache_plan(layer, tier_map, batch, step, plan, stream=None):
