@@ -246,3 +246,54 @@ def dense_ffn(w_gate, w_up, w_down, x) -> np.ndarray:
     if _load().orc_dense_ffn(d, d_ff, _p(w_gate), _p(w_up), _p(w_down), _p(x), _p(y)) != 0:
         raise ValueError("orc_dense_ffn failed")
     return y
+
+
+class TierPoolCache:
+    """Per-tier record arena: one step-atomic LRU slot cache per tier, each
+    with slots of that tier's record size (Sec. 5.3's isolated cache unit,
+    split by precision so that an INT4 neuron does not take an FP16-sized
+    slot). A neuron required at step tier t (the highest tier any batch row
+    asks for) is looked up in tier t's cache only: HIT if resident there,
+    else NEW there (LRU victim, or BYPASS into that pool's staging slots).
+    A neuron can be resident in several pools at once, each pool holding its
+    own tier's record, so there are no REFILLs and the FFN output stays a
+    function of the step's selection alone.
+
+    C, S: {tier: resident slots}, {tier: staging slots}. Global slot ids are
+    numbered in tier blocks, FP16 first: block t holds pool t's resident
+    slots then its staging slots. The merged plan lists R in ascending id,
+    the fills (every non-HIT) in ascending id, and the evictions of pool
+    FP16, then INT8, then INT4, each in its victim order."""
+
+    TIERS = (3, 2, 1)
+
+    def __init__(self, d_ff: int, C: dict, S: dict):
+        self.d_ff = d_ff
+        self.pools = {t: LRUCache(d_ff, C[t], S[t]) for t in self.TIERS}
+        self.first, off = {}, 0
+        for t in self.TIERS:
+            self.first[t] = off
+            off += C[t] + S[t]
+
+    def plan(self, tier_map, step: int) -> dict:
+        tm = np.ascontiguousarray(tier_map, dtype=np.uint8)
+        if tm.ndim == 1:
+            tm = tm[None, :]
+        step_tier = tm.max(axis=0)
+        parts = {}
+        for t in self.TIERS:
+            sub = np.where((tm > 0) & (step_tier == t)[None, :], t, 0).astype(np.uint8)
+            p = self.pools[t].plan(sub, step)
+            p["req_slot"] = p["req_slot"] + self.first[t]
+            p["fill_slot"] = p["fill_slot"] + self.first[t]
+            parts[t] = p
+        res = {}
+        order = np.argsort(np.concatenate([parts[t]["req_ids"] for t in self.TIERS]), kind="stable")
+        for key in ("req_ids", "req_tier", "req_hit", "req_slot", "req_mask"):
+            res[key] = np.concatenate([parts[t][key] for t in self.TIERS])[order]
+        order = np.argsort(np.concatenate([parts[t]["fill_ids"] for t in self.TIERS]), kind="stable")
+        for key in ("fill_ids", "fill_tier", "fill_slot", "fill_from"):
+            res[key] = np.concatenate([parts[t][key] for t in self.TIERS])[order]
+        res["evicted_ids"] = np.concatenate([parts[t]["evicted_ids"] for t in self.TIERS])
+        res["counts"] = sum(parts[t]["counts"] for t in self.TIERS).astype(np.int32)
+        return res

@@ -509,3 +509,41 @@ def test_oracle_results_do_not_depend_on_threads():
     assert all(np.array_equal(r1[t], r4[t]) for t in (1, 2, 3))
     assert np.array_equal(s1.view(np.uint32), s4.view(np.uint32))
     assert np.array_equal(y1.view(np.uint64), y4.view(np.uint64))
+
+
+def test_tier_pools_are_independent_lru_caches():
+    """The per-tier arena: each pool is the step-atomic LRU brute force over
+    the requests of its tier alone, slots numbered in tier blocks; the merged
+    lists are the pools' lists in ascending id; no REFILL ever happens."""
+    d_ff, B = 60, 2
+    C = {3: 3, 2: 5, 1: 8}
+    S = {3: 20, 2: 20, 1: 20}
+    cache = oracle.TierPoolCache(d_ff, C, S)
+    first = {3: 0, 2: 23, 1: 48}
+    states = {t: ({}, [None] * C[t], [0] * C[t], [-1] * C[t]) for t in (3, 2, 1)}
+    rng = np.random.default_rng(12)
+    code = {"NEW": 0, "HIT": 1, "REFILL": 2, "BYPASS": 3}
+    for step in range(40):
+        tm = np.zeros((B, d_ff), np.uint8)
+        for b in range(B):
+            ids = rng.choice(d_ff, size=rng.integers(0, 12), replace=False)
+            tm[b, ids] = rng.integers(1, 4, size=ids.size)
+        p = cache.plan(tm, step)
+        st = tm.max(axis=0)
+        want = {}
+        evicted = []
+        for t in (3, 2, 1):
+            tiers = {i: (t if st[i] == t else 0) for i in range(d_ff)}
+            req, res, ev = _brute_lru_step(states[t], tiers, step, C[t])
+            for i in req:
+                want[i] = (t, code[res[i][0]], first[t] + res[i][1])
+            evicted += ev
+        req = sorted(want)
+        assert list(p["req_ids"]) == req
+        assert list(p["req_tier"]) == [want[i][0] for i in req]
+        assert list(p["req_hit"]) == [want[i][1] for i in req]
+        assert list(p["req_slot"]) == [want[i][2] for i in req]
+        assert 2 not in p["req_hit"]
+        assert list(p["fill_ids"]) == [i for i in req if want[i][1] != 1]
+        assert list(p["evicted_ids"]) == evicted
+        assert not p["fill_from"].any()
