@@ -92,6 +92,8 @@ def parse_args():
     p.add_argument("--ssd-fixed", type=int, default=4)
     p.add_argument("--ssd-slots", type=int, default=8)
     p.add_argument("--ssd-lookahead", type=int, default=2)
+    p.add_argument("--ratio-search", action="store_true",
+                   help="only the offline neuron-ratio search (Algorithm 1) on the 7B-shaped layer")
     p.add_argument("--batch-sweep", action="store_true",
                    help="only the batched-decode workload (7B-shaped layer, batch 8): LRU capacity "
                         "10/30/60%% x tiers 10/40/50 or all FP16, one JSON line")
@@ -782,6 +784,31 @@ def ssd_tier(args, torch, m2c, W):
             "dram_GB_all_layers": n_layers * layer_bytes / 1e9}
 
 
+def ratio_search(torch, m2c, W):
+    """Algorithm 1 (offline neuron-ratio search) on the 7B-shaped layer with
+    16 calibration tokens of its AR(1) input stream: starting from k = 20%
+    of d_ff at the low tier, FP16 vs INT4 (bit ratio 4) and FP16 vs INT8
+    (bit ratio 2); reports every candidate's proxy score, the chosen ratio
+    and the search's wall time."""
+    wl = W.WORKLOADS["llama2-7b"]
+    k, _, _ = wl.counts()
+    T = 16
+    ld = W.workload_layer(wl, 0, steps=T)
+    L = m2c.Layer(m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, wl.d_ff, wl.cache_slots()), ld)
+    x = torch.from_numpy(np.ascontiguousarray(ld.x[:, 0].view(np.uint16))).cuda()
+    out = {"workload": wl.name, "calibration_tokens": T, "n_low0": k, "searches": []}
+    for step, n in ((32, 4), (64, 2)):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        cands, uqs, best = m2c.m2c_ratio_search(L.handle, x, T, k, step, n)
+        el = time.perf_counter() - t0
+        out["searches"].append({"bit_ratio": n, "step": step, "candidates": cands, "uq": uqs,
+                                "best": cands[best], "best_uq": uqs[best], "seconds": el})
+        log(f"ratio search n={n}: best {cands[best]} uq {uqs[best]:.4e} in {el:.2f} s")
+    L.close()
+    return out
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -824,6 +851,9 @@ def main():
         wl_p = W.WORKLOADS[args.only_predict]
         print(json.dumps({"predict_isolated": predict_isolated(wl_p, 8, args.ffn_reps, torch, m2c,
                                                                W)}), flush=True)
+        return
+    if args.ratio_search:
+        print(json.dumps({"ratio_search": ratio_search(torch, m2c, W)}), flush=True)
         return
     if args.ssd_tier:
         print(json.dumps({"ssd_tier": ssd_tier(args, torch, m2c, W)}), flush=True)

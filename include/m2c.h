@@ -415,6 +415,28 @@ m2c_status m2c_layer_create_from_dram(const m2c_layer_desc* desc, m2c_dram* dram
                                       const uint16_t* pred_a, const uint16_t* pred_b,
                                       const float* score_bias, m2c_layer** out);
 
+/* Offline neuron-ratio search (Sec. 5.2 "Offline Neuron Ratio Search",
+ * Algorithm 1) on an FFN-error proxy of the paper's entropy estimate, which
+ * needs a trained language model. Candidate i = 1, 2, ... has
+ * n_high = i * step FP16 neurons and n_low = n_low0 - i * step * bit_ratio
+ * low-precision ones (INT4 for bit_ratio 4, INT8 for bit_ratio 2), while
+ * n_low >= 0: the bytes of the active neurons stay the same. Its score is
+ *   uq = sum_t |y_t - y*_t|^2 / sum_t |y*_t|^2
+ * over the T calibration tokens x (dev fp16 [T][d_model]): y_t is this
+ * layer's sparse FFN with the top n_high + n_low neurons by predictor score,
+ * the n_high best at FP16, the rest at the low tier; y*_t the FFN with every
+ * neuron at FP16. Each FFN runs through the layer's predict, plan, fill and
+ * FFN kernels on `stream`. The chosen candidate is the one with the lowest
+ * score, a later one winning ties (the comparison UQ_best >= UQ_score).
+ * Needs k_max == d_ff (the all-FP16 reference). Outputs (host, room for
+ * max_candidates): n_high, n_low, uq per candidate, *count candidates,
+ * *best the chosen index (-1 if none). Synchronous; allocates its buffers;
+ * leaves the layer's cache cold (reset). */
+m2c_status m2c_ratio_search(m2c_layer* layer, const uint16_t* x, int32_t T, int32_t n_low0,
+                            int32_t step, int32_t bit_ratio, int32_t max_candidates,
+                            int32_t* n_high, int32_t* n_low, double* uq, int32_t* count,
+                            int32_t* best, void* stream);
+
 /* Test support. Copies one record of the host store (no device work). */
 m2c_status m2c_debug_read_record(const m2c_layer* layer, int32_t tier, int32_t neuron, void* out,
                                  size_t bytes);

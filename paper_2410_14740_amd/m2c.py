@@ -135,6 +135,8 @@ def load(path: str = LIB_PATH):
         "m2c_dram_get_log": (I32, [P, P, P, I32, ctypes.POINTER(I32)]),
         "m2c_layer_create_from_dram": (I32, [ctypes.POINTER(LayerDesc), P, I32, P, P, P,
                                              ctypes.POINTER(P)]),
+        "m2c_ratio_search": (I32, [P, P, I32, I32, I32, I32, I32, P, P, P,
+                                   ctypes.POINTER(I32), ctypes.POINTER(I32), P]),
         "m2c_last_error": (ctypes.c_char_p, []),
         "m2c_build_id": (ctypes.c_char_p, []),
     }
@@ -357,6 +359,20 @@ def m2c_layer_create_from_dram(desc: LayerDesc, dram, index: int, pred_a, pred_b
     _check(load().m2c_layer_create_from_dram(ctypes.byref(desc), dram, index, _ptr(pred_a),
                                              _ptr(pred_b), _ptr(score_bias), ctypes.byref(out)))
     return out.value
+
+
+def m2c_ratio_search(layer, x, T: int, n_low0: int, step: int, bit_ratio: int, stream=None):
+    """Algorithm 1 on the FFN-error proxy: ([(n_high, n_low)], [uq], best index)."""
+    cap = max(1, n_low0 // max(1, step * bit_ratio) + 1)
+    nh = np.empty(cap, np.int32)
+    nl = np.empty(cap, np.int32)
+    uq = np.empty(cap, np.float64)
+    cnt, best = ctypes.c_int32(), ctypes.c_int32()
+    _check(load().m2c_ratio_search(layer, _ptr(x), T, n_low0, step, bit_ratio, cap, nh.ctypes.data,
+                                   nl.ctypes.data, uq.ctypes.data, ctypes.byref(cnt),
+                                   ctypes.byref(best), _stream(stream)))
+    n = cnt.value
+    return list(zip(nh[:n].tolist(), nl[:n].tolist())), uq[:n].tolist(), best.value
 
 
 def m2c_last_error() -> str:
