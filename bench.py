@@ -53,6 +53,9 @@ def parse_args():
     p.add_argument("--policy", choices=("exact", "dominance"), default="exact",
                    help="cache hits: exact tier (default) or a resident tier at or above the "
                         "requested one")
+    p.add_argument("--tier-pools", action="store_true",
+                   help="per-tier record arena: the HBM of the workload's C FP16-sized slots split "
+                        "into one pool per tier, each the same multiple of its tier's demand")
     p.add_argument("--policy-sweep", action="store_true",
                    help="only the cache-policy measurement: hit rates of exact-tier and "
                         "dominance hits, LRU at C = 30%% and at C = k (the ATU regime), against "
@@ -110,12 +113,13 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def build_stack(wl, n_layers, steps_total, weight_sets, torch, m2c, W, flags=0):
+def build_stack(wl, n_layers, steps_total, weight_sets, torch, m2c, W, flags=0, tier_slots=None):
     """Create every layer (weights drawn in a thread pool, layers created in
     order) and stage every layer's decode inputs on the device."""
     k, n16, n8 = wl.counts()
     C = wl.cache_slots()
-    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, flags=flags)
+    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, flags=flags,
+                         tier_slots=tier_slots)
     x_dev = torch.empty((n_layers, steps_total, wl.d_model), dtype=torch.float16, device="cuda")
     layers, first = [], None
 
@@ -560,7 +564,7 @@ class _StageEvents:
 
 
 def run_stack(wl, n_layers, steps, warmup, weight_sets, flags, overlap_steps, stage_events,
-              torch, m2c, W):
+              torch, m2c, W, tier_slots=None):
     """The decode pipeline over the whole stack: `warmup` untimed steps,
     `steps` timed ones between a synchronization on each side, then
     `overlap_steps` untimed steps with events around every stage."""
@@ -569,7 +573,7 @@ def run_stack(wl, n_layers, steps, warmup, weight_sets, flags, overlap_steps, st
     steps_total = warmup + steps
     t_setup = time.perf_counter()
     layers, x_dev, ld0 = build_stack(wl, n_layers, steps_total + overlap_steps, weight_sets, torch,
-                                     m2c, W, flags=flags)
+                                     m2c, W, flags=flags, tier_slots=tier_slots)
     log(f"setup {time.perf_counter() - t_setup:.1f} s")
     d, d_ff = wl.d_model, wl.d_ff
     tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
@@ -874,8 +878,13 @@ def main():
     weight_sets = args.weight_sets if args.weight_sets >= 0 else (
         8 if wl.name == "llama2-70b" else 0)
     flags = ffn_flags | (m2c.FLAG_DOMINANT_HITS if args.policy == "dominance" else 0)
+    tier_slots = None
+    if args.tier_pools:
+        tier_slots = m2c.pool_slots_for_budget(wl.d_model, {3: n16, 2: n8, 1: n4},
+                                               wl.cache_slots() * 6 * wl.d_model)
+        log(f"per-tier arena: {tier_slots} resident slots (FP16, INT8, INT4 pools)")
     r = run_stack(wl, n_layers, args.steps, args.warmup, weight_sets, flags, args.overlap_steps,
-                  args.stage_events, torch, m2c, W)
+                  args.stage_events, torch, m2c, W, tier_slots=tier_slots)
     log(f"stack: {r['tokens_per_s']:.2f} tokens/s")
     log(f"isolated sparse FFN on {args.ffn_layers} {wl.name}-shaped layers")
     iso = ffn_isolated(wl, args.ffn_layers, args.ffn_reps, torch, m2c, W, flags=ffn_flags)
@@ -934,7 +943,10 @@ def main():
                        "pinned host store",
             "distinct_weight_sets": weight_sets or n_layers,
             "cache_policy": "LRU, " + ("dominance hits" if args.policy == "dominance"
-                                       else "exact-tier hits"),
+                                       else "exact-tier hits") + (
+                ", per-tier arena {FP16, INT8, INT4} = " + str([tier_slots[3], tier_slots[2],
+                                                                tier_slots[1]])
+                if tier_slots else ""),
             "ffn": ffn_kind,
         },
         "us_per_layer_step": r["us_per_layer_step"],

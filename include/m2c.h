@@ -136,6 +136,9 @@ typedef struct {
                             smaller explicit values are rejected               */
   int32_t device;        /* HIP device ordinal                                  */
   int32_t flags;         /* M2C_FLAG_* bits, 0 for the defaults                 */
+  int32_t tier_slots[4]; /* with M2C_FLAG_TIER_POOLS: resident slots of the INT4
+                            [1], INT8 [2] and FP16 [3] pools, summing to
+                            cache_slots ([0] unused); otherwise ignored        */
 } m2c_layer_desc;
 
 /* m2c_layer_desc.flags */
@@ -152,7 +155,20 @@ enum {
      a resident tier below the requested one is a REFILL. The default is the
      exact-tier policy: any other resident tier is a REFILL. With dominance
      hits the output depends on the cache history, not only on the step. */
-  M2C_FLAG_DOMINANT_HITS = 2
+  M2C_FLAG_DOMINANT_HITS = 2,
+  /* Per-tier record arena: the cache unit is split into one pool per tier,
+     pool t with tier_slots[t] resident slots of record_stride[t] bytes (an
+     INT4 neuron no longer takes an FP16-sized slot, so the same HBM holds
+     more neurons). Each pool is its own step-atomic LRU cache over the
+     neurons whose step tier is t: HIT if resident in that pool, else NEW
+     there (victims from that pool, BYPASS into that pool's staging slots,
+     max(0, plan_capacity - tier_slots[t]) of them). A neuron may be resident
+     in several pools; there are no REFILLs. Global slot ids are numbered in
+     tier blocks, FP16 first (see m2c_layer_info.pool_first). Exact-tier
+     hits only (not with M2C_FLAG_DOMINANT_HITS); needs max_batch == 1,
+     d_model <= 8192, d_ff <= 32768, staging_slots == -1, and not
+     M2C_FLAG_DETERMINISTIC_FFN. */
+  M2C_FLAG_TIER_POOLS = 4
 };
 
 /* Sizes that follow from a descriptor. */
@@ -166,6 +182,15 @@ typedef struct {
   int64_t plan_bytes;       /* size of one plan buffer                        */
   int64_t host_store_bytes; /* pinned host neuron store (all three tiers)     */
   int64_t device_bytes;     /* device memory the layer owns                   */
+  /* Slots of the tier-t records, by tier [1..3]: global slot ids
+     [pool_first[t], pool_first[t] + pool_slots[t]), resident ones first,
+     each pool_stride[t] bytes. Without M2C_FLAG_TIER_POOLS every tier shares
+     one pool: pool_first 0, pool_slots C + S, pool_stride slot_bytes. */
+  int32_t pool_first[4];
+  int32_t pool_slots[4];
+  int32_t pool_resident[4]; /* resident slots of the pool (the rest stage)    */
+  int32_t pool_stride[4];
+  int64_t slot_arena_bytes; /* every pool plus the all-zero padding slot      */
 } m2c_layer_info;
 
 /* A plan is one caller-allocated device buffer of info.plan_bytes bytes,
@@ -440,8 +465,16 @@ m2c_status m2c_ratio_search(m2c_layer* layer, const uint16_t* x, int32_t T, int3
 /* Test support. Copies one record of the host store (no device work). */
 m2c_status m2c_debug_read_record(const m2c_layer* layer, int32_t tier, int32_t neuron, void* out,
                                  size_t bytes);
-/* Test support. Synchronizes the device, then copies slot `slot` (0..C+S-1). */
+/* Test support. Synchronizes the device, then copies slot `slot` (0..C+S-1;
+ * at most its pool's stride with M2C_FLAG_TIER_POOLS). */
 m2c_status m2c_debug_read_slot(const m2c_layer* layer, int32_t slot, void* out, size_t bytes);
+/* Test support. Synchronizes the device, then copies the tables of tier
+ * `tier`'s pool (M2C_FLAG_TIER_POOLS): slot_of int32 [d_ff] (pool-local
+ * resident slot or -1), slot_key int32 [tier_slots[tier]], slot_last int32
+ * [tier_slots[tier]]; any pointer may be NULL. */
+m2c_status m2c_debug_read_pool_tables(const m2c_layer* layer, int32_t tier, int32_t* slot_of,
+                                      int32_t* slot_key, int32_t* slot_last);
+
 /* Test support. Synchronizes the device, then copies the slot tables; any
  * pointer may be NULL. slot_of int32 [d_ff] (-1 = not resident);
  * slot_key int32 [C] (-1 = empty); slot_tier uint8 [C]; slot_last int32 [C]. */

@@ -185,11 +185,17 @@ static_assert(kFNPR * kFL <= kWorkSlotPad && kFWaves * kFL <= kWorkSlotPad,
 // workgroups of the CU already have in flight.
 template <int K>
 __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict__ work_slot, int d,
-                                      const uint8_t* __restrict__ slots, uint32_t sb,
+                                      const uint8_t* __restrict__ slots, const SlotMap& map,
                                       int n_slots, int tid, FBuf& b) {
   // byte offsets into the slot arena (below 4 GiB: checked at launch), so
-  // every address is the arena base plus one 32-bit register
-  const uint32_t zero = (uint32_t)n_slots * sb;
+  // every address is the arena base plus one 32-bit register; a task's
+  // records all live in its tier's pool (one pool for every tier unless the
+  // layer has a per-tier arena), and ids past the pools point at the zero slot
+  const uint32_t zero = map.zero;
+  const uint32_t tb = k.tier == 3 ? map.base[3] : k.tier == 2 ? map.base[2] : map.base[1];
+  const int tf = k.tier == 3 ? map.first[3] : k.tier == 2 ? map.first[2] : map.first[1];
+  const uint32_t ts = k.tier == 3 ? map.stride[3] : k.tier == 2 ? map.stride[2] : map.stride[1];
+  const uint32_t tc = k.tier == 3 ? map.count[3] : k.tier == 2 ? map.count[2] : map.count[1];
   const int lane = tid & 63;
   const int w = tid >> 6;
   const uint32_t ud = (uint32_t)d;
@@ -215,7 +221,7 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int v = __builtin_amdgcn_readfirstlane(wp[q * kFNPR + i]);
-        ids[q][i] = q * kFNPR + 4 * wu + i < n && v >= 0 && v < n_slots ? v : n_slots;
+        ids[q][i] = q * kFNPR + 4 * wu + i < n && (uint32_t)(v - tf) < tc ? v : n_slots;
       }
 #pragma unroll
     for (int j = 0; j < kFL; ++j) {
@@ -225,7 +231,7 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
       for (int i = 0; i < 4; ++i)  // round j >> lnv
         sv[i] = k.tier == 3 ? ids[j >> 2][i] : k.tier == 2 ? ids[j >> 1][i] : ids[j][i];
       const int slv = sub == 0 ? sv[0] : sub == 1 ? sv[1] : sub == 2 ? sv[2] : sv[3];
-      const uint32_t rec = (uint32_t)slv * sb;
+      const uint32_t rec = slv >= n_slots ? zero : tb + (uint32_t)(slv - tf) * ts;
       // the scale of an FP16 record (it has none) is read from the zero slot,
       // never from the data's own address: every load stays independent
       const uint32_t dp = colok ? rec + dbase + 16 * e : zero;
@@ -254,12 +260,13 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
       const int item = (wu * UW + uw) / upi;
       const int v = ids[uw];
       // the zero slot past the task (and for kind 0)
-      ids[uw] = k.kind == 1 && item < n && v >= 0 && v < n_slots ? v : n_slots;
+      ids[uw] = k.kind == 1 && item < n && (uint32_t)(v - tf) < tc ? v : n_slots;
     }
 #pragma unroll
     for (int j = 0; j < kFL; ++j) {
       const int part = (w * UW + j / K) % upi;
-      const uint32_t rec = (uint32_t)ids[j / K] * sb;
+      const int slu = ids[j / K];
+      const uint32_t rec = slu >= n_slots ? zero : tb + (uint32_t)(slu - tf) * ts;
       int q = lane + 64 * (j % K);
       const bool in = q < 2 * ncu;
       q = in ? q : 2 * ncu - 1;
@@ -456,10 +463,9 @@ inline size_t fused_lds_bytes(int d) {
 template <int K>
 __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void ffn_fused_kernel(
     const uint16_t* __restrict__ x, int d, const int32_t* __restrict__ counts,
-    const int32_t* __restrict__ work_slot, const uint8_t* __restrict__ slots, uint32_t sb,
-    int cap, int n_slots, unsigned long long* __restrict__ gen,
-    unsigned long long* __restrict__ hw, int32_t* __restrict__ status, float* __restrict__ y,
-    int withhold) {
+    const int32_t* __restrict__ work_slot, const uint8_t* __restrict__ slots, int cap,
+    int n_slots, unsigned long long* __restrict__ gen, unsigned long long* __restrict__ hw,
+    int32_t* __restrict__ status, float* __restrict__ y, int withhold, SlotMap map) {
   extern __shared__ uint4 xlds[];  // fused_lds_bytes(d)
   __shared__ FShared sh;
   const int tid = threadIdx.x;
@@ -489,9 +495,9 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
     const uint4* x4 = reinterpret_cast<const uint4*>(x);
     xv0 = x4[min(2 * tid, nc8 - 1)];
     xv1 = x4[min(2 * tid + 1, nc8 - 1)];
-    issue<K>(kc, work_slot, d, slots, sb, n_slots, tid, cur);
+    issue<K>(kc, work_slot, d, slots, map, n_slots, tid, cur);
   } else {
-    issue<K>(kc, work_slot, d, slots, sb, n_slots, tid, cur);
+    issue<K>(kc, work_slot, d, slots, map, n_slots, tid, cur);
   }
   const uint32_t epoch = (uint32_t)e0 + 1u;
   if (kc.kind == 1) {
@@ -592,9 +598,8 @@ hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* counts,
   const int d = L->desc.d_model;
   const size_t lds = fused_lds_bytes(d);
   hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, d, counts,
-                     work_slot, L->slots, (uint32_t)L->info.slot_bytes, L->cap,
-                     L->desc.cache_slots + L->S, L->st.ffn_gen, L->st.ffn_hw, L->st.status, y,
-                     L->ffn_withhold);
+                     work_slot, L->slots, L->cap, L->desc.cache_slots + L->S, L->st.ffn_gen,
+                     L->st.ffn_hw, L->st.status, y, L->ffn_withhold, L->map);
   return hipGetLastError();
 }
 
@@ -606,8 +611,7 @@ int loads_per_unit(int d) {
 }  // namespace
 
 bool ffn_fused_supported(const m2c_layer* L) {
-  const int64_t arena = (int64_t)(L->desc.cache_slots + L->S + 1) * L->info.slot_bytes;
-  return L->desc.d_model <= 8192 && arena < ((int64_t)1 << 32);
+  return L->desc.d_model <= 8192 && L->arena_bytes < ((int64_t)1 << 32);
 }
 
 int ffn_fused_grid(int d, int cap, int num_cus) {

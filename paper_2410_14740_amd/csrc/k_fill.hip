@@ -40,8 +40,8 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
                                                             const uint8_t* __restrict__ fill_from,
                                                             int32_t* __restrict__ slot_rec,
                                                             FillSrc src, uint8_t* __restrict__ slots,
-                                                            int64_t slot_bytes, int cap, int d_ff,
-                                                            int d, int n_slots) {
+                                                            SlotMap map, int cap, int d_ff, int d,
+                                                            int n_slots) {
   extern __shared__ u32x4 stage[];  // 2 d + 6 d / 128 bytes: one FP16 row and the scales
   int n = counts[M2C_CNT_FILL];
   n = n < 0 ? 0 : n > cap ? cap : n;
@@ -49,16 +49,20 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
     const int t = fill_tier[e];
     const int id = fill_ids[e], slot = fill_slot[e];
     // plans written by m2c_cache_plan always pass; anything else is skipped
+    // (workgroup-uniform: every thread reads the same entry), as is a slot
+    // outside the pool of the fill's tier
     if (t < 1 || t > 3 || id < 0 || id >= d_ff || slot < 0 || slot >= n_slots) continue;
+    if ((uint32_t)(slot - map.first[t]) >= (uint32_t)map.count[t]) continue;
     const bool derive = fill_from[e] == 3 && t < 3 && slot_rec[slot] == 4 * id + 3;
     __syncthreads();  // every thread has read slot_rec[slot] before it changes
     if (threadIdx.x == 0) slot_rec[slot] = 4 * id + t;
+    // where the slot's record starts (in the pool of the fill's tier)
+    uint8_t* rec = slots + map.base[t] + (int64_t)(slot - map.first[t]) * map.stride[t];
     if (derive) {
       // Derive in place (uniform over the workgroup), one d-element row at a
       // time: row v's codes land below byte 2 d (v + 1), which the staged
       // rows 0..v cover; the scales, which overlap the up row's FP16 bytes
       // for INT8, are written last.
-      uint8_t* rec = slots + (int64_t)slot * slot_bytes;
       uint16_t* sc_stage = reinterpret_cast<uint16_t*>(stage + ((2 * d) >> 4));
       const uint32_t* w = reinterpret_cast<const uint32_t*>(stage);
       const int G = d >> 7, lane = threadIdx.x & 63;
@@ -87,7 +91,7 @@ __global__ __launch_bounds__(kFillThreads) void fill_kernel(const int32_t* __res
     }
     const int64_t bytes = src.stride[t];  // multiple of 16, <= slot_bytes
     const u32x4* s = reinterpret_cast<const u32x4*>(src.host[t] + (int64_t)id * bytes);
-    u32x4* dst = reinterpret_cast<u32x4*>(slots + (int64_t)slot * slot_bytes);
+    u32x4* dst = reinterpret_cast<u32x4*>(rec);
     const int nvec = (int)(bytes >> 4);
     int v = threadIdx.x;
     for (; v + 3 * kFillThreads < nvec; v += 4 * kFillThreads) {
@@ -124,8 +128,8 @@ hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, const uint8_t* c
                      reinterpret_cast<const int32_t*>(plan + lay.counts),
                      reinterpret_cast<const int32_t*>(plan + lay.fill_ids), plan + lay.fill_tier,
                      reinterpret_cast<const int32_t*>(plan + lay.fill_slot), plan + lay.fill_from,
-                     L->st.slot_rec, src, L->slots, (int64_t)L->info.slot_bytes, L->cap,
-                     L->desc.d_ff, d, L->desc.cache_slots + L->S);
+                     L->st.slot_rec, src, L->slots, L->map, L->cap, L->desc.d_ff, d,
+                     L->desc.cache_slots + L->S);
   return hipGetLastError();
 }
 
@@ -137,16 +141,17 @@ __global__ __launch_bounds__(kFillThreads) void poison_kernel(const int32_t* __r
                                                               const int32_t* __restrict__ fill_slot,
                                                               const uint8_t* __restrict__ fill_from,
                                                               uint8_t* __restrict__ slots,
-                                                              int64_t slot_bytes, int cap,
-                                                              int n_slots) {
+                                                              SlotMap map, int cap, int n_slots) {
   int n = counts[M2C_CNT_FILL];
   n = n < 0 ? 0 : n > cap ? cap : n;
   const u32x4 ones = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
   for (int e = blockIdx.x; e < n; e += gridDim.x) {
     const int t = fill_tier[e], slot = fill_slot[e];
-    if (slot < 0 || slot >= n_slots || (fill_from[e] == 3 && t < 3)) continue;
-    u32x4* dst = reinterpret_cast<u32x4*>(slots + (int64_t)slot * slot_bytes);
-    for (int v = threadIdx.x; v < (int)(slot_bytes >> 4); v += kFillThreads) dst[v] = ones;
+    if (t < 1 || t > 3 || slot < 0 || slot >= n_slots || (fill_from[e] == 3 && t < 3)) continue;
+    if ((uint32_t)(slot - map.first[t]) >= (uint32_t)map.count[t]) continue;
+    u32x4* dst = reinterpret_cast<u32x4*>(slots + map.base[t] +
+                                          (int64_t)(slot - map.first[t]) * map.stride[t]);
+    for (int v = threadIdx.x; v < (int)(map.stride[t] >> 4); v += kFillThreads) dst[v] = ones;
   }
 }
 
@@ -155,7 +160,7 @@ hipError_t launch_poison_fill_slots(const m2c_layer* L, const uint8_t* plan, hip
   hipLaunchKernelGGL(poison_kernel, dim3(kFillBlocks), dim3(kFillThreads), 0, stream,
                      reinterpret_cast<const int32_t*>(plan + lay.counts), plan + lay.fill_tier,
                      reinterpret_cast<const int32_t*>(plan + lay.fill_slot), plan + lay.fill_from,
-                     L->slots, (int64_t)L->info.slot_bytes, L->cap, L->desc.cache_slots + L->S);
+                     L->slots, L->map, L->cap, L->desc.cache_slots + L->S);
   return hipGetLastError();
 }
 

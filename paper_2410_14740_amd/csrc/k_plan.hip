@@ -337,9 +337,14 @@ __device__ __forceinline__ void neuron_tiers(const uint8_t* __restrict__ tm, int
   t = t > 3 ? 3 : t;
 }
 
-__global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
+// pool_tier 0: the whole cache unit. pool_tier t (per-tier arena): only the
+// neurons whose step tier is t, against that pool's state. Every pool's
+// workgroup checks the whole required set against cap, so all of them leave
+// their pool unchanged together when it does not fit; the FP16 pool's
+// workgroup reports it (status word, and *abort for the merge).
+__device__ __forceinline__ void plan_fast_body(
     const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step, int dom,
-    DeviceState st, PlanPtrs P) {
+    const DeviceState& st, const PlanPtrs& P, int pool_tier, int32_t* __restrict__ abort_word) {
   __shared__ uint8_t s_info[kPJ * kPlanThreads];  // tier | code << 2 (1 hit, 2 refill, 0 new)
   __shared__ uint32_t s_touch[kPJ * kPlanThreads / 32];  // slots touched this step
   __shared__ unsigned long long s_ca[kPJ * kPWaves];  // R, NEW, fills per (chunk, wave)
@@ -347,12 +352,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
   __shared__ uint32_t s_cu[kPJ * kPWaves];            // slot compactions per (chunk, wave)
   __shared__ unsigned long long scan64[kPWaves + 1];
   __shared__ uint32_t scan32[kPWaves + 1];
-  __shared__ int sh_hit, sh_refill, sh_empty, sh_f[4], sh_der[2];
+  __shared__ int sh_hit, sh_refill, sh_empty, sh_f[4], sh_der[2], sh_all;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const unsigned long long lt = (1ull << lane) - 1ull;
   const int NJ = (d_ff + kPlanThreads - 1) / kPlanThreads;
   const int NC = (C + kPlanThreads - 1) / kPlanThreads;
   if (tid == 0) {
+    sh_all = 0;
     sh_hit = sh_refill = sh_empty = 0;
     sh_der[0] = sh_der[1] = 0;
     sh_f[0] = sh_f[1] = sh_f[2] = sh_f[3] = 0;
@@ -367,6 +373,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
     for (int g = 0; g < kPGroup; ++g) {
       const int i = min(tid + kPlanThreads * (j0 + g), d_ff - 1);
       neuron_tiers(tier_map, d_ff, i, B, t[g], m[g]);
+      if (pool_tier) {  // the whole required set, for the capacity check
+        const unsigned long long ba = __ballot(j0 + g < NJ && tid + kPlanThreads * (j0 + g) < d_ff &&
+                                               t[g] > 0);
+        if (lane == 0 && ba) atomicAdd(&sh_all, popc(ba));
+      }
+      if (pool_tier && t[g] != pool_tier) t[g] = 0;  // another pool's neuron
       sl[g] = st.slot_of[i];
     }
     int old[kPGroup];
@@ -399,14 +411,17 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
   const unsigned long long totB = scan_entries<unsigned long long>(s_cb, NJ * kPWaves, scan64);
   const int NREQ = fd3(totA, 0), NNEW = fd3(totA, 1), NF = fd3(totA, 2);
   const int N3 = fd3(totB, 0), N2 = fd3(totB, 1), N1 = fd3(totB, 2);
-  if (NREQ > cap) {  // workgroup-uniform: an empty plan, the cache untouched
+  const int NALL = pool_tier ? sh_all : NREQ;  // sh_all is final after the scans' barriers
+  if (NALL > cap) {  // workgroup-uniform: an empty plan, the cache untouched
     if (tid == 0) {
       for (int q = 0; q < M2C_NCOUNTS; ++q) P.counts[q] = 0;
-      P.counts[M2C_NCOUNTS - 1] = NREQ;
-      atomicOr(st.status, M2C_STATUS_PLAN_OVERFLOW);
+      P.counts[M2C_NCOUNTS - 1] = NALL;
+      if (pool_tier == 0 || pool_tier == 3) atomicOr(st.status, M2C_STATUS_PLAN_OVERFLOW);
+      if (pool_tier == 3) *abort_word = 1;
     }
     return;
   }
+  if (pool_tier == 3 && tid == 0) *abort_word = 0;
   // ---------------- A2: required list, NEW list, fill ids, work positions
   for (int j0 = 0; j0 < NJ; j0 += kPGroup) {
     int sl[kPGroup];
@@ -588,7 +603,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
     c[M2C_CNT_FILL_INT4] = F1;
     for (int q = 0; q < M2C_NCOUNTS; ++q) P.counts[q] = c[q];
     *st.lru_cur = 1 - cur;
-    atomicAdd(&st.stats[0], 1ull);
+    if (pool_tier == 0 || pool_tier == 3) atomicAdd(&st.stats[0], 1ull);  // one plan per step
     atomicAdd(&st.stats[1], (unsigned long long)NREQ);
     atomicAdd(&st.stats[2], (unsigned long long)sh_hit);
     atomicAdd(&st.stats[3], (unsigned long long)sh_refill);
@@ -606,7 +621,32 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
   }
 }
 
-__global__ void reset_kernel(DeviceState st, int d_ff, int C, int S) {
+__global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
+    const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step, int dom,
+    DeviceState st, PlanPtrs P, int32_t* __restrict__ abort_word) {
+  plan_fast_body(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word);
+}
+
+// Per-tier arena: workgroup q plans pool 3 - q (FP16, INT8, INT4) into its
+// own plan buffer; the pools are independent, so they run side by side.
+struct PoolJobs {
+  DeviceState st[3];
+  PlanPtrs P[3];
+  int C[3];
+};
+
+__global__ __launch_bounds__(kPlanThreads) void plan_pools_kernel(
+    const uint8_t* __restrict__ tier_map, int B, int d_ff, int cap, int step, PoolJobs jobs,
+    int32_t* __restrict__ abort_word) {
+  const int q = blockIdx.x;
+  plan_fast_body(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q], 3 - q,
+                 abort_word);
+}
+
+// Empties one cache unit (or one pool of the per-tier arena: its own
+// tables); clears n_rec entries of the fill's record table and, with
+// clear_stats, the counters.
+__global__ void reset_kernel(DeviceState st, int d_ff, int C, int n_rec, int clear_stats) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   const int n = gridDim.x * blockDim.x;
   for (int i = idx; i < d_ff; i += n) st.slot_of[i] = -1;
@@ -617,13 +657,125 @@ __global__ void reset_kernel(DeviceState st, int d_ff, int C, int S) {
     st.lru[s] = s;
     st.lru[C + s] = s;
   }
-  for (int s = idx; s < C + S; s += n) st.slot_rec[s] = -1;
+  for (int s = idx; s < n_rec; s += n) st.slot_rec[s] = -1;
   if (idx == 0) *st.lru_cur = 0;
-  if (idx < 16) st.stats[idx] = 0;
+  if (clear_stats && idx < 16) st.stats[idx] = 0;
 }
 
-hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int step, uint8_t* plan,
-                       hipStream_t stream) {
+// Per-tier arena: the three pools' plans (each over its own tier, in
+// ascending id) merged into the caller's plan. R and the fills are merged by
+// id (a neuron has one step tier, so the lists are disjoint: an entry's
+// position is its index in its own list plus the entries of the other lists
+// with smaller ids); the work list is the pools' lists in tier order; the
+// evictions are the pools' evictions in tier order. Slot ids become global.
+struct PoolPlan {
+  const int32_t* counts;
+  const int32_t* req_ids;
+  const uint8_t* req_hit;
+  const int32_t* req_slot;
+  const uint32_t* req_mask;
+  const int32_t* fill_ids;
+  const int32_t* fill_slot;
+  const int32_t* evicted_ids;
+};
+struct PoolPlans {
+  PoolPlan p[3];  // FP16, INT8, INT4
+};
+
+__device__ __forceinline__ int lower_bound(const int32_t* a, int n, int v) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (a[mid] < v) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(256) void plan_merge_kernel(PoolPlans pp, PlanPtrs out, SlotMap map,
+                                                          const int32_t* __restrict__ abort_word) {
+  const bool ab = *abort_word != 0;
+  int nr[3], nf[3], ne[3];
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    nr[q] = ab ? 0 : pp.p[q].counts[M2C_CNT_REQ];
+    nf[q] = ab ? 0 : pp.p[q].counts[M2C_CNT_FILL];
+    ne[q] = ab ? 0 : pp.p[q].counts[M2C_CNT_EVICT];
+  }
+  const int tid = blockIdx.x * blockDim.x + threadIdx.x, nth = gridDim.x * blockDim.x;
+  if (tid < M2C_NCOUNTS) {
+    int v = 0;
+    if (ab)
+      v = tid == M2C_NCOUNTS - 1 ? pp.p[0].counts[M2C_NCOUNTS - 1] : 0;
+    else if (tid <= M2C_CNT_FILL_INT4)
+      v = pp.p[0].counts[tid] + pp.p[1].counts[tid] + pp.p[2].counts[tid];
+    out.counts[tid] = v;
+  }
+  const int R = nr[0] + nr[1] + nr[2];
+  for (int e = tid; e < R; e += nth) {
+    const int q = e < nr[0] ? 0 : e < nr[0] + nr[1] ? 1 : 2;
+    const int p = e - (q > 0 ? nr[0] : 0) - (q > 1 ? nr[1] : 0);
+    const PoolPlan& P = pp.p[q];
+    const int t = 3 - q;
+    const int id = P.req_ids[p];
+    int pos = p;
+#pragma unroll
+    for (int u = 0; u < 3; ++u)
+      if (u != q) pos += lower_bound(pp.p[u].req_ids, nr[u], id);
+    const int gs = P.req_slot[p] + map.first[t];
+    out.req_ids[pos] = id;
+    out.req_tier[pos] = (uint8_t)t;
+    out.req_hit[pos] = P.req_hit[p];
+    out.req_slot[pos] = gs;
+    out.req_mask[pos] = P.req_mask[p];
+    out.work_slot[e] = gs;  // pool order = tier-major, ascending id inside a tier
+    out.work_mask[e] = P.req_mask[p];
+  }
+  const int NF = nf[0] + nf[1] + nf[2];
+  for (int e = tid; e < NF; e += nth) {
+    const int q = e < nf[0] ? 0 : e < nf[0] + nf[1] ? 1 : 2;
+    const int p = e - (q > 0 ? nf[0] : 0) - (q > 1 ? nf[1] : 0);
+    const PoolPlan& P = pp.p[q];
+    const int t = 3 - q;
+    const int id = P.fill_ids[p];
+    int pos = p;
+#pragma unroll
+    for (int u = 0; u < 3; ++u)
+      if (u != q) pos += lower_bound(pp.p[u].fill_ids, nf[u], id);
+    out.fill_ids[pos] = id;
+    out.fill_tier[pos] = (uint8_t)t;
+    out.fill_slot[pos] = P.fill_slot[p] + map.first[t];
+    out.fill_from[pos] = 0;
+  }
+  const int NE = ne[0] + ne[1] + ne[2];
+  for (int e = tid; e < NE; e += nth) {
+    const int q = e < ne[0] ? 0 : e < ne[0] + ne[1] ? 1 : 2;
+    const int p = e - (q > 0 ? ne[0] : 0) - (q > 1 ? ne[1] : 0);
+    out.evicted_ids[e] = pp.p[q].evicted_ids[p];
+  }
+}
+
+DeviceState pool_state(const m2c_layer* L, int t) {
+  DeviceState v = L->st;
+  if (!L->pools) return v;
+  const int q = 3 - t, rf = L->pool_rf[t];
+  v.slot_of = L->st.slot_of + (int64_t)q * L->desc.d_ff;
+  v.slot_key = L->st.slot_key + rf;
+  v.slot_tier = L->st.slot_tier + rf;
+  v.slot_last = L->st.slot_last + rf;
+  v.lru = L->st.lru + 2 * (int64_t)rf;
+  v.lru_cur = L->st.lru_cur + q;
+  const int64_t cap = L->cap;
+  v.new_pos = L->st.new_pos + q * cap;
+  v.work_pos = L->st.work_pos + q * cap;
+  v.vict_slot = L->st.vict_slot + q * cap;
+  v.vict_old = L->st.vict_old + q * cap;
+  v.fill_pos = L->st.fill_pos + q * cap;
+  v.prev_tier = L->st.prev_tier + q * cap;
+  return v;
+}
+
+static PlanPtrs plan_ptrs(const m2c_layer* L, uint8_t* plan) {
   const m2c_plan_layout& lay = L->layout;
   PlanPtrs P;
   P.counts = reinterpret_cast<int32_t*>(plan + lay.counts);
@@ -639,24 +791,66 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
   P.evicted_ids = reinterpret_cast<int32_t*>(plan + lay.evicted_ids);
   P.work_slot = reinterpret_cast<int32_t*>(plan + lay.work_slot);
   P.work_mask = reinterpret_cast<uint32_t*>(plan + lay.work_mask);
+  return P;
+}
+
+hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int step, uint8_t* plan,
+                       hipStream_t stream) {
+  const PlanPtrs P = plan_ptrs(L, plan);
   const int dom = (L->desc.flags & M2C_FLAG_DOMINANT_HITS) ? 1 : 0;
-  if (L->desc.d_ff <= kPJ * kPlanThreads)
-    hipLaunchKernelGGL(plan_fast_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
-                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, dom, L->st, P);
-  else
-    hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
-                       L->desc.d_ff, L->desc.cache_slots, L->cap, step, dom, L->st, P);
+  if (!L->pools) {
+    if (L->desc.d_ff <= kPJ * kPlanThreads)
+      hipLaunchKernelGGL(plan_fast_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
+                         L->desc.d_ff, L->desc.cache_slots, L->cap, step, dom, L->st, P,
+                         L->plan_abort);
+    else
+      hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
+                         L->desc.d_ff, L->desc.cache_slots, L->cap, step, dom, L->st, P);
+    return hipGetLastError();
+  }
+  // per-tier arena (d_ff <= 32768, checked at create): the three pools'
+  // plans side by side in one launch, into the layer's pool plans, then the
+  // merge into the caller's plan
+  PoolPlans pp;
+  PoolJobs jobs;
+  for (int q = 0; q < 3; ++q) {
+    const int t = 3 - q;
+    const PlanPtrs Pq = plan_ptrs(L, L->pool_plan + (int64_t)q * L->info.plan_bytes);
+    jobs.st[q] = pool_state(L, t);
+    jobs.P[q] = Pq;
+    jobs.C[q] = L->pool_C[t];
+    pp.p[q] = {Pq.counts, Pq.req_ids, Pq.req_hit, Pq.req_slot, Pq.req_mask, Pq.fill_ids,
+               Pq.fill_slot, Pq.evicted_ids};
+  }
+  hipLaunchKernelGGL(plan_pools_kernel, dim3(3), dim3(kPlanThreads), 0, stream, tier_map, batch,
+                     L->desc.d_ff, L->cap, step, jobs, L->plan_abort);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  int blocks = (L->cap + 255) / 256;
+  blocks = blocks < 1 ? 1 : blocks > 64 ? 64 : blocks;
+  hipLaunchKernelGGL(plan_merge_kernel, dim3(blocks), dim3(256), 0, stream, pp, P, L->map,
+                     L->plan_abort);
   return hipGetLastError();
 }
 
 hipError_t launch_reset(m2c_layer* L, hipStream_t stream) {
-  const int n = L->desc.d_ff > L->desc.cache_slots ? L->desc.d_ff : L->desc.cache_slots;
+  const int n_rec = L->desc.cache_slots + L->S;
+  int n = L->desc.d_ff > n_rec ? L->desc.d_ff : n_rec;
   int blocks = (n + 255) / 256;
   if (blocks < 1) blocks = 1;
   if (blocks > 1024) blocks = 1024;
-  hipLaunchKernelGGL(reset_kernel, dim3(blocks), dim3(256), 0, stream, L->st, L->desc.d_ff,
-                     L->desc.cache_slots, L->S);
-  return hipGetLastError();
+  if (!L->pools) {
+    hipLaunchKernelGGL(reset_kernel, dim3(blocks), dim3(256), 0, stream, L->st, L->desc.d_ff,
+                       L->desc.cache_slots, n_rec, 1);
+    return hipGetLastError();
+  }
+  for (int t = 3; t >= 1; --t) {
+    hipLaunchKernelGGL(reset_kernel, dim3(blocks), dim3(256), 0, stream, pool_state(L, t),
+                       L->desc.d_ff, L->pool_C[t], t == 3 ? n_rec : 0, t == 3 ? 1 : 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace m2c

@@ -88,8 +88,27 @@ m2c_status check_desc(const m2c_layer_desc* D, int* S_out, int* cap_out) {
   if (S < need)
     return fail(M2C_ERR_INVALID_ARG, "staging_slots %d: at least %d are needed (or -1)",
                 D->staging_slots, need);
-  if (D->flags & ~(M2C_FLAG_DETERMINISTIC_FFN | M2C_FLAG_DOMINANT_HITS))
+  if (D->flags & ~(M2C_FLAG_DETERMINISTIC_FFN | M2C_FLAG_DOMINANT_HITS | M2C_FLAG_TIER_POOLS))
     return fail(M2C_ERR_INVALID_ARG, "flags 0x%x: unknown bits", D->flags);
+  if (D->flags & M2C_FLAG_TIER_POOLS) {
+    if (D->flags & (M2C_FLAG_DETERMINISTIC_FFN | M2C_FLAG_DOMINANT_HITS))
+      return fail(M2C_ERR_INVALID_ARG, "tier pools take neither the deterministic FFN nor "
+                  "dominance hits");
+    if (D->max_batch != 1 || D->d_model > 8192 || D->d_ff > 32768 || D->staging_slots != -1)
+      return fail(M2C_ERR_INVALID_ARG, "tier pools need max_batch 1, d_model <= 8192, d_ff <= "
+                  "32768 and staging_slots -1");
+    int64_t sum = 0;
+    for (int t = 1; t <= 3; ++t) {
+      if (D->tier_slots[t] < 0 || D->tier_slots[t] > D->d_ff)
+        return fail(M2C_ERR_INVALID_ARG, "tier_slots[%d] %d: need [0, d_ff]", t, D->tier_slots[t]);
+      sum += D->tier_slots[t];
+    }
+    if (sum != D->cache_slots)
+      return fail(M2C_ERR_INVALID_ARG, "tier_slots sum to %lld, cache_slots is %d", (long long)sum,
+                  D->cache_slots);
+    S = 0;
+    for (int t = 1; t <= 3; ++t) S += cap - D->tier_slots[t] > 0 ? cap - D->tier_slots[t] : 0;
+  }
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) != hipSuccess || D->device < 0 || D->device >= ndev)
     return fail(M2C_ERR_INVALID_ARG, "device %d: %d HIP devices visible", D->device, ndev);
@@ -109,6 +128,48 @@ void fill_info_layout(m2c_layer* L) {
   I.slot_bytes = 6 * D.d_model;
   I.cache_slots = D.cache_slots;
   I.staging_slots = L->S;
+  // the slot arena: one pool per tier (FP16 first) or one pool of FP16-sized
+  // slots shared by the tiers, then the zero slot
+  L->pools = (D.flags & M2C_FLAG_TIER_POOLS) != 0;
+  int64_t arena = 0;
+  if (L->pools) {
+    int first = 0, rf = 0;
+    for (int t = 3; t >= 1; --t) {
+      L->pool_C[t] = D.tier_slots[t];
+      L->pool_S[t] = L->cap - L->pool_C[t] > 0 ? L->cap - L->pool_C[t] : 0;
+      L->pool_rf[t] = rf;
+      I.pool_first[t] = first;
+      I.pool_slots[t] = L->pool_C[t] + L->pool_S[t];
+      I.pool_resident[t] = L->pool_C[t];
+      I.pool_stride[t] = I.record_stride[t];
+      L->map.base[t] = (uint32_t)arena;
+      L->map.first[t] = first;
+      L->map.count[t] = I.pool_slots[t];
+      L->map.stride[t] = (uint32_t)I.record_stride[t];
+      arena += (int64_t)I.pool_slots[t] * I.pool_stride[t];
+      first += I.pool_slots[t];
+      rf += L->pool_C[t];
+    }
+  } else {
+    for (int t = 1; t <= 3; ++t) {
+      I.pool_first[t] = 0;
+      I.pool_slots[t] = D.cache_slots + L->S;
+      I.pool_resident[t] = D.cache_slots;
+      I.pool_stride[t] = I.slot_bytes;
+      L->map.base[t] = 0;
+      L->map.first[t] = 0;
+      L->map.count[t] = D.cache_slots + L->S;
+      L->map.stride[t] = (uint32_t)I.slot_bytes;
+    }
+    arena = (int64_t)(D.cache_slots + L->S) * I.slot_bytes;
+  }
+  L->map.base[0] = 0;
+  L->map.first[0] = 0;
+  L->map.count[0] = 0;
+  L->map.stride[0] = (uint32_t)I.slot_bytes;
+  L->map.zero = (uint32_t)arena;  // below 4 GiB when the one-launch FFN runs (checked there)
+  L->arena_bytes = arena + I.slot_bytes;
+  I.slot_arena_bytes = L->arena_bytes;
   I.plan_capacity = L->cap;
   m2c_plan_layout& P = L->layout;
   int64_t off = 0;
@@ -162,6 +223,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   const m2c_layer_desc& D = L->desc;
   const int64_t d = D.d_model, dff = D.d_ff, r = D.pred_rank, C = D.cache_slots;
   const int64_t cap = L->cap, mb = D.max_batch;
+  const int64_t np = L->pools ? 3 : 1;
   const int n_slices = (int)((d + 511) / 512);
   // (column slices) x (neuron groups) workgroups for the down projection:
   // about 512, at most 64 partial rows, groups of at least 16 neurons.
@@ -177,11 +239,11 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
   void* p_vslot; void* p_vold; void* p_fill_pos; void* p_prev_tier; void* p_have; void* p_stats;
   void* p_status;
-  void* p_gen; void* p_hw;
+  void* p_gen; void* p_hw; void* p_pool_plan; void* p_abort;
   Piece pieces[] = {
       // C resident + S staging slots, then one slot that stays zero: padding
       // lanes of the FFN kernels read it instead of branching around loads
-      {&p_slots, (C + L->S + 1) * (int64_t)L->info.slot_bytes},
+      {&p_slots, L->arena_bytes},
       {&p_pred_a, r * d * 2},
       {&p_pred_b, dff * r * 2},
       {&p_bias, with_bias ? dff * 4 : 0},
@@ -189,23 +251,26 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_scores, mb * dff * 4},
       {&p_h, 4 * cap * mb * 8},
       {&p_ypart, (int64_t)ng * mb * d * 4},
-      {&p_slot_of, dff * 4},
+      {&p_slot_of, (L->pools ? 3 : 1) * dff * 4},
       {&p_slot_key, C * 4},
       {&p_slot_tier, C},
       {&p_slot_last, C * 4},
       {&p_lru, 2 * C * 4},
-      {&p_lru_cur, 4},
-      {&p_new_pos, cap * 4},
-      {&p_work_pos, cap * 4},
-      {&p_vslot, cap * 4},
-      {&p_vold, cap * 4},
-      {&p_fill_pos, cap * 4},
-      {&p_prev_tier, cap},
+      {&p_lru_cur, 3 * 4},
+      // plan scratch, one set per pool (the pools are planned side by side)
+      {&p_new_pos, np * cap * 4},
+      {&p_work_pos, np * cap * 4},
+      {&p_vslot, np * cap * 4},
+      {&p_vold, np * cap * 4},
+      {&p_fill_pos, np * cap * 4},
+      {&p_prev_tier, np * cap},
       {&p_have, (C + L->S) * 4},
       {&p_stats, 16 * 8},
       {&p_status, 4},
       {&p_gen, (int64_t)m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus) * 8},
       {&p_hw, cap * 8},
+      {&p_pool_plan, L->pools ? 3 * L->info.plan_bytes : 0},
+      {&p_abort, 4},
   };
   int64_t total = 0;
   int64_t offs[sizeof(pieces) / sizeof(pieces[0])];
@@ -244,9 +309,11 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.status = (int32_t*)p_status;
   L->st.ffn_gen = (unsigned long long*)p_gen;
   L->st.ffn_hw = (unsigned long long*)p_hw;
+  L->pool_plan = (uint8_t*)p_pool_plan;
+  L->plan_abort = (int32_t*)p_abort;
   L->info.device_bytes = total;
-  HIPOK(hipMemset(L->slots + (C + L->S) * (int64_t)L->info.slot_bytes, 0, L->info.slot_bytes),
-        "clear the zero slot");
+  HIPOK(hipMemset(L->slots + L->map.zero, 0, L->info.slot_bytes), "clear the zero slot");
+  HIPOK(hipMemset(L->plan_abort, 0, 4), "clear the plan abort word");
   HIPOK(hipMemset(L->st.status, 0, 4), "clear the status word");
   L->ffn_grid = m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus);
   HIPOK(hipMemset(L->st.ffn_gen, 0, (size_t)(L->ffn_grid > 0 ? L->ffn_grid : 1) * 8),
@@ -714,13 +781,36 @@ m2c_status m2c_debug_read_record(const m2c_layer* L, int32_t tier, int32_t neuro
 
 m2c_status m2c_debug_read_slot(const m2c_layer* L, int32_t slot, void* out, size_t bytes) {
   if (!L || !out) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
-  if (slot < 0 || slot >= L->desc.cache_slots + L->S || (int64_t)bytes > L->info.slot_bytes)
+  int tier = 0;
+  for (int t = 1; t <= 3; ++t)
+    if (slot >= L->info.pool_first[t] && slot < L->info.pool_first[t] + L->info.pool_slots[t])
+      tier = t;
+  if (slot < 0 || tier == 0 || (int64_t)bytes > L->info.pool_stride[tier])
     return fail(M2C_ERR_INVALID_ARG, "slot %d / %zu bytes out of range", slot, bytes);
   DeviceGuard g(L->desc.device);
   HIPOK(hipDeviceSynchronize(), "synchronize");
-  HIPOK(hipMemcpy(out, L->slots + (int64_t)slot * L->info.slot_bytes, bytes,
-                  hipMemcpyDeviceToHost),
-        "read slot");
+  const int64_t off = L->map.base[tier] + (int64_t)(slot - L->map.first[tier]) * L->map.stride[tier];
+  HIPOK(hipMemcpy(out, L->slots + off, bytes, hipMemcpyDeviceToHost), "read slot");
+  return M2C_OK;
+}
+
+m2c_status m2c_debug_read_pool_tables(const m2c_layer* L, int32_t tier, int32_t* slot_of,
+                                      int32_t* slot_key, int32_t* slot_last) {
+  if (!L) return fail(M2C_ERR_INVALID_ARG, "NULL argument");
+  if (!L->pools || tier < 1 || tier > 3)
+    return fail(M2C_ERR_INVALID_ARG, "tier %d: the layer has %s", tier,
+                L->pools ? "pools 1..3" : "no tier pools");
+  DeviceGuard g(L->desc.device);
+  const m2c::DeviceState v = m2c::pool_state(L, tier);
+  const size_t C = (size_t)L->pool_C[tier];
+  HIPOK(hipDeviceSynchronize(), "synchronize");
+  if (slot_of)
+    HIPOK(hipMemcpy(slot_of, v.slot_of, (size_t)L->desc.d_ff * 4, hipMemcpyDeviceToHost),
+          "read slot_of");
+  if (slot_key && C)
+    HIPOK(hipMemcpy(slot_key, v.slot_key, C * 4, hipMemcpyDeviceToHost), "read slot_key");
+  if (slot_last && C)
+    HIPOK(hipMemcpy(slot_last, v.slot_last, C * 4, hipMemcpyDeviceToHost), "read slot_last");
   return M2C_OK;
 }
 

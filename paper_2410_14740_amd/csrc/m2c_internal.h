@@ -54,6 +54,19 @@ struct DeviceState {
   unsigned long long* ffn_hw = nullptr;   // [cap] (call tag, h) words of the one-launch FFN
 };
 
+// Where the record in a slot starts: a slot of tier t's pool at global id s,
+// first[t] <= s < first[t] + count[t], holds its record at byte
+// base[t] + (s - first[t]) * stride[t] of the arena; `zero` is the all-zero
+// padding slot (where every id outside the tier's pool points). Without tier
+// pools every tier maps with base 0, first 0, count C + S, stride slot_bytes.
+struct SlotMap {
+  uint32_t base[4];
+  int32_t first[4];
+  int32_t count[4];
+  uint32_t stride[4];
+  uint32_t zero;
+};
+
 }  // namespace m2c
 
 struct m2c_layer {
@@ -82,6 +95,15 @@ struct m2c_layer {
   int ffn_withhold = 0;  // test support: > 0 = h words withheld, polls before giving up
   m2c_dram* dram = nullptr;  // records come from this DRAM cache (store is null)
   int dram_index = -1;
+  // per-tier record arena (M2C_FLAG_TIER_POOLS)
+  bool pools = false;
+  int pool_C[4] = {0, 0, 0, 0};   // resident slots per tier
+  int pool_S[4] = {0, 0, 0, 0};   // staging slots per tier
+  int pool_rf[4] = {0, 0, 0, 0};  // first resident table index of the pool
+  m2c::SlotMap map;               // slot id -> byte offset, by tier
+  int64_t arena_bytes = 0;        // pools + zero slot
+  uint8_t* pool_plan = nullptr;   // [3][plan_bytes] the pools' own plans
+  int32_t* plan_abort = nullptr;  // [1] set when a step's required set overflowed
 };
 
 namespace m2c {
@@ -124,6 +146,8 @@ hipError_t launch_reset(m2c_layer* L, hipStream_t stream);
 hipError_t launch_fill(const m2c_layer* L, const uint8_t* plan, const uint8_t* const host[4],
                        hipStream_t stream);
 hipError_t launch_poison_fill_slots(const m2c_layer* L, const uint8_t* plan, hipStream_t stream);
+// The state and plan pointers of tier t's pool (M2C_FLAG_TIER_POOLS).
+DeviceState pool_state(const m2c_layer* L, int t);
 hipError_t launch_ffn(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan, float* y,
                       hipStream_t stream);
 hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const uint8_t* plan,

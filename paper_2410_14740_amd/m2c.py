@@ -37,12 +37,13 @@ class M2CError(RuntimeError):
 
 FLAG_DETERMINISTIC_FFN = 1
 FLAG_DOMINANT_HITS = 2
+FLAG_TIER_POOLS = 4
 
 
 class LayerDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "d_model", "d_ff", "pred_rank", "group", "k_max", "max_batch", "cache_slots",
-        "staging_slots", "device", "flags")]
+        "staging_slots", "device", "flags")] + [("tier_slots", ctypes.c_int32 * 4)]
 
 
 class LayerInfo(ctypes.Structure):
@@ -51,7 +52,9 @@ class LayerInfo(ctypes.Structure):
         ("slot_bytes", ctypes.c_int32), ("cache_slots", ctypes.c_int32),
         ("staging_slots", ctypes.c_int32), ("plan_capacity", ctypes.c_int32),
         ("plan_bytes", ctypes.c_int64), ("host_store_bytes", ctypes.c_int64),
-        ("device_bytes", ctypes.c_int64)]
+        ("device_bytes", ctypes.c_int64), ("pool_first", ctypes.c_int32 * 4),
+        ("pool_slots", ctypes.c_int32 * 4), ("pool_resident", ctypes.c_int32 * 4),
+        ("pool_stride", ctypes.c_int32 * 4), ("slot_arena_bytes", ctypes.c_int64)]
 
 
 PLAN_FIELDS = ("counts", "req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "fill_ids",
@@ -124,6 +127,7 @@ def load(path: str = LIB_PATH):
         "m2c_debug_read_record": (I32, [P, I32, I32, P, S]),
         "m2c_debug_read_slot": (I32, [P, I32, P, S]),
         "m2c_debug_read_tables": (I32, [P, P, P, P, P]),
+        "m2c_debug_read_pool_tables": (I32, [P, I32, P, P, P]),
         "m2c_debug_poison_fill_slots": (I32, [P, P, P]),
         "m2c_debug_ffn_withhold_h": (I32, [P, I32]),
         "m2c_layer_write_store": (I32, [P, ctypes.c_char_p, I64, ctypes.POINTER(I64)]),
@@ -375,6 +379,16 @@ def m2c_ratio_search(layer, x, T: int, n_low0: int, step: int, bit_ratio: int, s
     return list(zip(nh[:n].tolist(), nl[:n].tolist())), uq[:n].tolist(), best.value
 
 
+def m2c_debug_read_pool_tables(layer, tier: int, d_ff: int, C: int):
+    """(slot_of [d_ff], slot_key [C], slot_last [C]) of tier `tier`'s pool."""
+    slot_of = np.empty(d_ff, np.int32)
+    key = np.empty(max(C, 1), np.int32)
+    last = np.empty(max(C, 1), np.int32)
+    _check(load().m2c_debug_read_pool_tables(layer, tier, slot_of.ctypes.data, key.ctypes.data,
+                                             last.ctypes.data))
+    return slot_of, key[:C], last[:C]
+
+
 def m2c_last_error() -> str:
     return load().m2c_last_error().decode()
 
@@ -461,6 +475,23 @@ class Layer:
 
 
 def make_desc(d_model, d_ff, pred_rank, k_max, cache_slots, max_batch=1, staging_slots=-1,
-              device=0, flags=0) -> LayerDesc:
+              device=0, flags=0, tier_slots=None) -> LayerDesc:
+    """tier_slots: {tier: resident slots} of the per-tier arena; sets
+    FLAG_TIER_POOLS and cache_slots to their sum."""
+    ts = (ctypes.c_int32 * 4)(0, 0, 0, 0)
+    if tier_slots is not None:
+        for t in (1, 2, 3):
+            ts[t] = tier_slots[t]
+        cache_slots = sum(tier_slots[t] for t in (1, 2, 3))
+        flags |= FLAG_TIER_POOLS
     return LayerDesc(d_model, d_ff, pred_rank, 128, k_max, max_batch, cache_slots, staging_slots,
-                     device, flags)
+                     device, flags, ts)
+
+
+def pool_slots_for_budget(d_model: int, counts, budget_bytes: int) -> dict:
+    """Resident slots per tier for a per-tier arena of at most `budget_bytes`
+    of records: every pool gets the same multiple of its tier's per-step
+    demand (counts = {tier: neurons per step}), rounded down."""
+    stride = {t: (m2c_record_bytes(d_model, t) + 15) // 16 * 16 for t in (1, 2, 3)}
+    demand = sum(counts[t] * stride[t] for t in (1, 2, 3))
+    return {t: int(counts[t] * budget_bytes // demand) for t in (1, 2, 3)}

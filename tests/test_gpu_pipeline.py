@@ -74,18 +74,24 @@ def _check_plan(L, raw, o, where):
     assert g["counts"][m2c.CNT_FILL_DERIVED] == derived_fills(o), f"{where}: derived count"
 
 
+POOLS = {3: 20, 2: 80, 1: 120}  # below each tier's demand (35 / 140 / 175)
+
+
 @pytest.mark.parametrize("n_layers,lag,hold,poison,flags", [
     (4, 2, False, False, 0),
     (4, 2, True, True, 0),
     (2, 1, True, True, 0),
     (3, 2, True, True, m2c.FLAG_DOMINANT_HITS),
+    (3, 2, True, True, m2c.FLAG_TIER_POOLS),
 ])
 def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
     d, d_ff, r, steps = 512, 1400, 32, 12
     k = 350
     n16, n8 = k // 10, (k // 2) - k // 10
     C = 250  # below k: evictions and bypasses through staging slots every step
-    desc = m2c.make_desc(d, d_ff, r, k, C, flags=flags)
+    pools = bool(flags & m2c.FLAG_TIER_POOLS)
+    desc = (m2c.make_desc(d, d_ff, r, k, 0, tier_slots=POOLS) if pools
+            else m2c.make_desc(d, d_ff, r, k, C, flags=flags))
     policy = oracle.POLICY_DOMINANCE if flags & m2c.FLAG_DOMINANT_HITS else oracle.POLICY_EXACT
     lds = [W.make_layer(900 + n_layers, l, d, d_ff, r, steps, rhos=(0.8,)) for l in range(n_layers)]
     layers = [m2c.Layer(desc, ld) for ld in lds]
@@ -107,7 +113,10 @@ def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
     arch = archive.cpu()
     worst = 0.0
     for l, (L, ld) in enumerate(zip(layers, lds)):
-        cache = oracle.LRUCache(d_ff, C, L.info.staging_slots, policy)
+        if pools:
+            cache = oracle.TierPoolCache(d_ff, POOLS, {t: max(0, k - POOLS[t]) for t in (1, 2, 3)})
+        else:
+            cache = oracle.LRUCache(d_ff, C, L.info.staging_slots, policy)
         tot = np.zeros(16, np.int64)
         for t in range(steps):
             _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
@@ -119,9 +128,17 @@ def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
             err = r8_errors(yg[t, l], y_ref).max()
             worst = max(worst, err)
             assert err <= FFN_TOL, f"layer {l} step {t}: FFN error {err:.3e}"
-        slot_of, key, stier, last = m2c.m2c_debug_read_tables(L.handle, d_ff, C)
-        assert np.array_equal(slot_of, cache.slot_of) and np.array_equal(key, cache.slot_key[:C])
-        assert np.array_equal(stier, cache.slot_tier[:C]) and np.array_equal(last, cache.slot_last[:C])
+        if pools:
+            for tr in (1, 2, 3):
+                so, key, last = m2c.m2c_debug_read_pool_tables(L.handle, tr, d_ff, POOLS[tr])
+                pc = cache.pools[tr]
+                assert np.array_equal(so, pc.slot_of) and np.array_equal(key, pc.slot_key[:POOLS[tr]])
+                assert np.array_equal(last, pc.slot_last[:POOLS[tr]])
+        else:
+            slot_of, key, stier, last = m2c.m2c_debug_read_tables(L.handle, d_ff, C)
+            assert np.array_equal(slot_of, cache.slot_of) and np.array_equal(key, cache.slot_key[:C])
+            assert np.array_equal(stier, cache.slot_tier[:C])
+            assert np.array_equal(last, cache.slot_last[:C])
         st = L.stats()  # raises if a plan overflowed or an FFN gave up waiting
         assert (st.plans, st.req, st.hit, st.refill, st.new_, st.bypass) == (
             steps, tot[0], tot[1], tot[2], tot[3], tot[4])
