@@ -53,9 +53,13 @@ def parse_args():
     p.add_argument("--policy", choices=("exact", "dominance"), default="exact",
                    help="cache hits: exact tier (default) or a resident tier at or above the "
                         "requested one")
-    p.add_argument("--tier-pools", action="store_true",
-                   help="per-tier record arena: the HBM of the workload's C FP16-sized slots split "
-                        "into one pool per tier, each the same multiple of its tier's demand")
+    p.add_argument("--arena", choices=("pools", "single"), default="pools",
+                   help="pools (default): the HBM of the workload's C FP16-sized slots split into "
+                        "one pool per tier, each the same multiple of its tier's per-step demand; "
+                        "single: C FP16-sized slots shared by every tier")
+    p.add_argument("--no-variants", action="store_true",
+                   help="skip the single-arena stacks (exact-tier and dominance hits) reported "
+                        "beside the headline")
     p.add_argument("--policy-sweep", action="store_true",
                    help="only the cache-policy measurement: hit rates of exact-tier and "
                         "dominance hits, LRU at C = 30%% and at C = k (the ATU regime), against "
@@ -157,7 +161,7 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy):
+def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy, tier_slots=None):
     """The oracle on a bounded sample of the same work: layer 0 of the stack,
     consecutive decode steps of predict + select + LRU plan + fp64 sparse FFN
     until about `budget_s` seconds have run, timed twice: at one thread (the
@@ -185,7 +189,11 @@ def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy):
 
     def leg(threads, budget):
         oracle.set_threads(threads)
-        cache = oracle.LRUCache(wl.d_ff, C, max(0, cap - C), policy)
+        if tier_slots is None:
+            cache = oracle.LRUCache(wl.d_ff, C, max(0, cap - C), policy)
+        else:
+            cache = oracle.TierPoolCache(wl.d_ff, tier_slots,
+                                         {t: max(0, cap - tier_slots[t]) for t in (1, 2, 3)})
         t_start = time.perf_counter()
         done = 0
         for t in range(steps_avail):
@@ -879,13 +887,26 @@ def main():
         8 if wl.name == "llama2-70b" else 0)
     flags = ffn_flags | (m2c.FLAG_DOMINANT_HITS if args.policy == "dominance" else 0)
     tier_slots = None
-    if args.tier_pools:
+    if args.arena == "pools":
+        if args.policy == "dominance":
+            sys.exit("dominance hits need --arena single")
         tier_slots = m2c.pool_slots_for_budget(wl.d_model, {3: n16, 2: n8, 1: n4},
                                                wl.cache_slots() * 6 * wl.d_model)
         log(f"per-tier arena: {tier_slots} resident slots (FP16, INT8, INT4 pools)")
     r = run_stack(wl, n_layers, args.steps, args.warmup, weight_sets, flags, args.overlap_steps,
                   args.stage_events, torch, m2c, W, tier_slots=tier_slots)
     log(f"stack: {r['tokens_per_s']:.2f} tokens/s")
+    variants = {}
+    if not args.no_variants and tier_slots is not None:
+        for name, fl in (("single_arena_exact_tier", ffn_flags),
+                         ("single_arena_dominance", ffn_flags | m2c.FLAG_DOMINANT_HITS)):
+            rv = run_stack(wl, n_layers, args.steps, args.warmup, weight_sets, fl, 0, False, torch,
+                           m2c, W)
+            variants[name] = {"tokens_per_s": rv["tokens_per_s"],
+                              "us_per_layer_step": rv["us_per_layer_step"],
+                              "host_MB_per_layer_step": rv["pipeline"]["fill_MB_per_layer_step"],
+                              "cache": rv["pipeline"]["cache"]}
+            log(f"variant {name}: {rv['tokens_per_s']:.2f} tokens/s")
     log(f"isolated sparse FFN on {args.ffn_layers} {wl.name}-shaped layers")
     iso = ffn_isolated(wl, args.ffn_layers, args.ffn_reps, torch, m2c, W, flags=ffn_flags)
     extra = None
@@ -900,7 +921,7 @@ def main():
         log("timing the oracle on the host")
         cpu = cpu_baseline(wl, r["ld0"], n_layers, args.cpu_seconds, oracle,
                            oracle.POLICY_DOMINANCE if args.policy == "dominance"
-                           else oracle.POLICY_EXACT)
+                           else oracle.POLICY_EXACT, tier_slots)
 
     # HBM bytes per call from the committed counter summary of this layer
     # shape, or None when the FFN kernels have changed since it was taken
@@ -960,6 +981,7 @@ def main():
         # the fills are bound by the host link, not by HBM
         "host_link": r["host_link"],
         "cpu_baseline": cpu,
+        "variants": variants or None,
     }
     print(json.dumps(out), flush=True)
 
