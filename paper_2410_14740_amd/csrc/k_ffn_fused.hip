@@ -65,6 +65,7 @@ constexpr int kFSpin = 1 << 16;          // polls of one h word before giving up
 constexpr float kTwo24 = 16777216.0f;
 static_assert(kFMaxItems <= kFT, "one slot id / h word per thread");
 static_assert(kFLPN == 16, "the fold pairs lanes 16 and 32 apart");
+static_assert(kFSW == kFT, "the cross-wave fold gives thread c column c of the slice");
 
 struct FMap {
   int n3, n2, n1;  // work items by tier
@@ -443,14 +444,34 @@ struct FShared {
   float2 ab[kFWaves * kFL];    // h task: per-unit gate / up sums
 };
 
-// Down fold: kFT / kFLPN lane groups (lanes with equal tid / kFLPN) each hold
-// 16 columns of half a slice per lane; the groups are summed through LDS.
-// Lane t stores its q-th four sums as the 16-byte granule q * kFFoldStride + t
-// (consecutive lanes, consecutive granules); the 4-granule pad per q puts the
-// 64 reads of a wave (4 q x 4 column groups x 4 words) on 64 distinct banks.
-constexpr int kFGroups = kFT / kFLPN;
-constexpr int kFFoldStride = kFT + 4;
-constexpr size_t kFFoldBytes = (size_t)(3 * kFFoldStride + kFT) * 16;
+// Sum over the four lane groups of a wave (lanes 16 apart hold the same
+// columns of four neurons): 16 column sums per lane in, 4 out. Lanes l and
+// l + 32 swap halves of their sums (the lower lane keeps columns 0..7, the
+// upper 8..15), then lanes l and l + 16 within each half do the same with what
+// is left, so lane l ends with columns 4 (l / 16) .. 4 (l / 16) + 3.
+__device__ __forceinline__ void wave_fold16(const float (&acc)[16], float (&out)[4]) {
+  float a[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[e]),
+                                                    __float_as_uint(acc[8 + e]), false, false);
+    a[e] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a[e]),
+                                                    __float_as_uint(a[4 + e]), false, false);
+    out[e] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+}
+
+// Cross-wave sums of a down task: wave w stores the 32 columns of lane group
+// i (lane % 16) as row i of its [16][36] block (the 4-word pad spreads the 64
+// lanes' 16-byte stores over every bank); thread c then adds column c of the
+// kFWaves blocks.
+constexpr int kFRow = 36;
+constexpr int kFBlock = (kFSW / 32) * kFRow;
+constexpr size_t kFFoldBytes = (size_t)kFWaves * kFBlock * 4;
 
 // Dynamic LDS: x [d/8] | -128 * sums of 16 elements [d/16] | -8 * sums of 32
 // [d/32] for h tasks; the same bytes hold the fold of a down task.
@@ -556,37 +577,34 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
     }
     sh.h[tid] = h;
     __syncthreads();
-    // Lanes tid % kFLPN of every group share columns. Per half slice, each
-    // lane writes its 16 sums to LDS and thread c < 256 adds column c's
-    // kFGroups partials in a fixed order, then one fp32 atomic per column
-    // (a workgroup barrier does not wait for it).
+    // Per half slice: 16 column sums per lane, folded over the wave's four
+    // neurons of each round to 4 (columns 4 g .. 4 g + 3 of the half, g =
+    // lane / 16); then the waves through LDS and one fp32 atomic add per
+    // column.
+    // (each lane stores its own four sums of a half as soon as they are
+    // folded: the LDS bytes are not used otherwise by a down task)
     float* part = reinterpret_cast<float*>(xlds);
-    auto fold_half = [&](const float (&acc)[16], int half) {
-      float4* dst = reinterpret_cast<float4*>(part) + tid;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        dst[q * kFFoldStride] =
-            make_float4(acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]);
-      __syncthreads();
-      if (tid < kFLPN * 16) {
-        // column tid of the half slice: lane group member tid >> 4, sum (tid & 15)
-        const float* src = part + 4 * ((tid & 15) >> 2) * kFFoldStride + 4 * (tid >> 4) + (tid & 3);
-        float v = 0.0f;
-        for (int g = 0; g < kFGroups; ++g) v += src[g * kFLPN * 4];
-        const int col = kc.slice * kFSW + 32 * (tid >> 4) + 16 * half + (tid & 15);
-        if (col < d) atomicAdd(y + col, v);
-      }
-      __syncthreads();
-    };
+    float* row = part + (tid >> 6) * kFBlock + (tid & 15) * kFRow + 4 * ((tid & 63) >> 4);
     {
-      float acc[16];
+      float acc[16], o[4];
       compute_dn_half<0>(kc, cur, sh.h, tid, acc);
-      fold_half(acc, 0);
+      wave_fold16(acc, o);
+      *reinterpret_cast<float4*>(row) = make_float4(o[0], o[1], o[2], o[3]);
     }
     {
-      float acc[16];
+      float acc[16], o[4];
       compute_dn_half<1>(kc, cur, sh.h, tid, acc);
-      fold_half(acc, 1);
+      wave_fold16(acc, o);
+      *reinterpret_cast<float4*>(row + 16) = make_float4(o[0], o[1], o[2], o[3]);
+    }
+    __syncthreads();
+    {
+      const float* src = part + (tid >> 5) * kFRow + (tid & 31);
+      float v = 0.0f;
+#pragma unroll
+      for (int w = 0; w < kFWaves; ++w) v += src[w * kFBlock];
+      const int col = kc.slice * kFSW + tid;
+      if (col < d) atomicAdd(y + col, v);
     }
   }
   if (tid == 0) gen[t] = e0 + 1;
