@@ -282,6 +282,45 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
   }
 }
 
+// Unscaled dot products of one 16-byte chunk of INT8 (16 codes) or INT4 (32
+// codes) weights with their x elements (x0, x1 / xq: the chunk's x as it sits
+// in LDS), offset codes as fp16 denormals: sum of (q + 128) x or (q + 8) x,
+// times 2^-24.
+__device__ __forceinline__ float chunk_int8(const uint4 v, const uint4 x0, const uint4 x1) {
+  const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+  const uint32_t xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  float t = 0.0f;
+#pragma unroll
+  for (int u4 = 0; u4 < 4; ++u4) {
+    const uint32_t ob = wv[u4] ^ 0x80808080u;  // q + 128
+    const uint32_t l = __builtin_amdgcn_perm(0u, ob, 0x0c010c00u);
+    const uint32_t h = __builtin_amdgcn_perm(0u, ob, 0x0c030c02u);
+    t = fmaf(lo_f(l), lo_f(xv[2 * u4]), t);
+    t = fmaf(hi_f(l), hi_f(xv[2 * u4]), t);
+    t = fmaf(lo_f(h), lo_f(xv[2 * u4 + 1]), t);
+    t = fmaf(hi_f(h), hi_f(xv[2 * u4 + 1]), t);
+  }
+  return t;
+}
+__device__ __forceinline__ float chunk_int4(const uint4 v, const uint4 (&xq)[4]) {
+  const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+  float t = 0.0f;
+#pragma unroll
+  for (int u4 = 0; u4 < 4; ++u4) {
+    const uint32_t xw[4] = {xq[u4].x, xq[u4].y, xq[u4].z, xq[u4].w};  // x[8 u4 .. 8 u4 + 7]
+    const uint32_t ob = wv[u4] ^ 0x88888888u;  // q + 8
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) {
+      // nibbles s4 and s4 + 4 of the word go with x elements s4 and s4 + 4
+      const uint32_t p = (ob >> (4 * s4)) & 0x000f000fu;
+      const uint32_t xa = xw[s4 >> 1], xb = xw[2 + (s4 >> 1)];
+      t = fmaf(lo_f(p), (s4 & 1) ? hi_f(xa) : lo_f(xa), t);
+      t = fmaf(hi_f(p), (s4 & 1) ? hi_f(xb) : lo_f(xb), t);
+    }
+  }
+  return t;
+}
+
 // Gate / up partial dot products of an h task; per unit (a, b) into s_ab.
 template <int K>
 __device__ __forceinline__ void compute_h(const FTask& k, const FBuf& b, int d,
@@ -295,60 +334,70 @@ __device__ __forceinline__ void compute_h(const FTask& k, const FBuf& b, int d,
   float a[UW], bb[UW];
 #pragma unroll
   for (int uw = 0; uw < UW; ++uw) a[uw] = bb[uw] = 0.0f;
+  if (K >= 2 && d == 1024 * K) {
+    // A unit's rows fill its K loads exactly: load jj < K / 2 of a lane is
+    // the gate chunk c and load jj + K / 2 the up chunk c, so the x of c is
+    // read from LDS once for both.
 #pragma unroll
-  for (int j = 0; j < kFL; ++j) {
-    const int uw = j / K;
-    const int u = w * UW + uw;
-    const int part = u % upi;
-    int q = lane + 64 * (j % K);
-    q = q < 2 * ncu ? q : 2 * ncu - 1;
-    const bool up = q >= ncu;
-    const int c = part * ncu + (up ? q - ncu : q);
-    float p;
-    if (k.tier == 3) {
-      // + 0 * (scale read from the zero slot): keeps that load unconditional
-      p = fmaf(0.0f, h2f((uint16_t)b.s[j]), dot8_f16(b.v[j], xs[c], 0.0f));
-    } else if (k.tier == 2) {
-      const uint4 x0 = xs[2 * c], x1 = xs[2 * c + 1];
-      const uint32_t wv[4] = {b.v[j].x, b.v[j].y, b.v[j].z, b.v[j].w};
-      const uint32_t xv[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      float t = 0.0f;
+    for (int uw = 0; uw < UW; ++uw) {
+      const int part = (w * UW + uw) % upi;
 #pragma unroll
-      for (int u4 = 0; u4 < 4; ++u4) {
-        const uint32_t ob = wv[u4] ^ 0x80808080u;  // q + 128
-        const uint32_t l = __builtin_amdgcn_perm(0u, ob, 0x0c010c00u);
-        const uint32_t h = __builtin_amdgcn_perm(0u, ob, 0x0c030c02u);
-        t = fmaf(lo_f(l), lo_f(xv[2 * u4]), t);
-        t = fmaf(hi_f(l), hi_f(xv[2 * u4]), t);
-        t = fmaf(lo_f(h), lo_f(xv[2 * u4 + 1]), t);
-        t = fmaf(hi_f(h), hi_f(xv[2 * u4 + 1]), t);
-      }
-      p = h2f((uint16_t)b.s[j]) * fmaf(t, kTwo24, nx16[c]);
-    } else {
-      const uint32_t wv[4] = {b.v[j].x, b.v[j].y, b.v[j].z, b.v[j].w};
-      float t = 0.0f;
+      for (int jj = 0; jj < K / 2; ++jj) {
+        const int jg = uw * K + jj, ju = jg + K / 2;
+        const int c = part * ncu + lane + 64 * jj;
+        float pg, pu;
+        if (k.tier == 3) {
+          // + 0 * (scale read from the zero slot): keeps that load unconditional
+          const uint4 xc = xs[c];
+          pg = fmaf(0.0f, h2f((uint16_t)b.s[jg]), dot8_f16(b.v[jg], xc, 0.0f));
+          pu = fmaf(0.0f, h2f((uint16_t)b.s[ju]), dot8_f16(b.v[ju], xc, 0.0f));
+        } else if (k.tier == 2) {
+          const uint4 x0 = xs[2 * c], x1 = xs[2 * c + 1];
+          const float o = nx16[c];
+          pg = h2f((uint16_t)b.s[jg]) * fmaf(chunk_int8(b.v[jg], x0, x1), kTwo24, o);
+          pu = h2f((uint16_t)b.s[ju]) * fmaf(chunk_int8(b.v[ju], x0, x1), kTwo24, o);
+        } else {
+          uint4 xq[4];
 #pragma unroll
-      for (int u4 = 0; u4 < 4; ++u4) {
-        const uint4 xq = xs[4 * c + u4];  // x[8 u4 .. 8 u4 + 7] of the chunk, in pairs
-        const uint32_t xw[4] = {xq.x, xq.y, xq.z, xq.w};
-        const uint32_t ob = wv[u4] ^ 0x88888888u;  // q + 8
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-          // nibbles s4 and s4 + 4 of the word go with x elements s4 and s4 + 4
-          const uint32_t p = (ob >> (4 * s4)) & 0x000f000fu;
-          const uint32_t xa = xw[s4 >> 1], xb = xw[2 + (s4 >> 1)];
-          t = fmaf(lo_f(p), (s4 & 1) ? hi_f(xa) : lo_f(xa), t);
-          t = fmaf(hi_f(p), (s4 & 1) ? hi_f(xb) : lo_f(xb), t);
+          for (int u4 = 0; u4 < 4; ++u4) xq[u4] = xs[4 * c + u4];
+          const float o = nx32[c];
+          pg = h2f((uint16_t)b.s[jg]) * fmaf(chunk_int4(b.v[jg], xq), kTwo24, o);
+          pu = h2f((uint16_t)b.s[ju]) * fmaf(chunk_int4(b.v[ju], xq), kTwo24, o);
         }
+        a[uw] += pg;
+        bb[uw] += pu;
+        // one chunk at a time: keeps the x reads of later chunks from being
+        // hoisted into registers all at once
+        __builtin_amdgcn_sched_barrier(0);
       }
-      p = h2f((uint16_t)b.s[j]) * fmaf(t, kTwo24, nx32[c]);
     }
-    // lanes past the unit read the zero slot: data 0 (FP16) or scale 0
-    a[uw] += up ? 0.0f : p;
-    bb[uw] += up ? p : 0.0f;
-    // one chunk at a time: keeps the x reads of later chunks from being
-    // hoisted into registers all at once
-    __builtin_amdgcn_sched_barrier(0);
+  } else {
+#pragma unroll
+    for (int j = 0; j < kFL; ++j) {
+      const int uw = j / K;
+      const int u = w * UW + uw;
+      const int part = u % upi;
+      int q = lane + 64 * (j % K);
+      q = q < 2 * ncu ? q : 2 * ncu - 1;
+      const bool up = q >= ncu;
+      const int c = part * ncu + (up ? q - ncu : q);
+      float p;
+      if (k.tier == 3) {
+        p = fmaf(0.0f, h2f((uint16_t)b.s[j]), dot8_f16(b.v[j], xs[c], 0.0f));
+      } else if (k.tier == 2) {
+        p = h2f((uint16_t)b.s[j]) * fmaf(chunk_int8(b.v[j], xs[2 * c], xs[2 * c + 1]), kTwo24,
+                                         nx16[c]);
+      } else {
+        uint4 xq[4];
+#pragma unroll
+        for (int u4 = 0; u4 < 4; ++u4) xq[u4] = xs[4 * c + u4];
+        p = h2f((uint16_t)b.s[j]) * fmaf(chunk_int4(b.v[j], xq), kTwo24, nx32[c]);
+      }
+      // lanes past the unit read the zero slot: data 0 (FP16) or scale 0
+      a[uw] += up ? 0.0f : p;
+      bb[uw] += up ? p : 0.0f;
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 #pragma unroll
   for (int uw = 0; uw < UW; ++uw) {
