@@ -302,23 +302,36 @@ __device__ __forceinline__ float chunk_int8(const uint4 v, const uint4 x0, const
   }
   return t;
 }
+// INT4 codes to fp16 lanes by masks alone: nibble n of a word is x element n
+// of its 8; nibbles 0 | 4 and, after a shift by 8, 2 | 6 land in the low bits
+// of the two fp16 halves (value q + 8), nibbles 1 | 5 and 3 | 7 four bits up
+// (16 times that value, still an exact denormal). The two kinds are summed
+// apart and joined with an exact 1/16.
+struct Nib4 {
+  uint32_t p0, p1, p2, p3;  // nibbles (0, 4), (1, 5) x 16, (2, 6), (3, 7) x 16
+};
+__device__ __forceinline__ Nib4 nibbles(uint32_t w) {
+  const uint32_t w8 = w >> 8;
+  return {(w ^ 0x88888888u) & 0x000f000fu, (w ^ 0x88888888u) & 0x00f000f0u,
+          (w8 ^ 0x88888888u) & 0x000f000fu, (w8 ^ 0x88888888u) & 0x00f000f0u};
+}
 __device__ __forceinline__ float chunk_int4(const uint4 v, const uint4 (&xq)[4]) {
   const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-  float t = 0.0f;
+  float ta = 0.0f, tb = 0.0f;  // codes at their value, codes at 16 times it
 #pragma unroll
   for (int u4 = 0; u4 < 4; ++u4) {
     const uint32_t xw[4] = {xq[u4].x, xq[u4].y, xq[u4].z, xq[u4].w};  // x[8 u4 .. 8 u4 + 7]
-    const uint32_t ob = wv[u4] ^ 0x88888888u;  // q + 8
-#pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) {
-      // nibbles s4 and s4 + 4 of the word go with x elements s4 and s4 + 4
-      const uint32_t p = (ob >> (4 * s4)) & 0x000f000fu;
-      const uint32_t xa = xw[s4 >> 1], xb = xw[2 + (s4 >> 1)];
-      t = fmaf(lo_f(p), (s4 & 1) ? hi_f(xa) : lo_f(xa), t);
-      t = fmaf(hi_f(p), (s4 & 1) ? hi_f(xb) : lo_f(xb), t);
-    }
+    const Nib4 n = nibbles(wv[u4]);
+    ta = fmaf(lo_f(n.p0), lo_f(xw[0]), ta);
+    ta = fmaf(hi_f(n.p0), lo_f(xw[2]), ta);
+    tb = fmaf(lo_f(n.p1), hi_f(xw[0]), tb);
+    tb = fmaf(hi_f(n.p1), hi_f(xw[2]), tb);
+    ta = fmaf(lo_f(n.p2), lo_f(xw[1]), ta);
+    ta = fmaf(hi_f(n.p2), lo_f(xw[3]), ta);
+    tb = fmaf(lo_f(n.p3), hi_f(xw[1]), tb);
+    tb = fmaf(hi_f(n.p3), hi_f(xw[3]), tb);
   }
-  return t;
+  return fmaf(tb, 0.0625f, ta);
 }
 
 // Gate / up partial dot products of an h task; per unit (a, b) into s_ab.
@@ -466,17 +479,27 @@ __device__ __forceinline__ void compute_dn_half(const FTask& k, const FBuf& b, c
       const uint32_t ws[2] = {HALF ? b.v[q].z : b.v[q].x, HALF ? b.v[q].w : b.v[q].y};
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const uint32_t ob = ws[u] ^ 0x88888888u;
-#pragma unroll
-        for (int s4 = 0; s4 < 4; ++s4) {
-          const uint32_t p = (ob >> (4 * s4)) & 0x000f000fu;  // nibbles s4 and s4 + 4
-          acc[8 * u + s4] = fmaf(cs, lo_f(p), acc[8 * u + s4]);
-          acc[8 * u + s4 + 4] = fmaf(cs, hi_f(p), acc[8 * u + s4 + 4]);
-        }
+        // column 8 u + e is nibble e; odd columns sum 16 times their value.
+        // Nibbles 0..3 first, then 4..7 (after the barrier): fewer codes live.
+        const uint32_t w = ws[u] ^ 0x88888888u;
+        const uint32_t p0 = w & 0x000f000fu, p1 = w & 0x00f000f0u;
+        acc[8 * u + 0] = fmaf(cs, lo_f(p0), acc[8 * u + 0]);
+        acc[8 * u + 4] = fmaf(cs, hi_f(p0), acc[8 * u + 4]);
+        acc[8 * u + 1] = fmaf(cs, lo_f(p1), acc[8 * u + 1]);
+        acc[8 * u + 5] = fmaf(cs, hi_f(p1), acc[8 * u + 5]);
+        __builtin_amdgcn_sched_barrier(0);
+        const uint32_t w8 = w >> 8;
+        const uint32_t p2 = w8 & 0x000f000fu, p3 = w8 & 0x00f000f0u;
+        acc[8 * u + 2] = fmaf(cs, lo_f(p2), acc[8 * u + 2]);
+        acc[8 * u + 6] = fmaf(cs, hi_f(p2), acc[8 * u + 6]);
+        acc[8 * u + 3] = fmaf(cs, lo_f(p3), acc[8 * u + 3]);
+        acc[8 * u + 7] = fmaf(cs, hi_f(p3), acc[8 * u + 7]);
+        __builtin_amdgcn_sched_barrier(0);  // one word's codes live at a time
       }
     }
+    // exact: the odd columns' sums are 16 times the true ones, rounding included
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = fmaf(-8.0f, csum, acc[e]);
+    for (int e = 0; e < 16; ++e) acc[e] = fmaf(acc[e], (e & 1) ? 0.0625f : 1.0f, -8.0f * csum);
   }
 }
 
