@@ -232,6 +232,9 @@ typedef struct {
                           INT4), ascending id inside a tier: FFN work order;
                           512 spare entries follow (read, never used)         */
   int64_t work_mask;   /* uint32[cap] row masks in work order                 */
+  int64_t ffn_tasks;   /* the batch-1 FFN kernel's per-workgroup task table:
+                          library-internal format, written by m2c_cache_plan
+                          (empty for layers whose FFN does not use it)       */
   int64_t total_bytes;
 } m2c_plan_layout;
 

@@ -54,18 +54,29 @@ namespace m2c {
 
 namespace {
 
-constexpr int kFT = 512;                 // threads per workgroup
+#ifndef M2C_FFN_THREADS
+#define M2C_FFN_THREADS 256
+#endif
+constexpr int kFT = M2C_FFN_THREADS;     // threads per workgroup
 constexpr int kFWaves = kFT / 64;
 constexpr int kFL = 8;                   // 16-byte data loads per lane and task
 constexpr int kFSW = 512;                // down tasks: output columns per slice
 constexpr int kFLPN = kFSW / 32;         // lanes per neuron row of a slice
 constexpr int kFNPR = kFT / kFLPN;       // neurons per round of a down task
 constexpr int kFMaxItems = kFL * kFNPR;  // most work items of one task (INT4 down)
+// Rounds of kFNPR neurons per down task by tier (INT4, INT8, FP16): one
+// load per lane and round for INT4, two for INT8, four for FP16.
+constexpr int kDnRounds1 = kFL, kDnRounds2 = kFL / 2, kDnRounds3 = kFL / 4;
 constexpr int kFSpin = 1 << 16;          // polls of one h word before giving up
 constexpr float kTwo24 = 16777216.0f;
 static_assert(kFMaxItems <= kFT, "one slot id / h word per thread");
+// The task table in a plan: task count and zero slot (16 bytes), one 32-byte
+// header per workgroup, then kTaskIds slot ids per workgroup from a 256-byte
+// boundary.
+constexpr int kTaskIds = kFL * kFNPR;
+inline int64_t task_ids_offset(int grid) { return (16 + 32 * (int64_t)grid + 255) / 256 * 256; }
 static_assert(kFLPN == 16, "the fold pairs lanes 16 and 32 apart");
-static_assert(kFSW == kFT, "the cross-wave fold gives thread c column c of the slice");
+static_assert(kFSW % kFT == 0, "the cross-wave fold gives each thread whole columns of the slice");
 
 struct FMap {
   int n3, n2, n1;  // work items by tier
@@ -79,6 +90,14 @@ struct FTask {
   int tier;
   int lo, hi;
   int slice;
+};
+
+// A task as the FFN reads it from the table: the task and its tier's pool
+// (byte offset of the pool's first slot, its first slot id, slot count and
+// record stride).
+struct FTaskPool {
+  FTask k;
+  uint32_t tb, tf, tc, ts;
 };
 
 struct FBuf {
@@ -101,9 +120,9 @@ __device__ __forceinline__ FMap make_map(const int32_t* counts, int cap, int d) 
   m.w2 = (m.n2 + U / 2 - 1) / (U / 2);
   m.w3 = (m.n3 + U / 4 - 1) / (U / 4);
   m.n_slices = (d + kFSW - 1) / kFSW;
-  const int u1 = (m.n1 + 8 * kFNPR - 1) / (8 * kFNPR);
-  const int u2 = (m.n2 + 4 * kFNPR - 1) / (4 * kFNPR);
-  const int u3 = (m.n3 + 2 * kFNPR - 1) / (2 * kFNPR);
+  const int u1 = (m.n1 + kDnRounds1 * kFNPR - 1) / (kDnRounds1 * kFNPR);
+  const int u2 = (m.n2 + kDnRounds2 * kFNPR - 1) / (kDnRounds2 * kFNPR);
+  const int u3 = (m.n3 + kDnRounds3 * kFNPR - 1) / (kDnRounds3 * kFNPR);
   int end = 0;
 #pragma unroll
   for (int r = 0; r < 6; ++r) {
@@ -150,7 +169,7 @@ __device__ __forceinline__ FTask decode(const FMap& m, int t) {
     k.hi = base + min(per * (q + 1), n);
   } else {
     k.kind = 2;
-    const int per = (tier == 1 ? 8 : tier == 2 ? 4 : 2) * kFNPR;
+    const int per = (tier == 1 ? kDnRounds1 : tier == 2 ? kDnRounds2 : kDnRounds3) * kFNPR;
     const int run = q / m.n_slices;
     k.slice = q - run * m.n_slices;
     k.lo = base + per * run;
@@ -181,22 +200,20 @@ static_assert(kFNPR * kFL <= kWorkSlotPad && kFWaves * kFL <= kWorkSlotPad,
               "slot id reads stay inside the padded work_slot array");
 
 // Issue every load of task k into b: kFL data loads and kFL scale loads per
-// lane, whatever the kind. The slot ids come from work_slot by scalar
-// loads: wave-uniform reads that do not queue behind the vector loads other
-// workgroups of the CU already have in flight.
+// lane, whatever the kind. idt: the wave's slot ids from the task table (read
+// by scalar loads at the kernel's start), entry q * kFNPR + 4 w + i of the
+// task's row as idt[q][i].
 template <int K>
-__device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict__ work_slot, int d,
-                                      const uint8_t* __restrict__ slots, const SlotMap& map,
+__device__ __forceinline__ void issue(const FTaskPool& kp, const int (&idt)[kFL][4], int d,
+                                      const uint8_t* __restrict__ slots, uint32_t zero,
                                       int n_slots, int tid, FBuf& b) {
   // byte offsets into the slot arena (below 4 GiB: checked at launch), so
   // every address is the arena base plus one 32-bit register; a task's
   // records all live in its tier's pool (one pool for every tier unless the
   // layer has a per-tier arena), and ids past the pools point at the zero slot
-  const uint32_t zero = map.zero;
-  const uint32_t tb = k.tier == 3 ? map.base[3] : k.tier == 2 ? map.base[2] : map.base[1];
-  const int tf = k.tier == 3 ? map.first[3] : k.tier == 2 ? map.first[2] : map.first[1];
-  const uint32_t ts = k.tier == 3 ? map.stride[3] : k.tier == 2 ? map.stride[2] : map.stride[1];
-  const uint32_t tc = k.tier == 3 ? map.count[3] : k.tier == 2 ? map.count[2] : map.count[1];
+  const FTask& k = kp.k;
+  const uint32_t tb = kp.tb, ts = kp.ts, tc = kp.tc;
+  const int tf = (int)kp.tf;
   const int lane = tid & 63;
   const int w = tid >> 6;
   const uint32_t ud = (uint32_t)d;
@@ -208,20 +225,18 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
     const uint32_t dbase = k.tier == 3 ? 4 * ud + 2 * col : k.tier == 2 ? 2 * ud + col
                                                                         : ud + (col >> 1);
     const uint32_t sbase = (k.tier == 1 ? 3 * (ud >> 1) : 3 * ud) + 4 * G + 2 * (col >> 7);
-    // A wave covers the four neurons 4w .. 4w + 3 of every round. Their slot
-    // ids for all kFL rounds are read by scalar loads before the first one
-    // is used (one round trip; a tier with fewer rounds ignores the rest),
-    // then each lane picks its own.
+    // A wave covers the four neurons 4w .. 4w + 3 of every round (table
+    // entries q * kFNPR + 4 w + i; a tier with fewer rounds ignores the
+    // rest), then each lane picks its own.
     const int wu = __builtin_amdgcn_readfirstlane(w);
     const int n = k.hi - k.lo;
     const int sub = lane >> 4;
-    const int32_t* wp = work_slot + k.lo + 4 * wu;  // k.lo < cap: inside the spare tail
     int ids[kFL][4];
 #pragma unroll
     for (int q = 0; q < kFL; ++q)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int v = __builtin_amdgcn_readfirstlane(wp[q * kFNPR + i]);
+        const int v = idt[q][i];
         ids[q][i] = q * kFNPR + 4 * wu + i < n && (uint32_t)(v - tf) < tc ? v : n_slots;
       }
 #pragma unroll
@@ -247,15 +262,13 @@ __device__ __forceinline__ void issue(const FTask& k, const int32_t* __restrict_
     const int ncu = d >> 5;  // 16-byte chunks of each row in a unit
     const uint32_t row = k.tier == 3 ? 2 * ud : k.tier == 2 ? ud : (ud >> 1);
     const uint32_t sbase = k.tier == 1 ? 3 * (ud >> 1) : 3 * ud;
-    // The slot of a unit is the same for the whole wave: the UW slot ids of
-    // the wave's units are read by scalar loads before the first is used.
+    // The slot of a unit is the same for the whole wave: unit wu UW + uw of
+    // the task sits at table entry (uw / 4) kFNPR + 4 wu + uw % 4.
     const int wu = __builtin_amdgcn_readfirstlane(w);
     const int n = k.hi - k.lo;
     int ids[UW];
 #pragma unroll
-    for (int uw = 0; uw < UW; ++uw)  // item < kFWaves * kFL: inside the spare tail
-      ids[uw] = __builtin_amdgcn_readfirstlane(work_slot[k.lo + (wu * UW + uw) / upi]);
-    __builtin_amdgcn_sched_barrier(0);  // every load goes out before the first check
+    for (int uw = 0; uw < UW; ++uw) ids[uw] = idt[uw >> 2][uw & 3];
 #pragma unroll
     for (int uw = 0; uw < UW; ++uw) {
       const int item = (wu * UW + uw) / upi;
@@ -432,7 +445,7 @@ __device__ __forceinline__ void compute_dn_half(const FTask& k, const FBuf& b, c
   if (k.tier == 3) {
     // 4 loads per neuron and round, 8 columns each: this half is loads 2H, 2H+1
 #pragma unroll
-    for (int q = 0; q < kFL / 4; ++q) {
+    for (int q = 0; q < kDnRounds3; ++q) {
       const float c = fmaf(0.0f, h2f((uint16_t)b.s[4 * q]), s_h[q * kFNPR + r]);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
@@ -449,7 +462,7 @@ __device__ __forceinline__ void compute_dn_half(const FTask& k, const FBuf& b, c
     // 2 loads per neuron and round, 16 columns each: this half is load H
     float csum = 0.0f;
 #pragma unroll
-    for (int q = 0; q < kFL / 2; ++q) {
+    for (int q = 0; q < kDnRounds2; ++q) {
       const float c = s_h[q * kFNPR + r] * h2f((uint16_t)b.s[2 * q]);
       csum += c;
       const float cs = c * kTwo24;
@@ -472,7 +485,7 @@ __device__ __forceinline__ void compute_dn_half(const FTask& k, const FBuf& b, c
     // 1 load per neuron and round, 32 columns: this half is words 2H, 2H+1
     float csum = 0.0f;
 #pragma unroll
-    for (int q = 0; q < kFL; ++q) {
+    for (int q = 0; q < kDnRounds1; ++q) {
       const float c = s_h[q * kFNPR + r] * h2f((uint16_t)b.s[q]);
       csum += c;
       const float cs = c * kTwo24;
@@ -554,55 +567,106 @@ inline size_t fused_lds_bytes(int d) {
 
 // at most 80 VGPRs: three workgroups per CU
 template <int K>
-__global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void ffn_fused_kernel(
-    const uint16_t* __restrict__ x, int d, const int32_t* __restrict__ counts,
-    const int32_t* __restrict__ work_slot, const uint8_t* __restrict__ slots, int cap,
-    int n_slots, unsigned long long* __restrict__ gen, unsigned long long* __restrict__ hw,
-    int32_t* __restrict__ status, float* __restrict__ y, int withhold, SlotMap map) {
+#ifndef M2C_FFN_WAVES_PER_EU
+#define M2C_FFN_WAVES_PER_EU 5
+#endif
+__global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(M2C_FFN_WAVES_PER_EU))) void ffn_fused_kernel(
+    const uint16_t* __restrict__ x, const int32_t* __restrict__ tasks,
+    const int32_t* __restrict__ task_ids, unsigned long long* __restrict__ gen,
+    const uint8_t* __restrict__ slots, int d, int n_slots, const int32_t* __restrict__ work_slot,
+    unsigned long long* __restrict__ hw, int32_t* __restrict__ status, float* __restrict__ y,
+    int withhold) {
+  // (argument order: what the first round trip needs comes first, inside the
+  // preloaded kernel arguments)
   extern __shared__ uint4 xlds[];  // fused_lds_bytes(d)
   __shared__ FShared sh;
   const int tid = threadIdx.x;
   const int t = blockIdx.x;
-  const FMap m = make_map<K>(counts, cap, d);
-  const FTask kc = decode<K>(m, t);
+  // Everything the data loads need sits at addresses that depend on the
+  // workgroup id alone (task count, this task's header and its wave's slot
+  // ids, the call counter): one round trip of scalar loads before they go out.
+  const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int32_t* wp = task_ids + (int64_t)t * kTaskIds + 4 * wu;
+  int idt[kFL][4];
+#pragma unroll
+  for (int q = 0; q < kFL; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) idt[q][i] = __builtin_amdgcn_readfirstlane(wp[q * kFNPR + i]);
+  const int n_tasks = tasks[0];
+  const uint32_t zero = (uint32_t)tasks[1];
+  const int4 hd = reinterpret_cast<const int4*>(tasks + 4)[2 * t];
+  const int4 hp = reinterpret_cast<const int4*>(tasks + 4)[2 * t + 1];
+  const unsigned long long e0 = gen[t];  // the call count: only this workgroup touches gen[t]
+  // (every load above goes out before the first is used; the call count is
+  // needed only at the end, and this keeps its load in the first round trip
+  // instead of one of its own after the task header)
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::"s"((uint32_t)e0), "s"((uint32_t)(e0 >> 32)));
+  FTaskPool kp;
+  FTask& kc = kp.k;
+  kc.kind = t < n_tasks ? (hd.x & 0xff) : 0;
+  kc.tier = (hd.x >> 8) & 0xff;
+  kc.lo = hd.y;
+  kc.hi = hd.y + hd.z;
+  kc.slice = hd.w;
+  kp.tb = (uint32_t)hp.x;
+  kp.tf = (uint32_t)hp.y;
+  kp.tc = (uint32_t)hp.z;
+  kp.ts = (uint32_t)hp.w;
   if (kc.kind == 0) {
-    if (tid == 0) atomicAdd(gen + t, 1ull);  // keep this workgroup's count in step
+    if (tid == 0) gen[t] = e0 + 1;  // keep this workgroup's count in step
     return;
   }
   const int n_items = kc.hi - kc.lo;
   uint4* xs = xlds;
   float* nx16 = reinterpret_cast<float*>(xlds + (d >> 3));
   float* nx32 = nx16 + (d >> 4);
-  // the call count (only this workgroup touches gen[t]) and, for the h
-  // publish, this thread's item slot
-  const unsigned long long e0 = gen[t];
+  // for the h publish: this thread's item slot (needed only at the end)
   const bool okslot = tid < n_items;
   const int sl = work_slot[okslot ? kc.lo + tid : 0];
   FBuf cur;
-  uint4 xv0 = make_uint4(0, 0, 0, 0), xv1 = xv0;
+  // h tasks stage x: kXC chunks of 16 values per thread (chunk tid + k kFT)
+  constexpr int kXC = 8192 / 16 / kFT;
+  static_assert(kXC * kFT * 16 == 8192, "x staging covers d = 8192");
+  uint4 xv[kXC][2];
+  const int nc8 = d >> 3;
+  const uint4* x4 = reinterpret_cast<const uint4*>(x);
   if (kc.kind == 1) {
-    // x in registers, 16 values per thread; the data loads wait only for
-    // the scalar slot loads inside issue, and x arrives while they fly
-    static_assert(2 * kFT * 8 >= 8192, "x staging covers d = 8192");
-    const int nc8 = d >> 3;
-    const uint4* x4 = reinterpret_cast<const uint4*>(x);
-    xv0 = x4[min(2 * tid, nc8 - 1)];
-    xv1 = x4[min(2 * tid + 1, nc8 - 1)];
-    issue<K>(kc, work_slot, d, slots, map, n_slots, tid, cur);
+    // x in registers. With one chunk per thread it is loaded before the data
+    // loads (which wait only for the scalar slot loads inside issue) and
+    // arrives while they fly; more chunks are loaded after them (registers).
+#pragma unroll
+    for (int k = 0; k < kXC; ++k) {
+      if (kXC > 1) break;
+      const int c = tid + k * kFT;
+      xv[k][0] = x4[min(2 * c, nc8 - 1)];
+      xv[k][1] = x4[min(2 * c + 1, nc8 - 1)];
+    }
+    issue<K>(kp, idt, d, slots, zero, n_slots, tid, cur);
+#pragma unroll
+    for (int k = 0; k < kXC; ++k) {
+      if (kXC == 1) break;
+      const int c = tid + k * kFT;
+      xv[k][0] = x4[min(2 * c, nc8 - 1)];
+      xv[k][1] = x4[min(2 * c + 1, nc8 - 1)];
+    }
   } else {
-    issue<K>(kc, work_slot, d, slots, map, n_slots, tid, cur);
+    issue<K>(kp, idt, d, slots, zero, n_slots, tid, cur);
   }
   const uint32_t epoch = (uint32_t)e0 + 1u;
   if (kc.kind == 1) {
     // x into LDS and the chunk sums of this thread's 16 values, while the
     // task's loads are in flight
-    {
-      const bool own = 2 * tid < (d >> 3);
+#pragma unroll
+    for (int k = 0; k < kXC; ++k) {
+      const int c = tid + k * kFT;  // chunk of 16 x values
+      const bool own = 2 * c < (d >> 3);
       if (own) {
-        xs[2 * tid] = xv0;
-        xs[2 * tid + 1] = xv1;
+        xs[2 * c] = xv[k][0];
+        xs[2 * c + 1] = xv[k][1];
       }
-      const uint32_t ws[8] = {xv0.x, xv0.y, xv0.z, xv0.w, xv1.x, xv1.y, xv1.z, xv1.w};
+      const uint32_t ws[8] = {xv[k][0].x, xv[k][0].y, xv[k][0].z, xv[k][0].w,
+                              xv[k][1].x, xv[k][1].y, xv[k][1].z, xv[k][1].w};
       float sum = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) sum += lo_f(ws[e]) + hi_f(ws[e]);
@@ -610,8 +674,8 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
       // -8 * (sum of 32) = (-128 * sum of this 16 - 128 * sum of the neighbour's 16) / 16
       const float other = __int_as_float(
           __builtin_amdgcn_mov_dpp(__float_as_int(n16), 0xB1, 0xF, 0xF, false));
-      if (own) nx16[tid] = n16;
-      if (own && (tid & 1) == 0) nx32[tid >> 1] = (n16 + other) * 0.0625f;
+      if (own) nx16[c] = n16;
+      if (own && (c & 1) == 0) nx32[c >> 1] = (n16 + other) * 0.0625f;
     }
     __syncthreads();
     compute_h<K>(kc, cur, d, xs, nx16, nx32, tid, sh.ab);
@@ -670,12 +734,14 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
       *reinterpret_cast<float4*>(row + 16) = make_float4(o[0], o[1], o[2], o[3]);
     }
     __syncthreads();
-    {
-      const float* src = part + (tid >> 5) * kFRow + (tid & 31);
+#pragma unroll
+    for (int k = 0; k < kFSW / kFT; ++k) {
+      const int c = tid + k * kFT;  // column of the slice
+      const float* src = part + (c >> 5) * kFRow + (c & 31);
       float v = 0.0f;
 #pragma unroll
       for (int w = 0; w < kFWaves; ++w) v += src[w * kFBlock];
-      const int col = kc.slice * kFSW + tid;
+      const int col = kc.slice * kFSW + c;
       if (col < d) atomicAdd(y + col, v);
     }
   }
@@ -683,13 +749,72 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(6))) void f
 }
 
 template <int K>
-hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* counts,
+hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* tasks,
                         const int32_t* work_slot, float* y, hipStream_t stream) {
   const int d = L->desc.d_model;
   const size_t lds = fused_lds_bytes(d);
-  hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, d, counts,
-                     work_slot, L->slots, L->cap, L->desc.cache_slots + L->S, L->st.ffn_gen,
-                     L->st.ffn_hw, L->st.status, y, L->ffn_withhold, L->map);
+  const int32_t* task_ids = tasks + task_ids_offset(L->ffn_grid) / 4;
+  hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, tasks,
+                     task_ids, L->st.ffn_gen, L->slots, d, L->desc.cache_slots + L->S, work_slot,
+                     L->st.ffn_hw, L->st.status, y, L->ffn_withhold);
+  return hipGetLastError();
+}
+
+// The task table, one wave per task: the 32-byte header {kind | tier << 8,
+// first work item, items, slice, then the tier pool's byte offset, first slot
+// id, slot count, record stride} and the slot ids in the order the FFN's
+// waves read them (a down task's items in work order; an h task's units at
+// entry (uw / 4) kFNPR + 4 w + uw % 4 for unit w UW + uw). The table starts
+// with the task count and the zero slot's byte offset.
+template <int K>
+__global__ __launch_bounds__(256) void ffn_tasks_kernel(const int32_t* __restrict__ counts,
+                                                        const int32_t* __restrict__ work_slot,
+                                                        int cap, int d, int grid, SlotMap map,
+                                                        int32_t* __restrict__ tasks,
+                                                        int32_t* __restrict__ task_ids) {
+  constexpr int UW = kFL / K;
+  const FMap m = make_map<K>(counts, cap, d);
+  const int n_tasks = m.e[5] < grid ? m.e[5] : grid;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    tasks[0] = n_tasks;
+    tasks[1] = (int32_t)map.zero;
+  }
+  const int lane = threadIdx.x & 63;
+  const int nw = (int)(gridDim.x * blockDim.x) >> 6;
+  for (int t = (int)(blockIdx.x * blockDim.x + threadIdx.x) >> 6; t < n_tasks; t += nw) {
+    const FTask k = decode<K>(m, t);
+    const int n = k.hi - k.lo;
+    if (lane == 0) {
+      const int tr = k.tier;
+      int4* h = reinterpret_cast<int4*>(tasks + 4) + 2 * t;
+      h[0] = make_int4(k.kind | (tr << 8), k.lo, n, k.slice);
+      h[1] = make_int4((int)map.base[tr], map.first[tr], map.count[tr], (int)map.stride[tr]);
+    }
+    int32_t* out = task_ids + (int64_t)t * kTaskIds;
+    if (k.kind == 2) {
+      for (int e = lane; e < n; e += 64) out[e] = work_slot[k.lo + e];
+    } else if (k.kind == 1) {
+      const int upi = k.tier == 3 ? 4 : k.tier == 2 ? 2 : 1;
+      const int item = lane / upi;  // unit lane of the task
+      if (lane < kFWaves * UW && item < n) {
+        const int w = lane / UW, uw = lane % UW;
+        out[(uw >> 2) * kFNPR + 4 * w + (uw & 3)] = work_slot[k.lo + item];
+      }
+    }
+  }
+}
+
+template <int K>
+hipError_t launch_tasks(m2c_layer* L, uint8_t* plan, hipStream_t stream) {
+  const m2c_plan_layout& lay = L->layout;
+  int32_t* tasks = reinterpret_cast<int32_t*>(plan + lay.ffn_tasks);
+  int blocks = (L->ffn_grid + 3) / 4;
+  blocks = blocks < 1 ? 1 : blocks > 256 ? 256 : blocks;
+  hipLaunchKernelGGL(ffn_tasks_kernel<K>, dim3(blocks), dim3(256), 0, stream,
+                     reinterpret_cast<const int32_t*>(plan + lay.counts),
+                     reinterpret_cast<const int32_t*>(plan + lay.work_slot), L->cap,
+                     L->desc.d_model, L->ffn_grid, L->map, tasks,
+                     tasks + task_ids_offset(L->ffn_grid) / 4);
   return hipGetLastError();
 }
 
@@ -711,20 +836,38 @@ int ffn_fused_grid(int d, int cap, int num_cus) {
   // per slice at most cap / (FP16 neurons per run) + 1 per tier
   const int U = kFWaves * (kFL / loads_per_unit(d));
   const int64_t most = (int64_t)cap / (U / 4) + 3 +
-                       (int64_t)((d + kFSW - 1) / kFSW) * (cap / (2 * kFNPR) + 3);
+                       (int64_t)((d + kFSW - 1) / kFSW) * (cap / (kDnRounds3 * kFNPR) + 3);
   return (int)most;
 }
 
 hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
                             hipStream_t stream) {
   if (L->cap <= 0 || L->ffn_grid <= 0) return hipSuccess;
-  const int32_t* counts = reinterpret_cast<const int32_t*>(plan + L->layout.counts);
+  const int32_t* tasks = reinterpret_cast<const int32_t*>(plan + L->layout.ffn_tasks);
   const int32_t* work_slot = reinterpret_cast<const int32_t*>(plan + L->layout.work_slot);
   switch (loads_per_unit(L->desc.d_model)) {
-    case 1: return launch_fused<1>(L, x, counts, work_slot, y, stream);
-    case 2: return launch_fused<2>(L, x, counts, work_slot, y, stream);
-    case 4: return launch_fused<4>(L, x, counts, work_slot, y, stream);
-    default: return launch_fused<8>(L, x, counts, work_slot, y, stream);
+    case 1: return launch_fused<1>(L, x, tasks, work_slot, y, stream);
+    case 2: return launch_fused<2>(L, x, tasks, work_slot, y, stream);
+    case 4: return launch_fused<4>(L, x, tasks, work_slot, y, stream);
+    default: return launch_fused<8>(L, x, tasks, work_slot, y, stream);
+  }
+}
+
+bool ffn_tasks_used(const m2c_layer* L) {
+  return !(L->desc.flags & M2C_FLAG_DETERMINISTIC_FFN) && ffn_fused_supported(L) && L->cap > 0;
+}
+
+int64_t ffn_task_table_bytes(int grid) {
+  return task_ids_offset(grid) + (int64_t)grid * kTaskIds * 4;
+}
+
+hipError_t launch_ffn_tasks(m2c_layer* L, uint8_t* plan, hipStream_t stream) {
+  if (!ffn_tasks_used(L) || L->ffn_grid <= 0) return hipSuccess;
+  switch (loads_per_unit(L->desc.d_model)) {
+    case 1: return launch_tasks<1>(L, plan, stream);
+    case 2: return launch_tasks<2>(L, plan, stream);
+    case 4: return launch_tasks<4>(L, plan, stream);
+    default: return launch_tasks<8>(L, plan, stream);
   }
 }
 

@@ -806,7 +806,8 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
     else
       hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, tier_map, batch,
                          L->desc.d_ff, L->desc.cache_slots, L->cap, step, dom, L->st, P);
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? launch_ffn_tasks(L, plan, stream) : e;
   }
   // per-tier arena (d_ff <= 32768, checked at create): the three pools'
   // plans side by side in one launch, into the layer's pool plans, then the
@@ -815,7 +816,7 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
   PoolJobs jobs;
   for (int q = 0; q < 3; ++q) {
     const int t = 3 - q;
-    const PlanPtrs Pq = plan_ptrs(L, L->pool_plan + (int64_t)q * L->info.plan_bytes);
+    const PlanPtrs Pq = plan_ptrs(L, L->pool_plan + (int64_t)q * L->plan_core_bytes);
     jobs.st[q] = pool_state(L, t);
     jobs.P[q] = Pq;
     jobs.C[q] = L->pool_C[t];
@@ -830,7 +831,8 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
   blocks = blocks < 1 ? 1 : blocks > 64 ? 64 : blocks;
   hipLaunchKernelGGL(plan_merge_kernel, dim3(blocks), dim3(256), 0, stream, pp, P, L->map,
                      L->plan_abort);
-  return hipGetLastError();
+  e = hipGetLastError();
+  return e == hipSuccess ? launch_ffn_tasks(L, plan, stream) : e;
 }
 
 hipError_t launch_reset(m2c_layer* L, hipStream_t stream) {

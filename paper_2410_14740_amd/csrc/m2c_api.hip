@@ -192,6 +192,11 @@ void fill_info_layout(m2c_layer* L) {
   P.evicted_ids = take(4 * c);
   P.work_slot = take(4 * (c + m2c::kWorkSlotPad));
   P.work_mask = take(4 * c);
+  L->plan_core_bytes = off;
+  P.ffn_tasks = take(m2c::ffn_tasks_used(L)
+                         ? m2c::ffn_task_table_bytes(m2c::ffn_fused_grid(
+                               (int)L->desc.d_model, (int)c, L->num_cus))
+                         : 0);
   P.total_bytes = off;
   I.plan_bytes = off;
 }
@@ -269,7 +274,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_status, 4},
       {&p_gen, (int64_t)m2c::ffn_fused_grid((int)d, (int)cap, L->num_cus) * 8},
       {&p_hw, cap * 8},
-      {&p_pool_plan, L->pools ? 3 * L->info.plan_bytes : 0},
+      {&p_pool_plan, L->pools ? 3 * L->plan_core_bytes : 0},
       {&p_abort, 4},
   };
   int64_t total = 0;

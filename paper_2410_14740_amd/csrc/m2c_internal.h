@@ -102,7 +102,8 @@ struct m2c_layer {
   int pool_rf[4] = {0, 0, 0, 0};  // first resident table index of the pool
   m2c::SlotMap map;               // slot id -> byte offset, by tier
   int64_t arena_bytes = 0;        // pools + zero slot
-  uint8_t* pool_plan = nullptr;   // [3][plan_bytes] the pools' own plans
+  uint8_t* pool_plan = nullptr;   // [3][plan_core_bytes] the pools' own plans
+  int64_t plan_core_bytes = 0;    // a plan without the one-launch FFN's task table
   int32_t* plan_abort = nullptr;  // [1] set when a step's required set overflowed
 };
 
@@ -156,6 +157,12 @@ hipError_t launch_ffn_split(m2c_layer* L, const uint16_t* x, const uint8_t* plan
                             hipStream_t stream);
 bool ffn_fused_supported(const m2c_layer* L);
 int ffn_fused_grid(int d_model, int cap, int num_cus);  // workgroups (and gen counters) of the one-launch FFN
+// The one-launch FFN's task table in a plan: whether the layer's plans carry
+// one (batch-1 FFN calls use that kernel), its bytes for a grid, and the
+// kernel that writes it from the plan's counts and work order.
+bool ffn_tasks_used(const m2c_layer* L);
+int64_t ffn_task_table_bytes(int grid);
+hipError_t launch_ffn_tasks(m2c_layer* L, uint8_t* plan, hipStream_t stream);
 hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,
                             hipStream_t stream);
 

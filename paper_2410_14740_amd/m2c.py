@@ -59,7 +59,7 @@ class LayerInfo(ctypes.Structure):
 
 PLAN_FIELDS = ("counts", "req_ids", "req_tier", "req_hit", "req_slot", "req_mask", "fill_ids",
                "fill_tier", "fill_slot", "fill_from", "evicted_ids", "work_slot", "work_mask",
-               "total_bytes")
+               "ffn_tasks", "total_bytes")
 
 
 class PlanLayout(ctypes.Structure):

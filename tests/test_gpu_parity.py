@@ -545,7 +545,10 @@ def test_ffn_modes_accumulate_and_determinism(d, d_ff):
     """Both FFN paths add into y; the deterministic path repeats bit for bit
     and the fused path agrees with it to fp32 rounding. (Each of the fused
     path's per-workgroup atomic adds rounds at the magnitude of what y already
-    holds, so the cross-mode check starts from y = 0.)"""
+    holds, so the cross-mode check starts from y = 0; a column's sum is one
+    fp32 partial per down task that covers it, and their number follows the
+    task geometry, so the cross-mode bound is a quarter of the oracle
+    tolerance rather than a fixed multiple of one rounding.)"""
     ld = W.make_layer(61, 0, d, d_ff, 64, 1)
     k = d_ff // 5
     n16, n8 = _counts(k, (1, 10), (2, 5))
@@ -578,7 +581,7 @@ def test_ffn_modes_accumulate_and_determinism(d, d_ff):
         assert r8_errors(acc, y_ref).max() <= FFN_TOL  # accumulated into y
         outs[flags] = ys[0]
         L.close()
-    assert r8_errors(outs[0], outs[m2c.FLAG_DETERMINISTIC_FFN]).max() <= 1e-4
+    assert r8_errors(outs[0], outs[m2c.FLAG_DETERMINISTIC_FFN]).max() <= FFN_TOL / 4
 
 
 def test_plan_overflow_is_reported():
