@@ -92,19 +92,6 @@ struct FTask {
   int slice;
 };
 
-// A task as the FFN reads it from the table: the task and its tier's pool
-// (byte offset of the pool's first slot, its first slot id, slot count and
-// record stride).
-struct FTaskPool {
-  FTask k;
-  uint32_t tb, tf, tc, ts;
-};
-
-struct FBuf {
-  uint4 v[kFL];
-  uint32_t s[kFL];
-};
-
 // K: 16-byte loads per lane and unit (a unit is d bytes of a neuron's gate and
 // up rows); a wave takes kFL / K units of an h task.
 // Launch order of the six task regions: (kind, tier) per region.
@@ -199,102 +186,6 @@ __device__ __forceinline__ float hi_f(uint32_t p) {
 static_assert(kFNPR * kFL <= kWorkSlotPad && kFWaves * kFL <= kWorkSlotPad,
               "slot id reads stay inside the padded work_slot array");
 
-// Issue every load of task k into b: kFL data loads and kFL scale loads per
-// lane, whatever the kind. idt: the wave's slot ids from the task table (read
-// by scalar loads at the kernel's start), entry q * kFNPR + 4 w + i of the
-// task's row as idt[q][i].
-template <int K>
-__device__ __forceinline__ void issue(const FTaskPool& kp, const int (&idt)[kFL][4], int d,
-                                      const uint8_t* __restrict__ slots, uint32_t zero,
-                                      int n_slots, int tid, FBuf& b) {
-  // byte offsets into the slot arena (below 4 GiB: checked at launch), so
-  // every address is the arena base plus one 32-bit register; a task's
-  // records all live in its tier's pool (one pool for every tier unless the
-  // layer has a per-tier arena), and ids past the pools point at the zero slot
-  const FTask& k = kp.k;
-  const uint32_t tb = kp.tb, ts = kp.ts, tc = kp.tc;
-  const int tf = (int)kp.tf;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const uint32_t ud = (uint32_t)d;
-  const uint32_t G = ud >> 7;
-  if (k.kind == 2) {
-    const uint32_t col = (uint32_t)(k.slice * kFSW + 32 * (tid % kFLPN));
-    const bool colok = col < ud;
-    const int lnv = k.tier == 3 ? 2 : k.tier == 2 ? 1 : 0;  // log2 loads per neuron and round
-    const uint32_t dbase = k.tier == 3 ? 4 * ud + 2 * col : k.tier == 2 ? 2 * ud + col
-                                                                        : ud + (col >> 1);
-    const uint32_t sbase = (k.tier == 1 ? 3 * (ud >> 1) : 3 * ud) + 4 * G + 2 * (col >> 7);
-    // A wave covers the four neurons 4w .. 4w + 3 of every round (table
-    // entries q * kFNPR + 4 w + i; a tier with fewer rounds ignores the
-    // rest), then each lane picks its own.
-    const int wu = __builtin_amdgcn_readfirstlane(w);
-    const int n = k.hi - k.lo;
-    const int sub = lane >> 4;
-    int ids[kFL][4];
-#pragma unroll
-    for (int q = 0; q < kFL; ++q)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int v = idt[q][i];
-        ids[q][i] = q * kFNPR + 4 * wu + i < n && (uint32_t)(v - tf) < tc ? v : n_slots;
-      }
-#pragma unroll
-    for (int j = 0; j < kFL; ++j) {
-      const int e = j & ((1 << lnv) - 1);
-      int sv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)  // round j >> lnv
-        sv[i] = k.tier == 3 ? ids[j >> 2][i] : k.tier == 2 ? ids[j >> 1][i] : ids[j][i];
-      const int slv = sub == 0 ? sv[0] : sub == 1 ? sv[1] : sub == 2 ? sv[2] : sv[3];
-      const uint32_t rec = slv >= n_slots ? zero : tb + (uint32_t)(slv - tf) * ts;
-      // the scale of an FP16 record (it has none) is read from the zero slot,
-      // never from the data's own address: every load stays independent
-      const uint32_t dp = colok ? rec + dbase + 16 * e : zero;
-      const uint32_t sp = colok && k.tier != 3 ? rec + sbase : zero;
-      b.v[j] = ld16(slots + dp);
-      b.s[j] = ld2(slots + sp);
-    }
-  } else {
-    // h task (or nothing: kind 0 reads the zero slot with the same pattern)
-    constexpr int UW = kFL / K;
-    const int upi = k.tier == 3 ? 4 : k.tier == 2 ? 2 : 1;  // units per neuron
-    const int ncu = d >> 5;  // 16-byte chunks of each row in a unit
-    const uint32_t row = k.tier == 3 ? 2 * ud : k.tier == 2 ? ud : (ud >> 1);
-    const uint32_t sbase = k.tier == 1 ? 3 * (ud >> 1) : 3 * ud;
-    // The slot of a unit is the same for the whole wave: unit wu UW + uw of
-    // the task sits at table entry (uw / 4) kFNPR + 4 wu + uw % 4.
-    const int wu = __builtin_amdgcn_readfirstlane(w);
-    const int n = k.hi - k.lo;
-    int ids[UW];
-#pragma unroll
-    for (int uw = 0; uw < UW; ++uw) ids[uw] = idt[uw >> 2][uw & 3];
-#pragma unroll
-    for (int uw = 0; uw < UW; ++uw) {
-      const int item = (wu * UW + uw) / upi;
-      const int v = ids[uw];
-      // the zero slot past the task (and for kind 0)
-      ids[uw] = k.kind == 1 && item < n && (uint32_t)(v - tf) < tc ? v : n_slots;
-    }
-#pragma unroll
-    for (int j = 0; j < kFL; ++j) {
-      const int part = (w * UW + j / K) % upi;
-      const int slu = ids[j / K];
-      const uint32_t rec = slu >= n_slots ? zero : tb + (uint32_t)(slu - tf) * ts;
-      int q = lane + 64 * (j % K);
-      const bool in = q < 2 * ncu;
-      q = in ? q : 2 * ncu - 1;
-      const bool up = q >= ncu;
-      const uint32_t c = (uint32_t)(part * ncu + (up ? q - ncu : q));
-      const uint32_t g = k.tier == 2 ? (c >> 3) : (c >> 2);
-      const uint32_t dp = in ? rec + (up ? row : 0) + 16 * c : zero;
-      const uint32_t sp = in && k.tier != 3 ? rec + sbase + 2 * ((up ? G : 0) + g) : zero;
-      b.v[j] = ld16(slots + dp);
-      b.s[j] = ld2(slots + sp);
-    }
-  }
-}
-
 // Unscaled dot products of one 16-byte chunk of INT8 (16 codes) or INT4 (32
 // codes) weights with their x elements (x0, x1 / xq: the chunk's x as it sits
 // in LDS), offset codes as fp16 denormals: sum of (q + 128) x or (q + 8) x,
@@ -347,175 +238,6 @@ __device__ __forceinline__ float chunk_int4(const uint4 v, const uint4 (&xq)[4])
   return fmaf(tb, 0.0625f, ta);
 }
 
-// Gate / up partial dot products of an h task; per unit (a, b) into s_ab.
-template <int K>
-__device__ __forceinline__ void compute_h(const FTask& k, const FBuf& b, int d,
-                                          const uint4* xs, const float* nx16, const float* nx32,
-                                          int tid, float2* s_ab) {
-  constexpr int UW = kFL / K;
-  const int lane = tid & 63;
-  const int w = tid >> 6;
-  const int upi = k.tier == 3 ? 4 : k.tier == 2 ? 2 : 1;
-  const int ncu = d >> 5;
-  float a[UW], bb[UW];
-#pragma unroll
-  for (int uw = 0; uw < UW; ++uw) a[uw] = bb[uw] = 0.0f;
-  if (K >= 2 && d == 1024 * K) {
-    // A unit's rows fill its K loads exactly: load jj < K / 2 of a lane is
-    // the gate chunk c and load jj + K / 2 the up chunk c, so the x of c is
-    // read from LDS once for both.
-#pragma unroll
-    for (int uw = 0; uw < UW; ++uw) {
-      const int part = (w * UW + uw) % upi;
-#pragma unroll
-      for (int jj = 0; jj < K / 2; ++jj) {
-        const int jg = uw * K + jj, ju = jg + K / 2;
-        const int c = part * ncu + lane + 64 * jj;
-        float pg, pu;
-        if (k.tier == 3) {
-          // + 0 * (scale read from the zero slot): keeps that load unconditional
-          const uint4 xc = xs[c];
-          pg = fmaf(0.0f, h2f((uint16_t)b.s[jg]), dot8_f16(b.v[jg], xc, 0.0f));
-          pu = fmaf(0.0f, h2f((uint16_t)b.s[ju]), dot8_f16(b.v[ju], xc, 0.0f));
-        } else if (k.tier == 2) {
-          const uint4 x0 = xs[2 * c], x1 = xs[2 * c + 1];
-          const float o = nx16[c];
-          pg = h2f((uint16_t)b.s[jg]) * fmaf(chunk_int8(b.v[jg], x0, x1), kTwo24, o);
-          pu = h2f((uint16_t)b.s[ju]) * fmaf(chunk_int8(b.v[ju], x0, x1), kTwo24, o);
-        } else {
-          uint4 xq[4];
-#pragma unroll
-          for (int u4 = 0; u4 < 4; ++u4) xq[u4] = xs[4 * c + u4];
-          const float o = nx32[c];
-          pg = h2f((uint16_t)b.s[jg]) * fmaf(chunk_int4(b.v[jg], xq), kTwo24, o);
-          pu = h2f((uint16_t)b.s[ju]) * fmaf(chunk_int4(b.v[ju], xq), kTwo24, o);
-        }
-        a[uw] += pg;
-        bb[uw] += pu;
-        // one chunk at a time: keeps the x reads of later chunks from being
-        // hoisted into registers all at once
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < kFL; ++j) {
-      const int uw = j / K;
-      const int u = w * UW + uw;
-      const int part = u % upi;
-      int q = lane + 64 * (j % K);
-      q = q < 2 * ncu ? q : 2 * ncu - 1;
-      const bool up = q >= ncu;
-      const int c = part * ncu + (up ? q - ncu : q);
-      float p;
-      if (k.tier == 3) {
-        p = fmaf(0.0f, h2f((uint16_t)b.s[j]), dot8_f16(b.v[j], xs[c], 0.0f));
-      } else if (k.tier == 2) {
-        p = h2f((uint16_t)b.s[j]) * fmaf(chunk_int8(b.v[j], xs[2 * c], xs[2 * c + 1]), kTwo24,
-                                         nx16[c]);
-      } else {
-        uint4 xq[4];
-#pragma unroll
-        for (int u4 = 0; u4 < 4; ++u4) xq[u4] = xs[4 * c + u4];
-        p = h2f((uint16_t)b.s[j]) * fmaf(chunk_int4(b.v[j], xq), kTwo24, nx32[c]);
-      }
-      // lanes past the unit read the zero slot: data 0 (FP16) or scale 0
-      a[uw] += up ? 0.0f : p;
-      bb[uw] += up ? p : 0.0f;
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  }
-#pragma unroll
-  for (int uw = 0; uw < UW; ++uw) {
-    const float sa = wave_sum(a[uw]), sbv = wave_sum(bb[uw]);
-    if (lane == 0) s_ab[w * UW + uw] = make_float2(sa, sbv);
-  }
-}
-
-// Down projection of a down task: columns 16 * HALF .. 16 * HALF + 15 of the
-// lane's 32, for every neuron of the task (the two halves share the loaded
-// data and keep only 16 accumulators live). csum: sum of the lane's
-// coefficients, for the offset of INT8 / INT4 codes.
-template <int HALF>
-__device__ __forceinline__ void compute_dn_half(const FTask& k, const FBuf& b, const float* s_h,
-                                                int tid, float (&acc)[16]) {
-  const int r = tid / kFLPN;
-#pragma unroll
-  for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-  if (k.tier == 3) {
-    // 4 loads per neuron and round, 8 columns each: this half is loads 2H, 2H+1
-#pragma unroll
-    for (int q = 0; q < kDnRounds3; ++q) {
-      const float c = fmaf(0.0f, h2f((uint16_t)b.s[4 * q]), s_h[q * kFNPR + r]);
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const uint4 v = b.v[4 * q + 2 * HALF + e];
-        const uint32_t ws[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          acc[8 * e + 2 * u] = fmaf(c, lo_f(ws[u]), acc[8 * e + 2 * u]);
-          acc[8 * e + 2 * u + 1] = fmaf(c, hi_f(ws[u]), acc[8 * e + 2 * u + 1]);
-        }
-      }
-    }
-  } else if (k.tier == 2) {
-    // 2 loads per neuron and round, 16 columns each: this half is load H
-    float csum = 0.0f;
-#pragma unroll
-    for (int q = 0; q < kDnRounds2; ++q) {
-      const float c = s_h[q * kFNPR + r] * h2f((uint16_t)b.s[2 * q]);
-      csum += c;
-      const float cs = c * kTwo24;
-      const uint4 v = b.v[2 * q + HALF];
-      const uint32_t ws[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t ob = ws[u] ^ 0x80808080u;
-        const uint32_t l = __builtin_amdgcn_perm(0u, ob, 0x0c010c00u);
-        const uint32_t h = __builtin_amdgcn_perm(0u, ob, 0x0c030c02u);
-        acc[4 * u] = fmaf(cs, lo_f(l), acc[4 * u]);
-        acc[4 * u + 1] = fmaf(cs, hi_f(l), acc[4 * u + 1]);
-        acc[4 * u + 2] = fmaf(cs, lo_f(h), acc[4 * u + 2]);
-        acc[4 * u + 3] = fmaf(cs, hi_f(h), acc[4 * u + 3]);
-      }
-    }
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = fmaf(-128.0f, csum, acc[e]);
-  } else {
-    // 1 load per neuron and round, 32 columns: this half is words 2H, 2H+1
-    float csum = 0.0f;
-#pragma unroll
-    for (int q = 0; q < kDnRounds1; ++q) {
-      const float c = s_h[q * kFNPR + r] * h2f((uint16_t)b.s[q]);
-      csum += c;
-      const float cs = c * kTwo24;
-      const uint32_t ws[2] = {HALF ? b.v[q].z : b.v[q].x, HALF ? b.v[q].w : b.v[q].y};
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        // column 8 u + e is nibble e; odd columns sum 16 times their value.
-        // Nibbles 0..3 first, then 4..7 (after the barrier): fewer codes live.
-        const uint32_t w = ws[u] ^ 0x88888888u;
-        const uint32_t p0 = w & 0x000f000fu, p1 = w & 0x00f000f0u;
-        acc[8 * u + 0] = fmaf(cs, lo_f(p0), acc[8 * u + 0]);
-        acc[8 * u + 4] = fmaf(cs, hi_f(p0), acc[8 * u + 4]);
-        acc[8 * u + 1] = fmaf(cs, lo_f(p1), acc[8 * u + 1]);
-        acc[8 * u + 5] = fmaf(cs, hi_f(p1), acc[8 * u + 5]);
-        __builtin_amdgcn_sched_barrier(0);
-        const uint32_t w8 = w >> 8;
-        const uint32_t p2 = w8 & 0x000f000fu, p3 = w8 & 0x00f000f0u;
-        acc[8 * u + 2] = fmaf(cs, lo_f(p2), acc[8 * u + 2]);
-        acc[8 * u + 6] = fmaf(cs, hi_f(p2), acc[8 * u + 6]);
-        acc[8 * u + 3] = fmaf(cs, lo_f(p3), acc[8 * u + 3]);
-        acc[8 * u + 7] = fmaf(cs, hi_f(p3), acc[8 * u + 7]);
-        __builtin_amdgcn_sched_barrier(0);  // one word's codes live at a time
-      }
-    }
-    // exact: the odd columns' sums are 16 times the true ones, rounding included
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = fmaf(acc[e], (e & 1) ? 0.0625f : 1.0f, -8.0f * csum);
-  }
-}
-
 __device__ __forceinline__ unsigned long long load_word(const unsigned long long* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -565,7 +287,401 @@ inline size_t fused_lds_bytes(int d) {
   return xb > kFFoldBytes ? xb : kFFoldBytes;
 }
 
-// at most 80 VGPRs: three workgroups per CU
+// What a task needs besides its slot ids: the slot arena and its zero slot,
+// the pool of the task's tier (byte offset of its first slot, first slot id,
+// slot count, record stride) and the task's work items.
+struct FTaskArgs {
+  const uint8_t* slots;
+  uint32_t zero;
+  uint32_t tb, tf, tc, ts;
+  int d;
+  int lo, n;  // first work item, items
+  int slice;  // down task: column slice
+};
+
+// Byte offset of the record in slot v when `ok` and v lies in the task's
+// pool, else of the zero slot (every record byte there is 0). Offsets stay
+// below 4 GiB (checked at launch), so every address is the arena base plus
+// one 32-bit register.
+__device__ __forceinline__ uint32_t rec_of(const FTaskArgs& a, int v, bool ok) {
+  const uint32_t i = (uint32_t)(v - (int)a.tf);
+  return ok && i < a.tc ? a.tb + i * a.ts : a.zero;
+}
+
+// An h task of tier TIER (one code path per tier and kind: every branch
+// below is on a compile-time value or a wave-uniform one, and no path shares
+// blocks with another, so the loads of a task go out back to back).
+//   loads: x (from the caches, ahead of the records), then kFL 16-byte record
+//   loads per lane and, for INT8 / INT4, the group scale of each.
+//   x into LDS with the chunk sums for the code offsets, the gate / up sums
+//   of every unit, then h_i = silu(a_i) b_i per neuron as a (call tag, h)
+//   word. A unit whose slot id is past the task or outside the pool reads the
+//   zero slot, so its sums and h are exactly 0.
+template <int K, int TIER, bool EXACT>
+__device__ __forceinline__ void h_task(const FTaskArgs& a, const int (&idt)[kFL][4],
+                                       const uint16_t* __restrict__ x, uint4* xlds, FShared& sh,
+                                       unsigned long long* __restrict__ hw, uint32_t epoch,
+                                       int withhold, int tid) {
+  constexpr int UW = kFL / K;                             // units per wave
+  constexpr int upi = TIER == 3 ? 4 : TIER == 2 ? 2 : 1;  // units per neuron
+  constexpr int kXC = 8192 / 16 / kFT;                    // x chunks of 16 values per thread
+  static_assert(kXC * kFT * 16 == 8192, "x staging covers d = 8192");
+  const int lane = tid & 63;
+  const int w = tid >> 6;
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  // EXACT: d = 1024 K, a unit's rows fill its K loads exactly (every address
+  // offset is then a constant)
+  const int d = EXACT ? 1024 * K : a.d;
+  const uint32_t ud = (uint32_t)d;
+  const uint32_t G = ud >> 7;
+  const int ncu = d >> 5;  // 16-byte chunks of each row in a unit
+  const uint32_t row = TIER == 3 ? 2 * ud : TIER == 2 ? ud : (ud >> 1);
+  const uint32_t sbase = TIER == 1 ? 3 * (ud >> 1) : 3 * ud;
+  const int nc8 = d >> 3;
+  const uint4* x4 = reinterpret_cast<const uint4*>(x);
+  uint4 xv[kXC][2];
+#ifdef M2C_X_FIRST
+#pragma unroll
+  for (int k = 0; k < kXC; ++k) {
+    const int c = tid + k * kFT;
+    xv[k][0] = x4[min(2 * c, nc8 - 1)];
+    xv[k][1] = x4[min(2 * c + 1, nc8 - 1)];
+  }
+#endif
+  // unit wu UW + uw of the task sits at table entry (uw / 4) kFNPR + 4 wu + uw % 4
+  uint32_t rec[UW];
+#pragma unroll
+  for (int uw = 0; uw < UW; ++uw)
+    rec[uw] = rec_of(a, idt[uw >> 2][uw & 3], (wu * UW + uw) / upi < a.n);
+  uint4 v[kFL];
+  uint32_t sc[kFL];
+  int lane_u = lane;
+#pragma unroll
+  for (int j = 0; j < kFL; ++j) {
+    const int part = (wu * UW + j / K) % upi;
+    // per unit, the lane index through an opaque copy: the offsets are
+    // recomputed per unit instead of being kept live for the next one
+    if (!EXACT && j % K == 0) asm volatile("v_mov_b32 %0, %1" : "=v"(lane_u) : "v"(lane));
+    int q = lane_u + 64 * (j % K);
+    const bool in = q < 2 * ncu;
+    q = in ? q : 2 * ncu - 1;
+    const bool up = q >= ncu;
+    const uint32_t c = (uint32_t)(part * ncu + (up ? q - ncu : q));
+    const uint32_t g = TIER == 2 ? (c >> 3) : (c >> 2);
+    v[j] = ld16(a.slots + (in ? rec[j / K] + (up ? row : 0) + 16 * c : a.zero));
+    if (TIER != 3)
+      sc[j] = ld2(a.slots + (in ? rec[j / K] + sbase + 2 * ((up ? G : 0) + g) : a.zero));
+  }
+#ifndef M2C_X_FIRST
+#pragma unroll
+  for (int k = 0; k < kXC; ++k) {
+    const int c = tid + k * kFT;
+    xv[k][0] = x4[min(2 * c, nc8 - 1)];
+    xv[k][1] = x4[min(2 * c + 1, nc8 - 1)];
+  }
+#endif
+  // x into LDS and the chunk sums of this thread's 16 values, while the
+  // records are in flight
+  uint4* xs = xlds;
+  float* nx16 = reinterpret_cast<float*>(xlds + (d >> 3));
+  float* nx32 = nx16 + (d >> 4);
+#pragma unroll
+  for (int k = 0; k < kXC; ++k) {
+    const int c = tid + k * kFT;  // chunk of 16 x values
+    const bool own = 2 * c < nc8;
+    if (own) {
+      xs[2 * c] = xv[k][0];
+      xs[2 * c + 1] = xv[k][1];
+    }
+    if (TIER != 3) {
+      const uint32_t ws[8] = {xv[k][0].x, xv[k][0].y, xv[k][0].z, xv[k][0].w,
+                              xv[k][1].x, xv[k][1].y, xv[k][1].z, xv[k][1].w};
+      float sum = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum += lo_f(ws[e]) + hi_f(ws[e]);
+      const float n16 = -128.0f * sum;
+      // -8 * (sum of 32) = (-128 * sum of this 16 - 128 * sum of the neighbour's 16) / 16
+      const float other = __int_as_float(
+          __builtin_amdgcn_mov_dpp(__float_as_int(n16), 0xB1, 0xF, 0xF, false));
+      if (own) nx16[c] = n16;
+      if (own && (c & 1) == 0) nx32[c >> 1] = (n16 + other) * 0.0625f;
+    }
+  }
+  __syncthreads();
+  // each unit's gate / up sums go to LDS as soon as its loads are done, so
+  // only one unit's pair of partial sums is live at a time
+  auto unit_done = [&](int uw, float ga, float gb) {
+    const float sa = wave_sum(ga), sbv = wave_sum(gb);
+    if (lane == 0) sh.ab[w * UW + uw] = make_float2(sa, sbv);
+  };
+  if (K >= 2 && EXACT) {
+    // A unit's rows fill its K loads exactly: load jj < K / 2 of a lane is
+    // the gate chunk c and load jj + K / 2 the up chunk c, so the x of c is
+    // read from LDS once for both.
+#pragma unroll
+    for (int uw = 0; uw < UW; ++uw) {
+      const int part = (w * UW + uw) % upi;
+      float ga = 0.0f, gb = 0.0f;
+#pragma unroll
+      for (int jj = 0; jj < K / 2; ++jj) {
+        const int jg = uw * K + jj, ju = jg + K / 2;
+        const int c = part * ncu + lane + 64 * jj;
+        float pg, pu;
+        if (TIER == 3) {
+          const uint4 xc = xs[c];
+          pg = dot8_f16(v[jg], xc, 0.0f);
+          pu = dot8_f16(v[ju], xc, 0.0f);
+        } else if (TIER == 2) {
+          const uint4 x0 = xs[2 * c], x1 = xs[2 * c + 1];
+          const float o = nx16[c];
+          pg = h2f((uint16_t)sc[jg]) * fmaf(chunk_int8(v[jg], x0, x1), kTwo24, o);
+          pu = h2f((uint16_t)sc[ju]) * fmaf(chunk_int8(v[ju], x0, x1), kTwo24, o);
+        } else {
+          uint4 xq[4];
+#pragma unroll
+          for (int u4 = 0; u4 < 4; ++u4) xq[u4] = xs[4 * c + u4];
+          const float o = nx32[c];
+          pg = h2f((uint16_t)sc[jg]) * fmaf(chunk_int4(v[jg], xq), kTwo24, o);
+          pu = h2f((uint16_t)sc[ju]) * fmaf(chunk_int4(v[ju], xq), kTwo24, o);
+        }
+        ga += pg;
+        gb += pu;
+        // one chunk at a time: keeps the x reads of later chunks from being
+        // hoisted into registers all at once
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      unit_done(uw, ga, gb);
+    }
+  } else {
+    // the lane index through an opaque copy: the chunk indices below are
+    // recomputed instead of being kept live from the address computation
+    // across the loads (which costs registers, hence spills)
+    int lane_c;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(lane_c) : "v"(lane));
+    float ga = 0.0f, gb = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kFL; ++j) {
+      const int uw = j / K;
+      const int part = (w * UW + uw) % upi;
+      int q = lane_c + 64 * (j % K);
+      q = q < 2 * ncu ? q : 2 * ncu - 1;
+      const bool up = q >= ncu;
+      const int c = part * ncu + (up ? q - ncu : q);
+      float p;
+      if (TIER == 3) {
+        p = dot8_f16(v[j], xs[c], 0.0f);
+      } else if (TIER == 2) {
+        p = h2f((uint16_t)sc[j]) * fmaf(chunk_int8(v[j], xs[2 * c], xs[2 * c + 1]), kTwo24,
+                                        nx16[c]);
+      } else {
+        uint4 xq[4];
+#pragma unroll
+        for (int u4 = 0; u4 < 4; ++u4) xq[u4] = xs[4 * c + u4];
+        p = h2f((uint16_t)sc[j]) * fmaf(chunk_int4(v[j], xq), kTwo24, nx32[c]);
+      }
+      // lanes past the unit read the zero slot: data 0 (FP16) or scale 0
+      ga += up ? 0.0f : p;
+      gb += up ? p : 0.0f;
+      __builtin_amdgcn_sched_barrier(0);
+      if (j % K == K - 1) {
+        unit_done(uw, ga, gb);
+        ga = gb = 0.0f;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < a.n) {
+    float sa = sh.ab[tid * upi].x, sbv = sh.ab[tid * upi].y;
+#pragma unroll
+    for (int u = 1; u < upi; ++u) {
+      sa += sh.ab[tid * upi + u].x;
+      sbv += sh.ab[tid * upi + u].y;
+    }
+    const float h = silu_mul(sa, sbv);
+    const unsigned long long word =
+        ((unsigned long long)epoch << 32) | (unsigned long long)__float_as_uint(h);
+    if (withhold == 0)  // test support withholds the word to drive the give-up path
+      __hip_atomic_store(hw + a.lo + tid, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Down projection of a down task: columns 16 * HALF .. 16 * HALF + 15 of the
+// lane's 32, for every neuron of the task (the two halves share the loaded
+// data and keep only 16 accumulators live). csum: sum of the lane's
+// coefficients, for the offset of INT8 / INT4 codes. sc[q]: the group scale
+// of the lane's neuron in round q.
+template <int HALF, int TIER>
+__device__ __forceinline__ void compute_dn_half(const uint4 (&v)[kFL], const uint32_t (&sc)[kFL],
+                                                const float* s_h, int tid, float (&acc)[16]) {
+  const int r = tid / kFLPN;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+  if (TIER == 3) {
+    // 4 loads per neuron and round, 8 columns each: this half is loads 2H, 2H+1
+#pragma unroll
+    for (int q = 0; q < kDnRounds3; ++q) {
+      const float c = s_h[q * kFNPR + r];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const uint4 vv = v[4 * q + 2 * HALF + e];
+        const uint32_t ws[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          acc[8 * e + 2 * u] = fmaf(c, lo_f(ws[u]), acc[8 * e + 2 * u]);
+          acc[8 * e + 2 * u + 1] = fmaf(c, hi_f(ws[u]), acc[8 * e + 2 * u + 1]);
+        }
+      }
+    }
+  } else if (TIER == 2) {
+    // 2 loads per neuron and round, 16 columns each: this half is load H
+    float csum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kDnRounds2; ++q) {
+      const float c = s_h[q * kFNPR + r] * h2f((uint16_t)sc[q]);
+      csum += c;
+      const float cs = c * kTwo24;
+      const uint4 vv = v[2 * q + HALF];
+      const uint32_t ws[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t ob = ws[u] ^ 0x80808080u;
+        const uint32_t l = __builtin_amdgcn_perm(0u, ob, 0x0c010c00u);
+        const uint32_t h = __builtin_amdgcn_perm(0u, ob, 0x0c030c02u);
+        acc[4 * u] = fmaf(cs, lo_f(l), acc[4 * u]);
+        acc[4 * u + 1] = fmaf(cs, hi_f(l), acc[4 * u + 1]);
+        acc[4 * u + 2] = fmaf(cs, lo_f(h), acc[4 * u + 2]);
+        acc[4 * u + 3] = fmaf(cs, hi_f(h), acc[4 * u + 3]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = fmaf(-128.0f, csum, acc[e]);
+  } else {
+    // 1 load per neuron and round, 32 columns: this half is words 2H, 2H+1
+    float csum = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kDnRounds1; ++q) {
+      const float c = s_h[q * kFNPR + r] * h2f((uint16_t)sc[q]);
+      csum += c;
+      const float cs = c * kTwo24;
+      const uint32_t ws[2] = {HALF ? v[q].z : v[q].x, HALF ? v[q].w : v[q].y};
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        // column 8 u + e is nibble e; odd columns sum 16 times their value.
+        // Nibbles 0..3 first, then 4..7 (after the barrier): fewer codes live.
+        const uint32_t w = ws[u] ^ 0x88888888u;
+        const uint32_t p0 = w & 0x000f000fu, p1 = w & 0x00f000f0u;
+        acc[8 * u + 0] = fmaf(cs, lo_f(p0), acc[8 * u + 0]);
+        acc[8 * u + 4] = fmaf(cs, hi_f(p0), acc[8 * u + 4]);
+        acc[8 * u + 1] = fmaf(cs, lo_f(p1), acc[8 * u + 1]);
+        acc[8 * u + 5] = fmaf(cs, hi_f(p1), acc[8 * u + 5]);
+        __builtin_amdgcn_sched_barrier(0);
+        const uint32_t w8 = w >> 8;
+        const uint32_t p2 = w8 & 0x000f000fu, p3 = w8 & 0x00f000f0u;
+        acc[8 * u + 2] = fmaf(cs, lo_f(p2), acc[8 * u + 2]);
+        acc[8 * u + 6] = fmaf(cs, hi_f(p2), acc[8 * u + 6]);
+        acc[8 * u + 3] = fmaf(cs, lo_f(p3), acc[8 * u + 3]);
+        acc[8 * u + 7] = fmaf(cs, hi_f(p3), acc[8 * u + 7]);
+        __builtin_amdgcn_sched_barrier(0);  // one word's codes live at a time
+      }
+    }
+    // exact: the odd columns' sums are 16 times the true ones, rounding included
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = fmaf(acc[e], (e & 1) ? 0.0625f : 1.0f, -8.0f * csum);
+  }
+}
+
+// A down task of tier TIER: a 512-column slice of y over a run of neurons.
+//   loads: kFL 16-byte loads per lane (a wave covers neurons 4 w .. 4 w + 3
+//   of every round, lane group lane / 16 its own one, 32 columns per lane)
+//   and, for INT8 / INT4, one group scale per round;
+//   then the h words of the run (polled, bounded), the column sums per lane,
+//   the fold over the wave's lane groups and the waves, one fp32 atomic add
+//   per column.
+template <int TIER>
+__device__ __forceinline__ void dn_task(const FTaskArgs& a, const int (&idt)[kFL][4],
+                                        uint4* xlds, FShared& sh,
+                                        const unsigned long long* __restrict__ hw,
+                                        int32_t* __restrict__ status, float* __restrict__ y,
+                                        uint32_t epoch, int withhold, int tid) {
+  constexpr int lnv = TIER == 3 ? 2 : TIER == 2 ? 1 : 0;  // log2 loads per neuron and round
+  constexpr int R = kFL >> lnv;                            // rounds
+  const int lane = tid & 63;
+  const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t ud = (uint32_t)a.d;
+  const uint32_t G = ud >> 7;
+  const uint32_t col = (uint32_t)(a.slice * kFSW + 32 * (tid % kFLPN));
+  const bool colok = col < ud;
+  const uint32_t dbase = TIER == 3 ? 4 * ud + 2 * col : TIER == 2 ? 2 * ud + col : ud + (col >> 1);
+  const uint32_t sbase = (TIER == 1 ? 3 * (ud >> 1) : 3 * ud) + 4 * G + 2 * (col >> 7);
+  const int sub = lane >> 4;
+  uint32_t rec[R];
+#pragma unroll
+  for (int q = 0; q < R; ++q) {
+    uint32_t rr[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rr[i] = rec_of(a, idt[q][i], q * kFNPR + 4 * wu + i < a.n);
+    rec[q] = sub == 0 ? rr[0] : sub == 1 ? rr[1] : sub == 2 ? rr[2] : rr[3];
+  }
+  uint4 v[kFL];
+  uint32_t sc[kFL];
+#pragma unroll
+  for (int j = 0; j < kFL; ++j) {
+    const int q = j >> lnv, e = j & ((1 << lnv) - 1);
+    v[j] = ld16(a.slots + (colok ? rec[q] + dbase + 16 * e : a.zero));
+    if (TIER != 3 && e == 0) sc[q] = ld2(a.slots + (colok ? rec[q] + sbase : a.zero));
+  }
+  // the h words of the run, polled after every load has been issued
+  float h = 0.0f;
+  if (tid < a.n) {
+    unsigned long long hv = load_word(hw + a.lo + tid);
+    const int limit = withhold > 0 ? withhold : kFSpin;
+    int spins = 0;
+    while ((uint32_t)(hv >> 32) != epoch) {
+      if (++spins > limit) {
+        atomicOr(status, M2C_STATUS_FFN_WAIT);
+        hv = 0;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+      hv = load_word(hw + a.lo + tid);
+    }
+    h = __uint_as_float((uint32_t)hv);
+  }
+  sh.h[tid] = h;
+  __syncthreads();
+  // Per half slice: 16 column sums per lane, folded over the wave's four
+  // neurons of each round to 4 (columns 4 g .. 4 g + 3 of the half, g =
+  // lane / 16); then the waves through LDS and one fp32 atomic add per
+  // column. (Each lane stores its own four sums of a half as soon as they
+  // are folded: the LDS bytes are not used otherwise by a down task.)
+  float* part = reinterpret_cast<float*>(xlds);
+  float* row = part + (tid >> 6) * kFBlock + (tid & 15) * kFRow + 4 * ((tid & 63) >> 4);
+  {
+    float acc[16], o[4];
+    compute_dn_half<0, TIER>(v, sc, sh.h, tid, acc);
+    wave_fold16(acc, o);
+    *reinterpret_cast<float4*>(row) = make_float4(o[0], o[1], o[2], o[3]);
+  }
+  {
+    float acc[16], o[4];
+    compute_dn_half<1, TIER>(v, sc, sh.h, tid, acc);
+    wave_fold16(acc, o);
+    *reinterpret_cast<float4*>(row + 16) = make_float4(o[0], o[1], o[2], o[3]);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kFSW / kFT; ++k) {
+    const int c = tid + k * kFT;  // column of the slice
+    const float* src = part + (c >> 5) * kFRow + (c & 31);
+    float s = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kFWaves; ++w) s += src[w * kFBlock];
+    const int cy = a.slice * kFSW + c;
+    if (cy < a.d) atomicAdd(y + cy, s);
+  }
+}
+
+// at most 96 VGPRs: five workgroups per CU
 template <int K>
 #ifndef M2C_FFN_WAVES_PER_EU
 #define M2C_FFN_WAVES_PER_EU 5
@@ -573,9 +689,8 @@ template <int K>
 __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(M2C_FFN_WAVES_PER_EU))) void ffn_fused_kernel(
     const uint16_t* __restrict__ x, const int32_t* __restrict__ tasks,
     const int32_t* __restrict__ task_ids, unsigned long long* __restrict__ gen,
-    const uint8_t* __restrict__ slots, int d, int n_slots, const int32_t* __restrict__ work_slot,
-    unsigned long long* __restrict__ hw, int32_t* __restrict__ status, float* __restrict__ y,
-    int withhold) {
+    const uint8_t* __restrict__ slots, int d, unsigned long long* __restrict__ hw,
+    int32_t* __restrict__ status, float* __restrict__ y, int withhold) {
   // (argument order: what the first round trip needs comes first, inside the
   // preloaded kernel arguments)
   extern __shared__ uint4 xlds[];  // fused_lds_bytes(d)
@@ -602,161 +717,60 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(M2C_FFN_WAV
   // instead of one of its own after the task header)
   __builtin_amdgcn_sched_barrier(0);
   asm volatile("" ::"s"((uint32_t)e0), "s"((uint32_t)(e0 >> 32)));
-  FTaskPool kp;
-  FTask& kc = kp.k;
-  kc.kind = t < n_tasks ? (hd.x & 0xff) : 0;
-  kc.tier = (hd.x >> 8) & 0xff;
-  kc.lo = hd.y;
-  kc.hi = hd.y + hd.z;
-  kc.slice = hd.w;
-  kp.tb = (uint32_t)hp.x;
-  kp.tf = (uint32_t)hp.y;
-  kp.tc = (uint32_t)hp.z;
-  kp.ts = (uint32_t)hp.w;
-  if (kc.kind == 0) {
+  const int kind = t < n_tasks ? (hd.x & 0xff) : 0;
+  const int tier = (hd.x >> 8) & 0xff;
+  if (kind != 1 && kind != 2) {
     if (tid == 0) gen[t] = e0 + 1;  // keep this workgroup's count in step
     return;
   }
-  const int n_items = kc.hi - kc.lo;
-  uint4* xs = xlds;
-  float* nx16 = reinterpret_cast<float*>(xlds + (d >> 3));
-  float* nx32 = nx16 + (d >> 4);
-  // for the h publish: this thread's item slot (needed only at the end)
-  const bool okslot = tid < n_items;
-  const int sl = work_slot[okslot ? kc.lo + tid : 0];
-  FBuf cur;
-  // h tasks stage x: kXC chunks of 16 values per thread (chunk tid + k kFT)
-  constexpr int kXC = 8192 / 16 / kFT;
-  static_assert(kXC * kFT * 16 == 8192, "x staging covers d = 8192");
-  uint4 xv[kXC][2];
-  const int nc8 = d >> 3;
-  const uint4* x4 = reinterpret_cast<const uint4*>(x);
-  if (kc.kind == 1) {
-    // x in registers. With one chunk per thread it is loaded before the data
-    // loads (which wait only for the scalar slot loads inside issue) and
-    // arrives while they fly; more chunks are loaded after them (registers).
-#pragma unroll
-    for (int k = 0; k < kXC; ++k) {
-      if (kXC > 1) break;
-      const int c = tid + k * kFT;
-      xv[k][0] = x4[min(2 * c, nc8 - 1)];
-      xv[k][1] = x4[min(2 * c + 1, nc8 - 1)];
-    }
-    issue<K>(kp, idt, d, slots, zero, n_slots, tid, cur);
-#pragma unroll
-    for (int k = 0; k < kXC; ++k) {
-      if (kXC == 1) break;
-      const int c = tid + k * kFT;
-      xv[k][0] = x4[min(2 * c, nc8 - 1)];
-      xv[k][1] = x4[min(2 * c + 1, nc8 - 1)];
-    }
-  } else {
-    issue<K>(kp, idt, d, slots, zero, n_slots, tid, cur);
-  }
+  FTaskArgs a;
+  a.slots = slots;
+  a.zero = zero;
+  a.tb = (uint32_t)hp.x;
+  a.tf = (uint32_t)hp.y;
+  a.tc = (uint32_t)hp.z;
+  a.ts = (uint32_t)hp.w;
+  a.d = d;
+  a.lo = hd.y;
+  a.n = hd.z;
+  a.slice = hd.w;
   const uint32_t epoch = (uint32_t)e0 + 1u;
-  if (kc.kind == 1) {
-    // x into LDS and the chunk sums of this thread's 16 values, while the
-    // task's loads are in flight
-#pragma unroll
-    for (int k = 0; k < kXC; ++k) {
-      const int c = tid + k * kFT;  // chunk of 16 x values
-      const bool own = 2 * c < (d >> 3);
-      if (own) {
-        xs[2 * c] = xv[k][0];
-        xs[2 * c + 1] = xv[k][1];
-      }
-      const uint32_t ws[8] = {xv[k][0].x, xv[k][0].y, xv[k][0].z, xv[k][0].w,
-                              xv[k][1].x, xv[k][1].y, xv[k][1].z, xv[k][1].w};
-      float sum = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sum += lo_f(ws[e]) + hi_f(ws[e]);
-      const float n16 = -128.0f * sum;
-      // -8 * (sum of 32) = (-128 * sum of this 16 - 128 * sum of the neighbour's 16) / 16
-      const float other = __int_as_float(
-          __builtin_amdgcn_mov_dpp(__float_as_int(n16), 0xB1, 0xF, 0xF, false));
-      if (own) nx16[c] = n16;
-      if (own && (c & 1) == 0) nx32[c >> 1] = (n16 + other) * 0.0625f;
-    }
-    __syncthreads();
-    compute_h<K>(kc, cur, d, xs, nx16, nx32, tid, sh.ab);
-    __syncthreads();
-    const int upi = kc.tier == 3 ? 4 : kc.tier == 2 ? 2 : 1;
-    if (tid < n_items) {
-      float sa = sh.ab[tid * upi].x, sbv = sh.ab[tid * upi].y;
-      for (int u = 1; u < upi; ++u) {
-        sa += sh.ab[tid * upi + u].x;
-        sbv += sh.ab[tid * upi + u].y;
-      }
-      const float h = sl >= 0 && sl < n_slots ? silu_mul(sa, sbv) : 0.0f;
-      const unsigned long long word =
-          ((unsigned long long)epoch << 32) | (unsigned long long)__float_as_uint(h);
-      if (withhold == 0)  // test support withholds the word to drive the give-up path
-        __hip_atomic_store(hw + kc.lo + tid, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (kind == 1) {
+    if (K >= 2 && d == 1024 * K) {
+      if (tier == 1)
+        h_task<K, 1, true>(a, idt, x, xlds, sh, hw, epoch, withhold, tid);
+      else if (tier == 2)
+        h_task<K, 2, true>(a, idt, x, xlds, sh, hw, epoch, withhold, tid);
+      else
+        h_task<K, 3, true>(a, idt, x, xlds, sh, hw, epoch, withhold, tid);
+    } else {
+      if (tier == 1)
+        h_task<K, 1, false>(a, idt, x, xlds, sh, hw, epoch, withhold, tid);
+      else if (tier == 2)
+        h_task<K, 2, false>(a, idt, x, xlds, sh, hw, epoch, withhold, tid);
+      else
+        h_task<K, 3, false>(a, idt, x, xlds, sh, hw, epoch, withhold, tid);
     }
   } else {
-    // the h words of the run, polled after every data load has been issued
-    float h = 0.0f;
-    if (tid < n_items) {
-      unsigned long long hv = load_word(hw + kc.lo + tid);
-      const int limit = withhold > 0 ? withhold : kFSpin;
-      int spins = 0;
-      while ((uint32_t)(hv >> 32) != epoch) {
-        if (++spins > limit) {
-          atomicOr(status, M2C_STATUS_FFN_WAIT);
-          hv = 0;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        hv = load_word(hw + kc.lo + tid);
-      }
-      h = __uint_as_float((uint32_t)hv);
-    }
-    sh.h[tid] = h;
-    __syncthreads();
-    // Per half slice: 16 column sums per lane, folded over the wave's four
-    // neurons of each round to 4 (columns 4 g .. 4 g + 3 of the half, g =
-    // lane / 16); then the waves through LDS and one fp32 atomic add per
-    // column.
-    // (each lane stores its own four sums of a half as soon as they are
-    // folded: the LDS bytes are not used otherwise by a down task)
-    float* part = reinterpret_cast<float*>(xlds);
-    float* row = part + (tid >> 6) * kFBlock + (tid & 15) * kFRow + 4 * ((tid & 63) >> 4);
-    {
-      float acc[16], o[4];
-      compute_dn_half<0>(kc, cur, sh.h, tid, acc);
-      wave_fold16(acc, o);
-      *reinterpret_cast<float4*>(row) = make_float4(o[0], o[1], o[2], o[3]);
-    }
-    {
-      float acc[16], o[4];
-      compute_dn_half<1>(kc, cur, sh.h, tid, acc);
-      wave_fold16(acc, o);
-      *reinterpret_cast<float4*>(row + 16) = make_float4(o[0], o[1], o[2], o[3]);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < kFSW / kFT; ++k) {
-      const int c = tid + k * kFT;  // column of the slice
-      const float* src = part + (c >> 5) * kFRow + (c & 31);
-      float v = 0.0f;
-#pragma unroll
-      for (int w = 0; w < kFWaves; ++w) v += src[w * kFBlock];
-      const int col = kc.slice * kFSW + c;
-      if (col < d) atomicAdd(y + col, v);
-    }
+    if (tier == 1)
+      dn_task<1>(a, idt, xlds, sh, hw, status, y, epoch, withhold, tid);
+    else if (tier == 2)
+      dn_task<2>(a, idt, xlds, sh, hw, status, y, epoch, withhold, tid);
+    else
+      dn_task<3>(a, idt, xlds, sh, hw, status, y, epoch, withhold, tid);
   }
   if (tid == 0) gen[t] = e0 + 1;
 }
 
 template <int K>
-hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* tasks,
-                        const int32_t* work_slot, float* y, hipStream_t stream) {
+hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* tasks, float* y,
+                        hipStream_t stream) {
   const int d = L->desc.d_model;
   const size_t lds = fused_lds_bytes(d);
   const int32_t* task_ids = tasks + task_ids_offset(L->ffn_grid) / 4;
   hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, tasks,
-                     task_ids, L->st.ffn_gen, L->slots, d, L->desc.cache_slots + L->S, work_slot,
-                     L->st.ffn_hw, L->st.status, y, L->ffn_withhold);
+                     task_ids, L->st.ffn_gen, L->slots, d, L->st.ffn_hw, L->st.status, y,
+                     L->ffn_withhold);
   return hipGetLastError();
 }
 
@@ -844,12 +858,11 @@ hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan
                             hipStream_t stream) {
   if (L->cap <= 0 || L->ffn_grid <= 0) return hipSuccess;
   const int32_t* tasks = reinterpret_cast<const int32_t*>(plan + L->layout.ffn_tasks);
-  const int32_t* work_slot = reinterpret_cast<const int32_t*>(plan + L->layout.work_slot);
   switch (loads_per_unit(L->desc.d_model)) {
-    case 1: return launch_fused<1>(L, x, tasks, work_slot, y, stream);
-    case 2: return launch_fused<2>(L, x, tasks, work_slot, y, stream);
-    case 4: return launch_fused<4>(L, x, tasks, work_slot, y, stream);
-    default: return launch_fused<8>(L, x, tasks, work_slot, y, stream);
+    case 1: return launch_fused<1>(L, x, tasks, y, stream);
+    case 2: return launch_fused<2>(L, x, tasks, y, stream);
+    case 4: return launch_fused<4>(L, x, tasks, y, stream);
+    default: return launch_fused<8>(L, x, tasks, y, stream);
   }
 }
 
