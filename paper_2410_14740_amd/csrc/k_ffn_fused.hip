@@ -157,8 +157,15 @@ __device__ __forceinline__ FTask decode(const FMap& m, int t) {
   } else {
     k.kind = 2;
     const int per = (tier == 1 ? kDnRounds1 : tier == 2 ? kDnRounds2 : kDnRounds3) * kFNPR;
-    const int run = q / m.n_slices;
-    k.slice = q - run * m.n_slices;
+    // Runs in blocks of 8, slice-major within a block: workgroup b runs on
+    // XCD b % 8, so all slices of a run (which read the same scale lines of
+    // the run's records) land on one XCD and its L2.
+    const int nr = (n + per - 1) / per;
+    const int blk = q / (8 * m.n_slices);
+    const int within = q - blk * 8 * m.n_slices;
+    const int nb = min(8, nr - 8 * blk);
+    k.slice = within / nb;
+    const int run = 8 * blk + (within - k.slice * nb);
     k.lo = base + per * run;
     k.hi = base + min(per * (run + 1), n);
   }
