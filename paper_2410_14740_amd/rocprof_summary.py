@@ -10,6 +10,8 @@ profiles/, and read the counter figures back for bench.py.
     python -m paper_2410_14740_amd.rocprof_summary kernels --name NAME --command CMD \
         --kernel NAME1 --kernel NAME2 --trace ... --fetch ... --write ... \
         --copy-fetch ... --copy-write ... --copy-bytes B --algorithmic-bytes A --out profiles/NAME.md
+    python -m paper_2410_14740_amd.rocprof_summary counters --name NAME --command CMD \
+        --kernel NAME --pmc DIR/PREFIX_counter_collection.csv [--pmc ...] --last N --out profiles/NAME.md
 
 The FFN summary holds the average duration of each sparse-FFN kernel over the
 last N back-to-back calls of the trace, the HBM bytes per call from the
@@ -135,6 +137,45 @@ def kernels_summary(a) -> str:
     return "\n".join(lines)
 
 
+def counters_summary(a) -> str:
+    """Mean value per dispatch of every counter in the given collection files
+    (one rocprofv3 --pmc pass each), over the last N dispatches of the named
+    kernel, with the ratios that say where its time goes."""
+    vals = collections.defaultdict(list)
+    for path in a.pmc:
+        for r in csv.DictReader(open(path)):
+            if a.kernel in r["Kernel_Name"]:
+                vals[r["Counter_Name"]].append(float(r["Counter_Value"]))
+    mean = {k: sum(v[-a.last:]) / len(v[-a.last:]) for k, v in vals.items() if v}
+    lines = [f"# {a.name}", "", a.description, "", "Commands (from the repository root, on one MI355X):", ""]
+    lines += [f"    {c}" for c in a.command]
+    lines += ["", f"| Counter (`{a.kernel}`, mean of the last {a.last} dispatches) | Value |", "|---|---|"]
+    for k in sorted(mean):
+        lines.append(f"| `{k}` | {mean[k]:.1f} |")
+    derived = {}
+    if mean.get("SQ_WAVES"):
+        w = mean["SQ_WAVES"]
+        for k in ("SQ_INSTS_VALU", "SQ_INSTS_VMEM_RD", "SQ_INSTS_SALU", "SQ_INSTS_LDS", "SQ_INSTS_SMEM"):
+            if k in mean:
+                derived[f"{k} per wave"] = mean[k] / w
+    if mean.get("SQ_WAVE_CYCLES"):
+        wc = mean["SQ_WAVE_CYCLES"]
+        for k in ("SQ_WAIT_INST_ANY", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_ANY"):
+            if k in mean:
+                derived[f"{k} / SQ_WAVE_CYCLES"] = mean[k] / wc
+    if mean.get("TCC_REQ_sum") and "TCC_HIT_sum" in mean:
+        derived["L2 hit rate (TCC_HIT / TCC_REQ)"] = mean["TCC_HIT_sum"] / mean["TCC_REQ_sum"]
+    if mean.get("GRBM_GUI_ACTIVE") and "SQ_BUSY_CYCLES" in mean:
+        derived["SQ_BUSY_CYCLES / GRBM_GUI_ACTIVE"] = mean["SQ_BUSY_CYCLES"] / mean["GRBM_GUI_ACTIVE"]
+    if derived:
+        lines += ["", "| Derived | Value |", "|---|---|"]
+        for k, v in derived.items():
+            lines.append(f"| {k} | {v:.3f} |")
+    lines += ["", "```json", json.dumps({"kernel": a.kernel, "last": a.last, "mean": mean,
+                                         "derived": derived}, indent=1, sort_keys=True), "```", ""]
+    return "\n".join(lines)
+
+
 def stats_summary(a) -> str:
     rows = list(csv.DictReader(open(a.stats)))
     lines = [f"# {a.name}", "", a.description, "", "Command (from the repository root, on one MI355X):", ""]
@@ -181,13 +222,21 @@ def main():
     kp.add_argument("--algorithmic-bytes", type=int, required=True)
     kp.add_argument("--command", action="append", required=True)
     kp.add_argument("--description", default="")
+    cp = sub.add_parser("counters")
+    for n in ("--name", "--kernel", "--out"):
+        cp.add_argument(n, required=True)
+    cp.add_argument("--pmc", action="append", required=True)
+    cp.add_argument("--last", type=int, default=40)
+    cp.add_argument("--command", action="append", required=True)
+    cp.add_argument("--description", default="")
     s = sub.add_parser("stats")
     for n in ("--stats", "--out", "--name"):
         s.add_argument(n, required=True)
     s.add_argument("--command", action="append", required=True)
     s.add_argument("--description", default="")
     a = p.parse_args()
-    text = {"ffn": ffn_summary, "kernels": kernels_summary, "stats": stats_summary}[a.mode](a)
+    text = {"ffn": ffn_summary, "kernels": kernels_summary, "stats": stats_summary,
+            "counters": counters_summary}[a.mode](a)
     with open(a.out, "w") as fh:
         fh.write(text)
     print(text)
