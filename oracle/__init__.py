@@ -263,23 +263,48 @@ class TierPoolCache:
     numbered in tier blocks, FP16 first: block t holds pool t's resident
     slots then its staging slots. The merged plan lists R in ascending id,
     the fills (every non-HIT) in ascending id, and the evictions of pool
-    FP16, then INT8, then INT4, each in its victim order."""
+    FP16, then INT8, then INT4, each in its victim order.
+
+    policy POLICY_DOMINANCE (dominance hits across the pools): before the
+    pools plan, a neuron required at tier t that is not resident in pool t
+    but is resident in a pool of higher precision is served by the lowest
+    such pool, as a HIT at that pool's tier (its record holds more bits of
+    the same weights); residency is taken at the start of the step. Every
+    other neuron stays with its own tier's pool."""
 
     TIERS = (3, 2, 1)
 
-    def __init__(self, d_ff: int, C: dict, S: dict):
+    def __init__(self, d_ff: int, C: dict, S: dict, policy: int = POLICY_EXACT):
         self.d_ff = d_ff
+        self.policy = policy
         self.pools = {t: LRUCache(d_ff, C[t], S[t]) for t in self.TIERS}
         self.first, off = {}, 0
         for t in self.TIERS:
             self.first[t] = off
             off += C[t] + S[t]
 
+    def resolve(self, step_tier) -> np.ndarray:
+        """The pool tier each neuron is served from this step (0 = not
+        required), as the dominance policy picks it; the step tier itself
+        under POLICY_EXACT."""
+        res = np.array(step_tier, dtype=np.uint8, copy=True)
+        if self.policy != POLICY_DOMINANCE:
+            return res
+        for n in np.nonzero(res)[0]:
+            t = int(res[n])
+            if self.pools[t].slot_of[n] >= 0:
+                continue
+            for hi in range(t + 1, 4):
+                if self.pools[hi].slot_of[n] >= 0:
+                    res[n] = hi
+                    break
+        return res
+
     def plan(self, tier_map, step: int) -> dict:
         tm = np.ascontiguousarray(tier_map, dtype=np.uint8)
         if tm.ndim == 1:
             tm = tm[None, :]
-        step_tier = tm.max(axis=0)
+        step_tier = self.resolve(tm.max(axis=0))
         parts = {}
         for t in self.TIERS:
             sub = np.where((tm > 0) & (step_tier == t)[None, :], t, 0).astype(np.uint8)

@@ -511,18 +511,25 @@ def test_oracle_results_do_not_depend_on_threads():
     assert np.array_equal(y1.view(np.uint64), y4.view(np.uint64))
 
 
-def test_tier_pools_are_independent_lru_caches():
+@pytest.mark.parametrize("policy,d_ff,C", [
+    (oracle.POLICY_EXACT, 60, {3: 3, 2: 5, 1: 8}),
+    (oracle.POLICY_DOMINANCE, 60, {3: 3, 2: 5, 1: 8}),
+    (oracle.POLICY_DOMINANCE, 30, {3: 10, 2: 10, 1: 6})])
+def test_tier_pools_are_independent_lru_caches(policy, d_ff, C):
     """The per-tier arena: each pool is the step-atomic LRU brute force over
     the requests of its tier alone, slots numbered in tier blocks; the merged
-    lists are the pools' lists in ascending id; no REFILL ever happens."""
-    d_ff, B = 60, 2
-    C = {3: 3, 2: 5, 1: 8}
+    lists are the pools' lists in ascending id; no REFILL ever happens.
+    Dominance: a neuron not resident in its own tier's pool but resident (at
+    the step's start, in the brute force's own tables) in a pool of higher
+    precision is that lowest such pool's request, a HIT at its tier."""
+    B = 2
     S = {3: 20, 2: 20, 1: 20}
-    cache = oracle.TierPoolCache(d_ff, C, S)
-    first = {3: 0, 2: 23, 1: 48}
+    cache = oracle.TierPoolCache(d_ff, C, S, policy)
+    first = {3: 0, 2: C[3] + S[3], 1: C[3] + S[3] + C[2] + S[2]}
     states = {t: ({}, [None] * C[t], [0] * C[t], [-1] * C[t]) for t in (3, 2, 1)}
     rng = np.random.default_rng(12)
     code = {"NEW": 0, "HIT": 1, "REFILL": 2, "BYPASS": 3}
+    dominance_hits = 0
     for step in range(40):
         tm = np.zeros((B, d_ff), np.uint8)
         for b in range(B):
@@ -530,6 +537,14 @@ def test_tier_pools_are_independent_lru_caches():
             tm[b, ids] = rng.integers(1, 4, size=ids.size)
         p = cache.plan(tm, step)
         st = tm.max(axis=0)
+        if policy == oracle.POLICY_DOMINANCE:
+            for i in range(d_ff):
+                t = int(st[i])
+                if t and i not in states[t][0]:
+                    up = [u for u in (1, 2, 3) if u > t and i in states[u][0]]
+                    if up:
+                        st[i] = min(up)
+                        dominance_hits += 1
         want = {}
         evicted = []
         for t in (3, 2, 1):
@@ -547,3 +562,5 @@ def test_tier_pools_are_independent_lru_caches():
         assert list(p["fill_ids"]) == [i for i in req if want[i][1] != 1]
         assert list(p["evicted_ids"]) == evicted
         assert not p["fill_from"].any()
+    if policy == oracle.POLICY_DOMINANCE:
+        assert dominance_hits > 10
