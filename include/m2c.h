@@ -164,10 +164,12 @@ enum {
      there (victims from that pool, BYPASS into that pool's staging slots,
      max(0, plan_capacity - tier_slots[t]) of them). A neuron may be resident
      in several pools; there are no REFILLs. Global slot ids are numbered in
-     tier blocks, FP16 first (see m2c_layer_info.pool_first). Exact-tier
-     hits only (not with M2C_FLAG_DOMINANT_HITS); needs max_batch == 1,
-     d_model <= 8192, d_ff <= 32768, staging_slots == -1, and not
-     M2C_FLAG_DETERMINISTIC_FFN. */
+     tier blocks, FP16 first (see m2c_layer_info.pool_first). With
+     M2C_FLAG_DOMINANT_HITS a neuron required at tier t that is not resident
+     in pool t but is resident (at the start of the step) in a pool of higher
+     precision is served by the lowest such pool, a HIT at that pool's tier
+     (req_tier and the FFN carry it). Needs max_batch == 1, d_model <= 8192,
+     d_ff <= 32768, staging_slots == -1, and not M2C_FLAG_DETERMINISTIC_FFN. */
   M2C_FLAG_TIER_POOLS = 4
 };
 

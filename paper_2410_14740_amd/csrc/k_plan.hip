@@ -643,6 +643,30 @@ __global__ __launch_bounds__(kPlanThreads) void plan_pools_kernel(
                  abort_word);
 }
 
+// Per-tier arena with dominance hits: the pool that serves each neuron this
+// step. A neuron required at tier t (its highest tier over the batch rows)
+// that is not resident in pool t but is resident in a pool of higher
+// precision goes to the lowest such pool, as a hit at that pool's tier; any
+// other neuron keeps its tier. Residency is read before any pool plans the
+// step. slot_of: the pools' tables [3][d_ff], FP16 first.
+__global__ __launch_bounds__(256) void pool_resolve_kernel(const uint8_t* __restrict__ tier_map,
+                                                           int B, int d_ff,
+                                                           const int32_t* __restrict__ slot_of,
+                                                           uint8_t* __restrict__ out) {
+  for (int n = blockIdx.x * blockDim.x + threadIdx.x; n < d_ff; n += gridDim.x * blockDim.x) {
+    int t = 0;
+    for (int b = 0; b < B; ++b) t = max(t, (int)tier_map[(int64_t)b * d_ff + n]);
+    if (t >= 1 && t <= 3 && slot_of[(int64_t)(3 - t) * d_ff + n] < 0) {
+      for (int hi = t + 1; hi <= 3; ++hi)
+        if (slot_of[(int64_t)(3 - hi) * d_ff + n] >= 0) {
+          t = hi;
+          break;
+        }
+    }
+    out[n] = (uint8_t)t;
+  }
+}
+
 // Empties one cache unit (or one pool of the per-tier arena: its own
 // tables); clears n_rec entries of the fill's record table and, with
 // clear_stats, the counters.
@@ -823,8 +847,21 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
     pp.p[q] = {Pq.counts, Pq.req_ids, Pq.req_hit, Pq.req_slot, Pq.req_mask, Pq.fill_ids,
                Pq.fill_slot, Pq.evicted_ids};
   }
-  hipLaunchKernelGGL(plan_pools_kernel, dim3(3), dim3(kPlanThreads), 0, stream, tier_map, batch,
-                     L->desc.d_ff, L->cap, step, jobs, L->plan_abort);
+  const uint8_t* pool_map = tier_map;
+  int pool_batch = batch;
+  if (dom) {
+    const int d_ff = L->desc.d_ff;
+    int blocks = (d_ff + 255) / 256;
+    blocks = blocks > 128 ? 128 : blocks;
+    hipLaunchKernelGGL(pool_resolve_kernel, dim3(blocks), dim3(256), 0, stream, tier_map, batch,
+                       d_ff, L->st.slot_of, L->pool_res);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    pool_map = L->pool_res;
+    pool_batch = 1;
+  }
+  hipLaunchKernelGGL(plan_pools_kernel, dim3(3), dim3(kPlanThreads), 0, stream, pool_map,
+                     pool_batch, L->desc.d_ff, L->cap, step, jobs, L->plan_abort);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   int blocks = (L->cap + 255) / 256;

@@ -91,9 +91,8 @@ m2c_status check_desc(const m2c_layer_desc* D, int* S_out, int* cap_out) {
   if (D->flags & ~(M2C_FLAG_DETERMINISTIC_FFN | M2C_FLAG_DOMINANT_HITS | M2C_FLAG_TIER_POOLS))
     return fail(M2C_ERR_INVALID_ARG, "flags 0x%x: unknown bits", D->flags);
   if (D->flags & M2C_FLAG_TIER_POOLS) {
-    if (D->flags & (M2C_FLAG_DETERMINISTIC_FFN | M2C_FLAG_DOMINANT_HITS))
-      return fail(M2C_ERR_INVALID_ARG, "tier pools take neither the deterministic FFN nor "
-                  "dominance hits");
+    if (D->flags & M2C_FLAG_DETERMINISTIC_FFN)
+      return fail(M2C_ERR_INVALID_ARG, "tier pools do not take the deterministic FFN");
     if (D->max_batch != 1 || D->d_model > 8192 || D->d_ff > 32768 || D->staging_slots != -1)
       return fail(M2C_ERR_INVALID_ARG, "tier pools need max_batch 1, d_model <= 8192, d_ff <= "
                   "32768 and staging_slots -1");
@@ -244,7 +243,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
   void* p_vslot; void* p_vold; void* p_fill_pos; void* p_prev_tier; void* p_have; void* p_stats;
   void* p_status;
-  void* p_gen; void* p_hw; void* p_pool_plan; void* p_abort;
+  void* p_gen; void* p_hw; void* p_pool_plan; void* p_abort; void* p_pool_res;
   Piece pieces[] = {
       // C resident + S staging slots, then one slot that stays zero: padding
       // lanes of the FFN kernels read it instead of branching around loads
@@ -276,6 +275,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_hw, cap * 8},
       {&p_pool_plan, L->pools ? 3 * L->plan_core_bytes : 0},
       {&p_abort, 4},
+      {&p_pool_res, L->pools ? dff : 0},
   };
   int64_t total = 0;
   int64_t offs[sizeof(pieces) / sizeof(pieces[0])];
@@ -316,6 +316,7 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.ffn_hw = (unsigned long long*)p_hw;
   L->pool_plan = (uint8_t*)p_pool_plan;
   L->plan_abort = (int32_t*)p_abort;
+  L->pool_res = (uint8_t*)p_pool_res;
   L->info.device_bytes = total;
   HIPOK(hipMemset(L->slots + L->map.zero, 0, L->info.slot_bytes), "clear the zero slot");
   HIPOK(hipMemset(L->plan_abort, 0, 4), "clear the plan abort word");

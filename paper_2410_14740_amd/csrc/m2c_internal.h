@@ -103,6 +103,7 @@ struct m2c_layer {
   m2c::SlotMap map;               // slot id -> byte offset, by tier
   int64_t arena_bytes = 0;        // pools + zero slot
   uint8_t* pool_plan = nullptr;   // [3][plan_core_bytes] the pools' own plans
+  uint8_t* pool_res = nullptr;    // [d_ff] serving pool's tier per neuron (pools with dominance hits)
   int64_t plan_core_bytes = 0;    // a plan without the one-launch FFN's task table
   int32_t* plan_abort = nullptr;  // [1] set when a step's required set overflowed
 };

@@ -83,6 +83,7 @@ POOLS = {3: 20, 2: 80, 1: 120}  # below each tier's demand (35 / 140 / 175)
     (2, 1, True, True, 0),
     (3, 2, True, True, m2c.FLAG_DOMINANT_HITS),
     (3, 2, True, True, m2c.FLAG_TIER_POOLS),
+    (3, 2, True, True, m2c.FLAG_TIER_POOLS | m2c.FLAG_DOMINANT_HITS),
 ])
 def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
     d, d_ff, r, steps = 512, 1400, 32, 12
@@ -90,8 +91,8 @@ def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
     n16, n8 = k // 10, (k // 2) - k // 10
     C = 250  # below k: evictions and bypasses through staging slots every step
     pools = bool(flags & m2c.FLAG_TIER_POOLS)
-    desc = (m2c.make_desc(d, d_ff, r, k, 0, tier_slots=POOLS) if pools
-            else m2c.make_desc(d, d_ff, r, k, C, flags=flags))
+    desc = (m2c.make_desc(d, d_ff, r, k, 0, flags=flags & ~m2c.FLAG_TIER_POOLS, tier_slots=POOLS)
+            if pools else m2c.make_desc(d, d_ff, r, k, C, flags=flags))
     policy = oracle.POLICY_DOMINANCE if flags & m2c.FLAG_DOMINANT_HITS else oracle.POLICY_EXACT
     lds = [W.make_layer(900 + n_layers, l, d, d_ff, r, steps, rhos=(0.8,)) for l in range(n_layers)]
     layers = [m2c.Layer(desc, ld) for ld in lds]
@@ -114,7 +115,8 @@ def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
     worst = 0.0
     for l, (L, ld) in enumerate(zip(layers, lds)):
         if pools:
-            cache = oracle.TierPoolCache(d_ff, POOLS, {t: max(0, k - POOLS[t]) for t in (1, 2, 3)})
+            cache = oracle.TierPoolCache(d_ff, POOLS, {t: max(0, k - POOLS[t]) for t in (1, 2, 3)},
+                                         policy)
         else:
             cache = oracle.LRUCache(d_ff, C, L.info.staging_slots, policy)
         tot = np.zeros(16, np.int64)

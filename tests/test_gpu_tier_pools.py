@@ -3,7 +3,8 @@ TierPoolCache: tiers, every plan field (slots in tier blocks), each pool's
 tables, the counters and the FFN outputs over several steps, with pools
 smaller than their tier's demand (evictions and bypasses in every pool),
 larger (hits), an empty pool, the 70B shape at the HBM budget of C = k
-FP16-sized slots, and the overflow report."""
+FP16-sized slots, and the overflow report; with exact-tier hits and with
+dominance hits across the pools (M2C_FLAG_DOMINANT_HITS)."""
 import numpy as np
 import pytest
 
@@ -22,14 +23,16 @@ def _x16(ld, t):
     return torch.from_numpy(np.ascontiguousarray(ld.x[t].view(np.uint16))).cuda().view(torch.float16)
 
 
-def _run(ld, steps, k, n16, n8, tier_slots, label):
+def _run(ld, steps, k, n16, n8, tier_slots, label, dominance=False):
     d, d_ff = ld.d_model, ld.d_ff
-    L = m2c.Layer(m2c.make_desc(d, d_ff, ld.pred_rank, k, 0, tier_slots=tier_slots), ld)
+    flags = m2c.FLAG_DOMINANT_HITS if dominance else 0
+    L = m2c.Layer(m2c.make_desc(d, d_ff, ld.pred_rank, k, 0, flags=flags, tier_slots=tier_slots), ld)
     info = L.info
     C = {t: tier_slots[t] for t in (1, 2, 3)}
     S = {t: info.pool_slots[t] - C[t] for t in (1, 2, 3)}
     assert all(S[t] == max(0, k - C[t]) for t in (1, 2, 3))
-    cache = oracle.TierPoolCache(d_ff, C, S)
+    cache = oracle.TierPoolCache(d_ff, C, S,
+                                 oracle.POLICY_DOMINANCE if dominance else oracle.POLICY_EXACT)
     assert [info.pool_first[t] for t in (3, 2, 1)] == [cache.first[t] for t in (3, 2, 1)]
     assert all(info.pool_stride[t] == info.record_stride[t] for t in (1, 2, 3))
     tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
@@ -75,18 +78,22 @@ def _run(ld, steps, k, n16, n8, tier_slots, label):
     return worst, tot
 
 
+@pytest.mark.parametrize("dominance", [False, True])
 @pytest.mark.parametrize("tier_slots", [{3: 60, 2: 150, 1: 250}, {3: 400, 2: 500, 1: 700},
                                         {3: 0, 2: 300, 1: 300}])
-def test_tier_pools_tiny(tier_slots):
+def test_tier_pools_tiny(tier_slots, dominance):
     ld = W.make_layer(W.WORKLOADS["tiny"].seed, 11, 1024, 2752, 128, 10, rhos=(0.85,))
     k, n16, n8 = 688, 229, 229
-    worst, tot = _run(ld, 10, k, n16, n8, tier_slots, f"pools {tier_slots}")
+    worst, tot = _run(ld, 10, k, n16, n8, tier_slots, f"pools {tier_slots} dom {dominance}",
+                      dominance)
     assert tot[1] > 0  # hits happened
-    say(f"pools {tier_slots}: worst FFN error {worst:.2e}, hits {tot[1]}, bypass {tot[4]}")
+    say(f"pools {tier_slots} dominance {dominance}: worst FFN error {worst:.2e}, hits {tot[1]}, "
+        f"bypass {tot[4]}")
 
 
 @pytest.mark.timeout(900)
-def test_tier_pools_llama70b_layer_at_the_same_budget():
+@pytest.mark.parametrize("dominance", [False, True])
+def test_tier_pools_llama70b_layer_at_the_same_budget(dominance):
     """The 70B shape with the HBM of C = k = 2867 FP16-sized slots split into
     pools that each hold the same multiple of their tier's demand."""
     wl = W.WORKLOADS["llama2-70b"]
@@ -95,8 +102,9 @@ def test_tier_pools_llama70b_layer_at_the_same_budget():
     k, n16, n8 = wl.counts()
     budget = wl.cache_slots() * 6 * wl.d_model
     ts = m2c.pool_slots_for_budget(wl.d_model, {3: n16, 2: n8, 1: k - n16 - n8}, budget)
-    worst, tot = _run(ld, 8, k, n16, n8, ts, "70B pools")
-    say(f"70B pools {ts}: worst FFN error {worst:.2e}, hit rate {tot[1] / tot[0]:.3f}")
+    worst, tot = _run(ld, 8, k, n16, n8, ts, f"70B pools dom {dominance}", dominance)
+    say(f"70B pools {ts} dominance {dominance}: worst FFN error {worst:.2e}, "
+        f"hit rate {tot[1] / tot[0]:.3f}")
 
 
 def test_tier_pools_overflow_leaves_everything_unchanged():
@@ -123,7 +131,7 @@ def test_tier_pools_overflow_leaves_everything_unchanged():
 
 def test_tier_pool_descriptor_checks():
     ld = W.make_layer(18, 0, 256, 300, 16, 1)
-    for kw in ({"flags": m2c.FLAG_DOMINANT_HITS}, {"max_batch": 2}, {"staging_slots": 10}):
+    for kw in ({"flags": m2c.FLAG_DETERMINISTIC_FFN}, {"max_batch": 2}, {"staging_slots": 10}):
         with pytest.raises(m2c.M2CError) as e:
             m2c.Layer(m2c.make_desc(256, 300, 16, 20, 0, tier_slots={3: 5, 2: 5, 1: 5}, **kw), ld)
         assert e.value.status == m2c.M2C_ERR_INVALID_ARG
