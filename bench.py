@@ -50,16 +50,18 @@ def parse_args():
                         "pinned neuron stores (0 = every layer its own weights; -1 = 8 for the "
                         "70B stack, whose 80 stores would take 199 GB of pinned host memory, "
                         "else 0). Every layer keeps its own predictor, inputs and slot cache.")
-    p.add_argument("--policy", choices=("exact", "dominance"), default="exact",
-                   help="cache hits: exact tier (default) or a resident tier at or above the "
-                        "requested one")
+    p.add_argument("--policy", choices=("exact", "dominance"), default="dominance",
+                   help="cache hits: a resident tier at or above the requested one (default; "
+                        "with the per-tier arena, a neuron missing from its tier's pool is served "
+                        "by the lowest higher-precision pool that holds it) or the exact tier")
     p.add_argument("--arena", choices=("pools", "single"), default="pools",
                    help="pools (default): the HBM of the workload's C FP16-sized slots split into "
                         "one pool per tier, each the same multiple of its tier's per-step demand; "
                         "single: C FP16-sized slots shared by every tier")
     p.add_argument("--no-variants", action="store_true",
-                   help="skip the single-arena stacks (exact-tier and dominance hits) reported "
-                        "beside the headline")
+                   help="skip the other policy and arena stacks (per-tier arena with the other "
+                        "policy, single arena with exact-tier and dominance hits) reported beside "
+                        "the headline")
     p.add_argument("--policy-sweep", action="store_true",
                    help="only the cache-policy measurement: hit rates of exact-tier and "
                         "dominance hits, LRU at C = 30%% and at C = k (the ATU regime), against "
@@ -193,7 +195,7 @@ def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy, tier_slots=None):
             cache = oracle.LRUCache(wl.d_ff, C, max(0, cap - C), policy)
         else:
             cache = oracle.TierPoolCache(wl.d_ff, tier_slots,
-                                         {t: max(0, cap - tier_slots[t]) for t in (1, 2, 3)})
+                                         {t: max(0, cap - tier_slots[t]) for t in (1, 2, 3)}, policy)
         t_start = time.perf_counter()
         done = 0
         for t in range(steps_avail):
@@ -888,8 +890,6 @@ def main():
     flags = ffn_flags | (m2c.FLAG_DOMINANT_HITS if args.policy == "dominance" else 0)
     tier_slots = None
     if args.arena == "pools":
-        if args.policy == "dominance":
-            sys.exit("dominance hits need --arena single")
         tier_slots = m2c.pool_slots_for_budget(wl.d_model, {3: n16, 2: n8, 1: n4},
                                                wl.cache_slots() * 6 * wl.d_model)
         log(f"per-tier arena: {tier_slots} resident slots (FP16, INT8, INT4 pools)")
@@ -898,10 +898,16 @@ def main():
     log(f"stack: {r['tokens_per_s']:.2f} tokens/s")
     variants = {}
     if not args.no_variants and tier_slots is not None:
-        for name, fl in (("single_arena_exact_tier", ffn_flags),
-                         ("single_arena_dominance", ffn_flags | m2c.FLAG_DOMINANT_HITS)):
+        # the other cache policies and arenas at the same HBM budget
+        others = [("single_arena_exact_tier", ffn_flags, None),
+                  ("single_arena_dominance", ffn_flags | m2c.FLAG_DOMINANT_HITS, None)]
+        if args.policy == "dominance":
+            others.insert(0, ("pools_exact_tier", ffn_flags, tier_slots))
+        else:
+            others.insert(0, ("pools_dominance", ffn_flags | m2c.FLAG_DOMINANT_HITS, tier_slots))
+        for name, fl, ts in others:
             rv = run_stack(wl, n_layers, args.steps, args.warmup, weight_sets, fl, 0, False, torch,
-                           m2c, W)
+                           m2c, W, tier_slots=ts)
             variants[name] = {"tokens_per_s": rv["tokens_per_s"],
                               "us_per_layer_step": rv["us_per_layer_step"],
                               "host_MB_per_layer_step": rv["pipeline"]["fill_MB_per_layer_step"],
