@@ -654,15 +654,14 @@ __global__ __launch_bounds__(256) void pool_resolve_kernel(const uint8_t* __rest
                                                            const int32_t* __restrict__ slot_of,
                                                            uint8_t* __restrict__ out) {
   for (int n = blockIdx.x * blockDim.x + threadIdx.x; n < d_ff; n += gridDim.x * blockDim.x) {
+    // every load at once (one memory round trip; this kernel runs beside the
+    // fills, whose host reads make each round trip long)
+    const bool r3 = slot_of[n] >= 0, r2 = slot_of[(int64_t)d_ff + n] >= 0,
+               r1 = slot_of[2 * (int64_t)d_ff + n] >= 0;
     int t = 0;
     for (int b = 0; b < B; ++b) t = max(t, (int)tier_map[(int64_t)b * d_ff + n]);
-    if (t >= 1 && t <= 3 && slot_of[(int64_t)(3 - t) * d_ff + n] < 0) {
-      for (int hi = t + 1; hi <= 3; ++hi)
-        if (slot_of[(int64_t)(3 - hi) * d_ff + n] >= 0) {
-          t = hi;
-          break;
-        }
-    }
+    const bool own = t == 3 ? r3 : t == 2 ? r2 : t == 1 ? r1 : true;
+    if (!own) t = (t < 2 && r2) ? 2 : r3 ? 3 : t;
     out[n] = (uint8_t)t;
   }
 }
@@ -716,8 +715,44 @@ __device__ __forceinline__ int lower_bound(const int32_t* a, int n, int v) {
   return lo;
 }
 
-__global__ __launch_bounds__(256) void plan_merge_kernel(PoolPlans pp, PlanPtrs out, SlotMap map,
-                                                          const int32_t* __restrict__ abort_word) {
+// The merged lists are in ascending id order: an entry's position is its
+// position in its pool's list plus its rank (a binary search) in each other
+// pool's list. The pools' id lists are staged in LDS first (one memory round
+// trip for all of them), so the searches cost no further round trips; lists
+// longer than the staging area are searched in global memory.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeIds = 4096;  // ids staged per list kind (required, fills)
+
+// One of three kernel-argument values by a runtime index, as selects of
+// values already in registers (indexing the argument struct would read it
+// from memory).
+template <typename T>
+__device__ __forceinline__ T pick(int q, T a, T b, T c) {
+  return q == 0 ? a : q == 1 ? b : c;
+}
+
+__device__ __forceinline__ void stage_ids(int32_t* __restrict__ dst, const int32_t* s0,
+                                          const int32_t* s1, const int32_t* s2, const int n[3]) {
+  const int tot = n[0] + n[1] + n[2];
+  int32_t v[kMergeIds / kMergeThreads];
+#pragma unroll
+  for (int c = 0; c < kMergeIds / kMergeThreads; ++c) {
+    const int e = c * kMergeThreads + (int)threadIdx.x;
+    const int q = e < n[0] ? 0 : e < n[0] + n[1] ? 1 : 2;
+    const int p = e - (q > 0 ? n[0] : 0) - (q > 1 ? n[1] : 0);
+    v[c] = e < tot ? pick(q, s0, s1, s2)[p] : 0;
+  }
+#pragma unroll
+  for (int c = 0; c < kMergeIds / kMergeThreads; ++c) {
+    const int e = c * kMergeThreads + (int)threadIdx.x;
+    if (e < tot) dst[e] = v[c];
+  }
+}
+
+__global__ __launch_bounds__(kMergeThreads) void plan_merge_kernel(PoolPlans pp, PlanPtrs out,
+                                                                    SlotMap map,
+                                                                    const int32_t* __restrict__ abort_word) {
+  __shared__ int32_t s_req[kMergeIds], s_fill[kMergeIds];
   const bool ab = *abort_word != 0;
   int nr[3], nf[3], ne[3];
 #pragma unroll
@@ -735,47 +770,60 @@ __global__ __launch_bounds__(256) void plan_merge_kernel(PoolPlans pp, PlanPtrs 
       v = pp.p[0].counts[tid] + pp.p[1].counts[tid] + pp.p[2].counts[tid];
     out.counts[tid] = v;
   }
-  const int R = nr[0] + nr[1] + nr[2];
+  const int R = nr[0] + nr[1] + nr[2], NF = nf[0] + nf[1] + nf[2];
+  const bool lr = R <= kMergeIds, lf = NF <= kMergeIds;  // uniform over the grid
+  {
+    if (lr) stage_ids(s_req, pp.p[0].req_ids, pp.p[1].req_ids, pp.p[2].req_ids, nr);
+    if (lf) stage_ids(s_fill, pp.p[0].fill_ids, pp.p[1].fill_ids, pp.p[2].fill_ids, nf);
+    __syncthreads();
+  }
   for (int e = tid; e < R; e += nth) {
     const int q = e < nr[0] ? 0 : e < nr[0] + nr[1] ? 1 : 2;
     const int p = e - (q > 0 ? nr[0] : 0) - (q > 1 ? nr[1] : 0);
-    const PoolPlan& P = pp.p[q];
     const int t = 3 - q;
-    const int id = P.req_ids[p];
+    const int id = lr ? s_req[e] : pick(q, pp.p[0].req_ids, pp.p[1].req_ids, pp.p[2].req_ids)[p];
     int pos = p;
 #pragma unroll
-    for (int u = 0; u < 3; ++u)
-      if (u != q) pos += lower_bound(pp.p[u].req_ids, nr[u], id);
-    const int gs = P.req_slot[p] + map.first[t];
+    for (int u = 0; u < 3; ++u) {
+      if (u == q) continue;
+      const int off = (u > 0 ? nr[0] : 0) + (u > 1 ? nr[1] : 0);
+      pos += lr ? lower_bound(s_req + off, nr[u], id) : lower_bound(pp.p[u].req_ids, nr[u], id);
+    }
+    const int gs = pick(q, pp.p[0].req_slot, pp.p[1].req_slot, pp.p[2].req_slot)[p] +
+                   pick(q, map.first[3], map.first[2], map.first[1]);
+    const uint32_t mk = pick(q, pp.p[0].req_mask, pp.p[1].req_mask, pp.p[2].req_mask)[p];
+    const uint8_t hit = pick(q, pp.p[0].req_hit, pp.p[1].req_hit, pp.p[2].req_hit)[p];
     out.req_ids[pos] = id;
     out.req_tier[pos] = (uint8_t)t;
-    out.req_hit[pos] = P.req_hit[p];
+    out.req_hit[pos] = hit;
     out.req_slot[pos] = gs;
-    out.req_mask[pos] = P.req_mask[p];
+    out.req_mask[pos] = mk;
     out.work_slot[e] = gs;  // pool order = tier-major, ascending id inside a tier
-    out.work_mask[e] = P.req_mask[p];
+    out.work_mask[e] = mk;
   }
-  const int NF = nf[0] + nf[1] + nf[2];
   for (int e = tid; e < NF; e += nth) {
     const int q = e < nf[0] ? 0 : e < nf[0] + nf[1] ? 1 : 2;
     const int p = e - (q > 0 ? nf[0] : 0) - (q > 1 ? nf[1] : 0);
-    const PoolPlan& P = pp.p[q];
     const int t = 3 - q;
-    const int id = P.fill_ids[p];
+    const int id = lf ? s_fill[e] : pick(q, pp.p[0].fill_ids, pp.p[1].fill_ids, pp.p[2].fill_ids)[p];
     int pos = p;
 #pragma unroll
-    for (int u = 0; u < 3; ++u)
-      if (u != q) pos += lower_bound(pp.p[u].fill_ids, nf[u], id);
+    for (int u = 0; u < 3; ++u) {
+      if (u == q) continue;
+      const int off = (u > 0 ? nf[0] : 0) + (u > 1 ? nf[1] : 0);
+      pos += lf ? lower_bound(s_fill + off, nf[u], id) : lower_bound(pp.p[u].fill_ids, nf[u], id);
+    }
     out.fill_ids[pos] = id;
     out.fill_tier[pos] = (uint8_t)t;
-    out.fill_slot[pos] = P.fill_slot[p] + map.first[t];
+    out.fill_slot[pos] = pick(q, pp.p[0].fill_slot, pp.p[1].fill_slot, pp.p[2].fill_slot)[p] +
+                         pick(q, map.first[3], map.first[2], map.first[1]);
     out.fill_from[pos] = 0;
   }
   const int NE = ne[0] + ne[1] + ne[2];
   for (int e = tid; e < NE; e += nth) {
     const int q = e < ne[0] ? 0 : e < ne[0] + ne[1] ? 1 : 2;
     const int p = e - (q > 0 ? ne[0] : 0) - (q > 1 ? ne[1] : 0);
-    out.evicted_ids[e] = pp.p[q].evicted_ids[p];
+    out.evicted_ids[e] = pick(q, pp.p[0].evicted_ids, pp.p[1].evicted_ids, pp.p[2].evicted_ids)[p];
   }
 }
 
@@ -864,9 +912,9 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
                      pool_batch, L->desc.d_ff, L->cap, step, jobs, L->plan_abort);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  int blocks = (L->cap + 255) / 256;
+  int blocks = (L->cap + kMergeThreads - 1) / kMergeThreads;
   blocks = blocks < 1 ? 1 : blocks > 64 ? 64 : blocks;
-  hipLaunchKernelGGL(plan_merge_kernel, dim3(blocks), dim3(256), 0, stream, pp, P, L->map,
+  hipLaunchKernelGGL(plan_merge_kernel, dim3(blocks), dim3(kMergeThreads), 0, stream, pp, P, L->map,
                      L->plan_abort);
   e = hipGetLastError();
   return e == hipSuccess ? launch_ffn_tasks(L, plan, stream) : e;
