@@ -297,6 +297,48 @@ __device__ __forceinline__ int fd3(unsigned long long v, int f) {
 }
 __device__ __forceinline__ int popc(unsigned long long v) { return __popcll(v); }
 
+// Exclusive prefixes of s_a[0..n) and s_b[0..n) (n <= kPlanThreads, one entry
+// of each per thread), in place, sharing the barriers; the totals go to *ta,
+// *tb. tmp: 2 (kPWaves + 1) entries. Contains barriers.
+__device__ void scan_entries2(unsigned long long* s_a, unsigned long long* s_b, int n,
+                              unsigned long long* tmp, unsigned long long* ta,
+                              unsigned long long* tb) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const unsigned long long va = tid < n ? s_a[tid] : 0ull, vb = tid < n ? s_b[tid] : 0ull;
+  unsigned long long ia = va, ib = vb;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const unsigned long long oa = __shfl_up(ia, off), ob = __shfl_up(ib, off);
+    if (lane >= off) {
+      ia += oa;
+      ib += ob;
+    }
+  }
+  if (lane == 63) {
+    tmp[wave] = ia;
+    tmp[kPWaves + 1 + wave] = ib;
+  }
+  __syncthreads();
+  if (tid < 2) {  // thread 0 the first array's wave totals, thread 1 the second's
+    unsigned long long* w = tmp + tid * (kPWaves + 1);
+    unsigned long long run = 0;
+    for (int q = 0; q < kPWaves; ++q) {
+      const unsigned long long t = w[q];
+      w[q] = run;
+      run += t;
+    }
+    w[kPWaves] = run;
+  }
+  __syncthreads();
+  if (tid < n) {
+    s_a[tid] = tmp[wave] + ia - va;
+    s_b[tid] = tmp[kPWaves + 1 + wave] + ib - vb;
+  }
+  *ta = tmp[kPWaves];
+  *tb = tmp[2 * kPWaves + 1];
+  __syncthreads();
+}
+
 // Exclusive prefix of s_v[0..n) (n <= kPlanThreads, one entry per thread), in
 // place; returns the total. Contains barriers.
 template <typename T>
@@ -311,12 +353,14 @@ __device__ T scan_entries(T* s_v, int n, T* tmp) {
 }
 
 // Step tier (max over rows, codes above FP16 read as FP16) and row mask of
-// neuron i.
+// neuron i. ONE_ROW: B is 1 (a separate instantiation, so that no branch
+// join forces a wait for the load).
+template <bool ONE_ROW>
 __device__ __forceinline__ void neuron_tiers(const uint8_t* __restrict__ tm, int d_ff, int i,
                                              int B, int& t, uint32_t& m) {
   t = 0;
   m = 0;
-  if (B == 1) {
+  if (ONE_ROW) {
     const int v = tm[i];
     t = v;
     m = v ? 1u : 0u;
@@ -342,17 +386,41 @@ __device__ __forceinline__ void neuron_tiers(const uint8_t* __restrict__ tm, int
 // workgroup checks the whole required set against cap, so all of them leave
 // their pool unchanged together when it does not fit; the FP16 pool's
 // workgroup reports it (status word, and *abort for the merge).
+//
+// Memory round trips are what a one-workgroup plan waits on, so each neuron's
+// slot and resident tier are kept in LDS from the first sweep to the second
+// (with one batch row the second sweep reads no global memory), and the LRU
+// order read for the victim count is kept for the victim pass. A pool's
+// slots hold records of its own tier only, so a resident neuron of a pool is
+// a hit without reading the slot's tier.
+// The plan's LDS (one per kernel, shared by the body's instantiations).
+struct PlanLds {
+  // tier | code << 2 (1 hit, 2 refill, 0 new) | resident tier << 4
+  uint8_t info[kPJ * kPlanThreads];
+  // per thread-owned index i = tid + kPlanThreads j: the slot of resident
+  // neuron i (sweeps A1, A2), then position i of the LRU order (C)
+  uint16_t sl[kPJ * kPlanThreads];
+  uint32_t touch[kPJ * kPlanThreads / 32];  // slots touched this step
+  unsigned long long ca[kPJ * kPWaves];     // R, NEW, fills per (chunk, wave)
+  unsigned long long cb[kPJ * kPWaves];     // FP16, INT8, INT4 per (chunk, wave)
+  uint32_t cu[kPJ * kPWaves];               // slot compactions per (chunk, wave)
+  unsigned long long scan64[2 * (kPWaves + 1)];
+  uint32_t scan32[kPWaves + 1];
+  int hit, refill, empty, all, f[4], der[2];
+};
+
+template <bool ONE_ROW>
 __device__ __forceinline__ void plan_fast_body(
     const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step, int dom,
-    const DeviceState& st, const PlanPtrs& P, int pool_tier, int32_t* __restrict__ abort_word) {
-  __shared__ uint8_t s_info[kPJ * kPlanThreads];  // tier | code << 2 (1 hit, 2 refill, 0 new)
-  __shared__ uint32_t s_touch[kPJ * kPlanThreads / 32];  // slots touched this step
-  __shared__ unsigned long long s_ca[kPJ * kPWaves];  // R, NEW, fills per (chunk, wave)
-  __shared__ unsigned long long s_cb[kPJ * kPWaves];  // FP16, INT8, INT4 per (chunk, wave)
-  __shared__ uint32_t s_cu[kPJ * kPWaves];            // slot compactions per (chunk, wave)
-  __shared__ unsigned long long scan64[kPWaves + 1];
-  __shared__ uint32_t scan32[kPWaves + 1];
-  __shared__ int sh_hit, sh_refill, sh_empty, sh_f[4], sh_der[2], sh_all;
+    const DeviceState& st, const PlanPtrs& P, int pool_tier, int32_t* __restrict__ abort_word,
+    PlanLds& sm) {
+  uint8_t* s_info = sm.info;
+  uint16_t* s_sl = sm.sl;
+  uint32_t* s_touch = sm.touch;
+  unsigned long long *s_ca = sm.ca, *s_cb = sm.cb, *scan64 = sm.scan64;
+  uint32_t *s_cu = sm.cu, *scan32 = sm.scan32;
+  int &sh_hit = sm.hit, &sh_refill = sm.refill, &sh_empty = sm.empty, &sh_all = sm.all;
+  int *sh_f = sm.f, *sh_der = sm.der;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const unsigned long long lt = (1ull << lane) - 1ull;
   const int NJ = (d_ff + kPlanThreads - 1) / kPlanThreads;
@@ -366,24 +434,27 @@ __device__ __forceinline__ void plan_fast_body(
   for (int w = tid; w < (C + 31) / 32; w += kPlanThreads) s_touch[w] = 0;
   __syncthreads();
   // ---------------- A1: classify and count (reads only)
+  // every load of a group is issued before the first value is used; the
+  // wave's counts stay in registers until the end of the sweep
+  int c_all = 0, c_hit = 0, c_ref = 0;
   for (int j0 = 0; j0 < NJ; j0 += kPGroup) {
     int t[kPGroup], sl[kPGroup];
     uint32_t m[kPGroup];
 #pragma unroll
     for (int g = 0; g < kPGroup; ++g) {
       const int i = min(tid + kPlanThreads * (j0 + g), d_ff - 1);
-      neuron_tiers(tier_map, d_ff, i, B, t[g], m[g]);
-      if (pool_tier) {  // the whole required set, for the capacity check
-        const unsigned long long ba = __ballot(j0 + g < NJ && tid + kPlanThreads * (j0 + g) < d_ff &&
-                                               t[g] > 0);
-        if (lane == 0 && ba) atomicAdd(&sh_all, popc(ba));
-      }
-      if (pool_tier && t[g] != pool_tier) t[g] = 0;  // another pool's neuron
+      neuron_tiers<ONE_ROW>(tier_map, d_ff, i, B, t[g], m[g]);
       sl[g] = st.slot_of[i];
     }
     int old[kPGroup];
 #pragma unroll
-    for (int g = 0; g < kPGroup; ++g) old[g] = sl[g] >= 0 ? st.slot_tier[sl[g]] : 0;
+    for (int g = 0; g < kPGroup; ++g) {
+      if (pool_tier) {  // the whole required set, for the capacity check
+        c_all += popc(__ballot(j0 + g < NJ && tid + kPlanThreads * (j0 + g) < d_ff && t[g] > 0));
+        if (t[g] != pool_tier) t[g] = 0;  // another pool's neuron
+      }
+      old[g] = sl[g] < 0 ? 0 : pool_tier ? pool_tier : st.slot_tier[sl[g]];
+    }
 #pragma unroll
     for (int g = 0; g < kPGroup; ++g) {
       const int j = j0 + g, i = tid + kPlanThreads * j;
@@ -392,7 +463,8 @@ __device__ __forceinline__ void plan_fast_body(
       const bool res = req && sl[g] >= 0;
       const bool hit = res && (old[g] == t[g] || (dom && old[g] > t[g]));
       if (hit) t[g] = old[g];  // the step tier of a hit is the resident tier
-      if (valid) s_info[i] = req ? (uint8_t)(t[g] | ((hit ? 1 : res ? 2 : 0) << 2)) : 0;
+      if (valid) s_info[i] = req ? (uint8_t)(t[g] | ((hit ? 1 : res ? 2 : 0) << 2) | (old[g] << 4)) : 0;
+      if (res) s_sl[i] = (uint16_t)sl[g];
       if (res) atomicOr(&s_touch[sl[g] >> 5], 1u << (sl[g] & 31));
       const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
                                b2 = __ballot(req && !hit), b3 = __ballot(req && t[g] == 3),
@@ -401,14 +473,19 @@ __device__ __forceinline__ void plan_fast_body(
       if (lane == 0 && j < NJ) {
         s_ca[j * kPWaves + wave] = pk3(popc(b0), popc(b1), popc(b2));
         s_cb[j * kPWaves + wave] = pk3(popc(b3), popc(b4), popc(b5));
-        if (bh) atomicAdd(&sh_hit, popc(bh));
-        if (br) atomicAdd(&sh_refill, popc(br));
       }
+      c_hit += popc(bh);
+      c_ref += popc(br);
     }
   }
+  if (lane == 0) {
+    if (c_all) atomicAdd(&sh_all, c_all);
+    if (c_hit) atomicAdd(&sh_hit, c_hit);
+    if (c_ref) atomicAdd(&sh_refill, c_ref);
+  }
   __syncthreads();
-  const unsigned long long totA = scan_entries<unsigned long long>(s_ca, NJ * kPWaves, scan64);
-  const unsigned long long totB = scan_entries<unsigned long long>(s_cb, NJ * kPWaves, scan64);
+  unsigned long long totA, totB;
+  scan_entries2(s_ca, s_cb, NJ * kPWaves, scan64, &totA, &totB);
   const int NREQ = fd3(totA, 0), NNEW = fd3(totA, 1), NF = fd3(totA, 2);
   const int N3 = fd3(totB, 0), N2 = fd3(totB, 1), N1 = fd3(totB, 2);
   const int NALL = pool_tier ? sh_all : NREQ;  // sh_all is final after the scans' barriers
@@ -424,21 +501,21 @@ __device__ __forceinline__ void plan_fast_body(
   if (pool_tier == 3 && tid == 0) *abort_word = 0;
   // ---------------- A2: required list, NEW list, fill ids, work positions
   for (int j0 = 0; j0 < NJ; j0 += kPGroup) {
-    int sl[kPGroup];
     uint32_t m[kPGroup];
 #pragma unroll
     for (int g = 0; g < kPGroup; ++g) {
-      const int i = min(tid + kPlanThreads * (j0 + g), d_ff - 1);
-      int tt;
-      neuron_tiers(tier_map, d_ff, i, B, tt, m[g]);
-      sl[g] = st.slot_of[i];
+      m[g] = 1u;  // one batch row: every required neuron's row mask
+      if (!ONE_ROW) {
+        int tt;
+        neuron_tiers<ONE_ROW>(tier_map, d_ff, min(tid + kPlanThreads * (j0 + g), d_ff - 1), B, tt, m[g]);
+      }
     }
 #pragma unroll
     for (int g = 0; g < kPGroup; ++g) {
       const int j = j0 + g, i = tid + kPlanThreads * j;
       const bool valid = j < NJ && i < d_ff;
       const int info = valid ? s_info[i] : 0;
-      const int t = info & 3, code = info >> 2;
+      const int t = info & 3, code = (info >> 2) & 3;
       const bool req = t > 0, res = code != 0, hit = code == 1;
       const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
                                b2 = __ballot(req && !hit), b3 = __ballot(req && t == 3),
@@ -455,11 +532,12 @@ __device__ __forceinline__ void plan_fast_body(
       st.work_pos[pos] = wp;
       int from = 0;
       if (res) {
-        P.req_slot[pos] = sl[g];
+        const int sl = s_sl[i];
+        P.req_slot[pos] = sl;
         P.req_hit[pos] = hit ? 1 : 2;
-        st.slot_last[sl[g]] = step;
-        from = st.slot_tier[sl[g]];
-        if (!hit) st.slot_tier[sl[g]] = (uint8_t)t;
+        st.slot_last[sl] = step;
+        from = info >> 4;
+        if (!hit) st.slot_tier[sl] = (uint8_t)t;
       } else {
         st.new_pos[fd3(pa, 1) + popc(b1 & lt)] = pos;
       }
@@ -487,6 +565,7 @@ __device__ __forceinline__ void plan_fast_body(
     for (int g = 0; g < kPGroup; ++g) {
       const int j = j0 + g;
       const bool valid = j < NC && tid + kPlanThreads * j < C;
+      if (valid) s_sl[tid + kPlanThreads * j] = (uint16_t)sv[g];
       const bool unt = valid && !((s_touch[sv[g] >> 5] >> (sv[g] & 31)) & 1u);
       const unsigned long long bu = __ballot(unt);
       if (lane == 0 && j < NC) s_cu[j * kPWaves + wave] = (uint32_t)popc(bu);
@@ -500,7 +579,8 @@ __device__ __forceinline__ void plan_fast_body(
     for (int j0 = 0; j0 < NC; j0 += kPGroup) {
       int sv[kPGroup];
 #pragma unroll
-      for (int g = 0; g < kPGroup; ++g) sv[g] = lru_in[min(tid + kPlanThreads * (j0 + g), C - 1)];
+      for (int g = 0; g < kPGroup; ++g)
+        sv[g] = s_sl[min(tid + kPlanThreads * (j0 + g), kPJ * kPlanThreads - 1)];
 #pragma unroll
       for (int g = 0; g < kPGroup; ++g) {
         const int j = j0 + g;
@@ -624,7 +704,11 @@ __device__ __forceinline__ void plan_fast_body(
 __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
     const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step, int dom,
     DeviceState st, PlanPtrs P, int32_t* __restrict__ abort_word) {
-  plan_fast_body(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word);
+  __shared__ PlanLds sm;
+  if (B == 1)
+    plan_fast_body<true>(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word, sm);
+  else
+    plan_fast_body<false>(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word, sm);
 }
 
 // Per-tier arena: workgroup q plans pool 3 - q (FP16, INT8, INT4) into its
@@ -639,8 +723,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_pools_kernel(
     const uint8_t* __restrict__ tier_map, int B, int d_ff, int cap, int step, PoolJobs jobs,
     int32_t* __restrict__ abort_word) {
   const int q = blockIdx.x;
-  plan_fast_body(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q], 3 - q,
-                 abort_word);
+  __shared__ PlanLds sm;
+  if (B == 1)
+    plan_fast_body<true>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q], 3 - q,
+                         abort_word, sm);
+  else
+    plan_fast_body<false>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q],
+                          3 - q, abort_word, sm);
 }
 
 // Per-tier arena with dominance hits: the pool that serves each neuron this
