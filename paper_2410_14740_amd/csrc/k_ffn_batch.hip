@@ -99,74 +99,94 @@ __device__ __forceinline__ void bh_tile(int b, int n3, int n2, int n1, int& tier
   }
 }
 
-// A operand of one group: lane (row r, lane group j) holds the 32 codes at
-// positions [32j, 32j + 32) of the group, for the gate and the up row.
+// One group (128 columns) of a tile on the matrix cores, as four
+// v_mfma_f32_16x16x32_f16 steps per row kind (gate, up). Lane (row r, lane
+// group j) supplies 8 codes of neuron row r per step; which 8 of the group's
+// 128 columns a (j, step) pair takes is chosen per tier so that every 16-byte
+// record load of a wave covers 64 contiguous bytes of each of its rows:
+//
+//   FP16  load e = step e:            columns 32 s + 8 j .. + 8
+//   INT8  load e = steps 2e, 2e + 1:  columns 64 (s >> 1) + 16 j + 8 (s & 1) .. + 8
+//   INT4  one load, word s = step s:  columns 32 j + 8 s .. + 8
+//
+// The B operand (x of the lane's batch column, same 8 columns) is read from
+// the wave's copy of the group's x rows in LDS, so both operands pair the
+// same columns whatever the mapping.
+typedef _Float16 half8v __attribute__((ext_vector_type(8)));
+constexpr int kBXRow = 136;  // halves per staged x row: 128 and a pad against bank conflicts
+// halves per row of the staged gate and up scales (2 G, padded to 16 bytes)
+__host__ __device__ constexpr int bh_scale_row(int G) { return 8 * ((G + 3) / 4); }
+
+__device__ __forceinline__ half8v h8(half4v lo, half4v hi) {
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+template <int TIER>
+__host__ __device__ constexpr int bh_xcol(int j, int s) {
+  return TIER == 3 ? 32 * s + 8 * j : TIER == 2 ? 64 * (s >> 1) + 16 * j + 8 * (s & 1) : 32 * j + 8 * s;
+}
+
 template <int TIER>
 struct GroupA {
   static constexpr int NV = TIER == 3 ? 4 : TIER == 2 ? 2 : 1;  // 16-byte loads per row
   uint4 g[NV], u[NV];
   __device__ __forceinline__ void load(const uint8_t* rec, int d, int grp, int j) {
     const int64_t row = TIER == 3 ? 2 * (int64_t)d : TIER == 2 ? d : (d >> 1);
-    // byte offset of element 128 grp + 32 j in a row
-    const int64_t off = TIER == 3 ? 2 * (int64_t)(128 * grp + 32 * j)
-                        : TIER == 2 ? (int64_t)(128 * grp + 32 * j)
-                                    : (int64_t)((128 * grp + 32 * j) >> 1);
 #pragma unroll
     for (int e = 0; e < NV; ++e) {
-      g[e] = *reinterpret_cast<const uint4*>(rec + off + 16 * e);
-      u[e] = *reinterpret_cast<const uint4*>(rec + row + off + 16 * e);
+      const int64_t off = TIER == 3   ? 256 * (int64_t)grp + 64 * e + 16 * j
+                          : TIER == 2 ? 128 * (int64_t)grp + 64 * e + 16 * j
+                                      : 64 * (int64_t)grp + 16 * j;
+      g[e] = *reinterpret_cast<const uint4*>(rec + off);
+      u[e] = *reinterpret_cast<const uint4*>(rec + row + off);
     }
   }
-  // codes [4s, 4s + 4) of the lane's 32
-  __device__ __forceinline__ static half4v step(const uint4 (&v)[NV], int s) {
+  // the 8 codes of step s, as exact fp16 values
+  __device__ __forceinline__ static half8v step(const uint4 (&v)[NV], int s) {
     if (TIER == 3) {
-      const uint4 c = v[s >> 1];  // 8 halves per 16 bytes: steps 2q, 2q + 1 in chunk q
-      return (s & 1) ? h4(c.z, c.w) : h4(c.x, c.y);
+      return __builtin_bit_cast(half8v, v[s]);
     } else if (TIER == 2) {
-      const uint4 c = v[s >> 2];  // 16 codes per 16 bytes: 4 steps per chunk
-      const uint32_t w = (s & 3) == 0 ? c.x : (s & 3) == 1 ? c.y : (s & 3) == 2 ? c.z : c.w;
-      return i8x4_to_h4(w);
+      const uint4 c = v[s >> 1];
+      return (s & 1) ? h8(i8x4_to_h4(c.z), i8x4_to_h4(c.w)) : h8(i8x4_to_h4(c.x), i8x4_to_h4(c.y));
     } else {
-      const uint4 c = v[0];  // 32 codes: 8 steps, 4 codes (16 bits) each
-      const uint32_t w = (s >> 1) == 0 ? c.x : (s >> 1) == 1 ? c.y : (s >> 1) == 2 ? c.z : c.w;
-      return i4x4_to_h4((s & 1) ? (w >> 16) : (w & 0xffffu));
+      const uint4 c = v[0];
+      const uint32_t w = s == 0 ? c.x : s == 1 ? c.y : s == 2 ? c.z : c.w;
+      return h8(i4x4_to_h4(w & 0xffffu), i4x4_to_h4(w >> 16));
     }
   }
 };
 
-// NT: 16-column tiles of the batch (1 for B <= 16, 2 for B <= 32). Pairs of
-// groups with both groups' loads in flight measured slower: they need more
-// than 128 VGPRs, one workgroup per CU.
+// NT: 16-column tiles of the batch (1 for B <= 16, 2 for B <= 32). s_xw: this
+// wave's x rows (16 NT of kBXRow halves; rows past the batch get zeros).
+// s_sc: the tile's gate and up group scales, [16][bh_scale_row(G)] halves.
 template <int TIER, int NT>
 __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, const uint16_t* x,
-                                        const uint16_t* zero_row, const uint8_t* rec,
-                                        const uint8_t* const (&srec)[4], float4v (&acc_g)[NT],
-                                        float4v (&acc_u)[NT]) {
+                                        const uint8_t* rec, uint16_t* s_xw, const uint16_t* s_sc,
+                                        float4v (&acc_g)[NT], float4v (&acc_u)[NT]) {
   const int j = lane >> 4, col = lane & 15;
-  // scales of the lane's result rows 4j + i, read with the group's codes
-  const int64_t sbase = TIER == 1 ? 3 * (int64_t)(d >> 1) : 3 * (int64_t)d;
   for (int grp = w; grp < G; grp += kBHWaves) {
-    // every load of the group is issued before the first use
-    uint32_t sgu[4][2];
-    if (TIER != 3) {
+    // every global load of the group is issued before the first use, none
+    // under a branch: x rows (row 4 q + j, 16-byte chunk col; rows past the
+    // batch re-read the last row and are stored as zeros) and the records
+    uint4 xr[4 * NT];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sgu[i][0] = *reinterpret_cast<const uint16_t*>(srec[i] + sbase + 2 * (int64_t)grp);
-        sgu[i][1] = *reinterpret_cast<const uint16_t*>(srec[i] + sbase + 2 * (int64_t)(G + grp));
-      }
-    }
-    uint4 xv[NT][4];  // x[n][128 grp + 32 j .. + 32] for the lane's batch column n
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int n = 16 * t + col;
-      const uint16_t* xr = n < B ? x + (int64_t)n * d : zero_row;
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        xv[t][e] = *reinterpret_cast<const uint4*>(xr + 128 * grp + 32 * j + 8 * e);
+    for (int q = 0; q < 4 * NT; ++q) {
+      const int row = min(4 * q + j, B - 1);
+      xr[q] = *reinterpret_cast<const uint4*>(x + (int64_t)row * d + 128 * grp + 8 * col);
     }
     GroupA<TIER> A;
     A.load(rec, d, grp, j);
-    __builtin_amdgcn_sched_barrier(0);
+    // (the x values are used here whatever the row, so that the compiler
+    // does not move the loads of rows past the batch under a branch)
+#pragma unroll
+    for (int q = 0; q < 4 * NT; ++q)
+      asm volatile("" : "+v"(xr[q].x), "+v"(xr[q].y), "+v"(xr[q].z), "+v"(xr[q].w));
+#pragma unroll
+    for (int q = 0; q < 4 * NT; ++q) {
+      const int row = 4 * q + j;
+      const uint4 v = row < B ? xr[q] : make_uint4(0u, 0u, 0u, 0u);
+      *reinterpret_cast<uint4*>(s_xw + row * kBXRow + 8 * col) = v;
+    }
     float4v tg[NT], tu[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -174,14 +194,14 @@ __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, co
       tu[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
     }
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      const half4v ag = GroupA<TIER>::step(A.g, s), au = GroupA<TIER>::step(A.u, s);
+    for (int s = 0; s < 4; ++s) {
+      const half8v ag = GroupA<TIER>::step(A.g, s), au = GroupA<TIER>::step(A.u, s);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const uint4 c = xv[t][s >> 1];
-        const half4v bx = (s & 1) ? h4(c.z, c.w) : h4(c.x, c.y);
-        tg[t] = __builtin_amdgcn_mfma_f32_16x16x16f16(ag, bx, tg[t], 0, 0, 0);
-        tu[t] = __builtin_amdgcn_mfma_f32_16x16x16f16(au, bx, tu[t], 0, 0, 0);
+        const half8v bx = *reinterpret_cast<const half8v*>(s_xw + (16 * t + col) * kBXRow +
+                                                            bh_xcol<TIER>(j, s));
+        tg[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ag, bx, tg[t], 0, 0, 0);
+        tu[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(au, bx, tu[t], 0, 0, 0);
       }
     }
     // rows 4j + i of the result: scale each by its neuron's group scale
@@ -189,8 +209,8 @@ __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, co
     for (int i = 0; i < 4; ++i) {
       float sg = 1.0f, su = 1.0f;
       if (TIER != 3) {
-        sg = h2f((uint16_t)sgu[i][0]);
-        su = h2f((uint16_t)sgu[i][1]);
+        sg = h2f(s_sc[(4 * j + i) * bh_scale_row(G) + grp]);
+        su = h2f(s_sc[(4 * j + i) * bh_scale_row(G) + G + grp]);
       }
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
@@ -201,13 +221,22 @@ __device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, co
   }
 }
 
+// LDS of ffn_bh_kernel: the waves' x rows, then (after the main loop, over
+// the same bytes) the waves' partial results; the tile's gate and up scales
+// follow, [16][bh_scale_row(G)] halves (rows padded to 16 bytes; G <= 128).
+template <int NT>
+__host__ __device__ constexpr int bh_lds_words() {
+  return (kBHWaves * 16 * NT * kBXRow * 2 + 16 * bh_scale_row(128) * 2) / 16;
+}
+static_assert(kBHWaves * 2 * 16 * 16 * 4 <= kBHWaves * 16 * kBXRow * 2, "partials fit over the x rows");
+
 template <int NT>
 __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     const uint16_t* __restrict__ x, int d, int B, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ work_slot, const uint32_t* __restrict__ work_mask,
     const uint8_t* __restrict__ slots, int64_t slot_bytes, int cap, int n_slots,
     float* __restrict__ hB) {
-  extern __shared__ float s_part[];  // [waves][2][16][16 NT]
+  __shared__ uint4 bh_lds[bh_lds_words<NT>()];
   __shared__ uint32_t s_mask[16];
   int n3, n2, n1;
   work_counts(counts, cap, n3, n2, n1);
@@ -217,6 +246,9 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
   const int G = d >> 7;
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint16_t* s_x = reinterpret_cast<uint16_t*>(bh_lds);
+  uint16_t* s_xw = s_x + w * 16 * NT * kBXRow;
+  uint16_t* s_sc = s_x + kBHWaves * 16 * NT * kBXRow;
   // The tile's slot ids by scalar loads (a wave-uniform range, inside the
   // plan's spare work_slot entries past the list), which do not queue behind
   // other workgroups' vector loads; each lane then picks the ids it needs with
@@ -232,12 +264,20 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
   for (int k = 0; k < 16; ++k) my_slot |= u[k] & -((lane & 15) == k);
   const uint32_t my_mask = work_mask[min(item0 + (lane & 15), cap - 1)];  // stored after the main loop
   const uint8_t* rec = slots + (int64_t)my_slot * slot_bytes;
-  const uint8_t* srec[4];
-  const int q = lane >> 4, mq0 = -(q == 0), mq1 = -(q == 1), mq2 = -(q == 2), mq3 = -(q == 3);
+  // the tile's gate and up scales (4 G contiguous bytes per record) into LDS
+  if (tier != 3) {
+    const int cpr = bh_scale_row(G) / 8;  // 16-byte chunks per row (the last may pass 4 G bytes)
+    const int r = threadIdx.x / cpr, c = threadIdx.x - r * cpr;
+    if (r < 16) {
+      int sr = 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    srec[i] = slots + (int64_t)((u[i] & mq0) | (u[4 + i] & mq1) | (u[8 + i] & mq2) | (u[12 + i] & mq3)) * slot_bytes;
-  const uint16_t* zero_row = reinterpret_cast<const uint16_t*>(slots + (int64_t)n_slots * slot_bytes);
+      for (int k = 0; k < 16; ++k) sr |= u[k] & -(r == k);
+      const int64_t sbase = tier == 1 ? 3 * (int64_t)(d >> 1) : 3 * (int64_t)d;
+      reinterpret_cast<uint4*>(s_sc)[r * cpr + c] =
+          *reinterpret_cast<const uint4*>(slots + (int64_t)sr * slot_bytes + sbase + 16 * c);
+    }
+  }
+  __syncthreads();
   float4v acc_g[NT], acc_u[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
@@ -245,13 +285,15 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     acc_u[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
   }
   if (tier == 3)
-    bh_tier<3, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
+    bh_tier<3, NT>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
   else if (tier == 2)
-    bh_tier<2, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
+    bh_tier<2, NT>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
   else
-    bh_tier<1, NT>(lane, w, d, G, B, x, zero_row, rec, srec, acc_g, acc_u);
+    bh_tier<1, NT>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
   if (threadIdx.x < 16) s_mask[threadIdx.x] = my_slot < n_slots ? my_mask : 0u;
+  __syncthreads();  // every wave is done with its x rows: the partials take their bytes
   // partials of the waves -> LDS: [w][gate/up][row][col]
+  float* s_part = reinterpret_cast<float*>(bh_lds);
   const int j = lane >> 4, col = lane & 15;
   constexpr int NC = 16 * NT;
 #pragma unroll
@@ -628,12 +670,10 @@ hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const ui
   // tiles of 8 (FP16) and 16 items: at most ceil(cap/8) + 2 for any split into tiers
   const int tiles = (cap + 7) / 8 + 2;
   if (batch <= 16) {
-    const size_t lds = (size_t)kBHWaves * 2 * 16 * 16 * 4;
-    hipLaunchKernelGGL(ffn_bh_kernel<1>, dim3(tiles), dim3(kBHThreads), lds, stream, x, d, batch,
+    hipLaunchKernelGGL(ffn_bh_kernel<1>, dim3(tiles), dim3(kBHThreads), 0, stream, x, d, batch,
                        counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
   } else {
-    const size_t lds = (size_t)kBHWaves * 2 * 16 * 32 * 4;
-    hipLaunchKernelGGL(ffn_bh_kernel<2>, dim3(tiles), dim3(kBHThreads), lds, stream, x, d, batch,
+    hipLaunchKernelGGL(ffn_bh_kernel<2>, dim3(tiles), dim3(kBHThreads), 0, stream, x, d, batch,
                        counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
   }
   hipError_t e = hipGetLastError();
