@@ -156,68 +156,106 @@ struct GroupA {
   }
 };
 
-// NT: 16-column tiles of the batch (1 for B <= 16, 2 for B <= 32). s_xw: this
-// wave's x rows (16 NT of kBXRow halves; rows past the batch get zeros).
-// s_sc: the tile's gate and up group scales, [16][bh_scale_row(G)] halves.
-template <int TIER, int NT>
-__device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, const uint16_t* x,
-                                        const uint8_t* rec, uint16_t* s_xw, const uint16_t* s_sc,
-                                        float4v (&acc_g)[NT], float4v (&acc_u)[NT]) {
-  const int j = lane >> 4, col = lane & 15;
-  for (int grp = w; grp < G; grp += kBHWaves) {
-    // every global load of the group is issued before the first use, none
-    // under a branch: x rows (row 4 q + j, 16-byte chunk col; rows past the
-    // batch re-read the last row and are stored as zeros) and the records
-    uint4 xr[4 * NT];
+// The global loads of one group: x rows 4 q + j (q < NXQ; 16-byte chunk
+// col; rows past the batch re-read the last row, and are stored as zeros)
+// and the records. Every load is unconditional.
+template <int TIER, int NXQ>
+struct BhLoads {
+  GroupA<TIER> A;
+  uint4 xr[NXQ];
+  __device__ __forceinline__ void issue(const uint16_t* x, const uint8_t* rec, int d, int B,
+                                        int grp, int lane) {
+    const int j = lane >> 4, col = lane & 15;
 #pragma unroll
-    for (int q = 0; q < 4 * NT; ++q) {
+    for (int q = 0; q < NXQ; ++q) {
       const int row = min(4 * q + j, B - 1);
       xr[q] = *reinterpret_cast<const uint4*>(x + (int64_t)row * d + 128 * grp + 8 * col);
     }
-    GroupA<TIER> A;
     A.load(rec, d, grp, j);
-    // (the x values are used here whatever the row, so that the compiler
-    // does not move the loads of rows past the batch under a branch)
+  }
+  // the x rows into the wave's LDS copy (the asm makes the values used
+  // whatever the row, so that no load of a row past the batch moves under
+  // a branch)
+  __device__ __forceinline__ void stage(uint16_t* s_xw, int B, int lane) {
+    const int j = lane >> 4, col = lane & 15;
 #pragma unroll
-    for (int q = 0; q < 4 * NT; ++q)
+    for (int q = 0; q < NXQ; ++q)
       asm volatile("" : "+v"(xr[q].x), "+v"(xr[q].y), "+v"(xr[q].z), "+v"(xr[q].w));
 #pragma unroll
-    for (int q = 0; q < 4 * NT; ++q) {
+    for (int q = 0; q < NXQ; ++q) {
       const int row = 4 * q + j;
-      const uint4 v = row < B ? xr[q] : make_uint4(0u, 0u, 0u, 0u);
-      *reinterpret_cast<uint4*>(s_xw + row * kBXRow + 8 * col) = v;
+      *reinterpret_cast<uint4*>(s_xw + row * kBXRow + 8 * col) =
+          row < B ? xr[q] : make_uint4(0u, 0u, 0u, 0u);
     }
-    float4v tg[NT], tu[NT];
+  }
+};
+
+// The arithmetic of one group, x staged in s_xw.
+template <int TIER, int NT>
+__device__ __forceinline__ void bh_compute(const GroupA<TIER>& A, const uint16_t* s_xw,
+                                           const uint16_t* s_sc, int G, int grp, int lane,
+                                           float4v (&acc_g)[NT], float4v (&acc_u)[NT]) {
+  const int j = lane >> 4, col = lane & 15;
+  float4v tg[NT], tu[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    tg[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+    tu[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const half8v ag = GroupA<TIER>::step(A.g, s), au = GroupA<TIER>::step(A.u, s);
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      tg[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
-      tu[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+      const half8v bx = *reinterpret_cast<const half8v*>(s_xw + (16 * t + col) * kBXRow +
+                                                          bh_xcol<TIER>(j, s));
+      tg[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ag, bx, tg[t], 0, 0, 0);
+      tu[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(au, bx, tu[t], 0, 0, 0);
+    }
+  }
+  // rows 4j + i of the result: scale each by its neuron's group scale
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float sg = 1.0f, su = 1.0f;
+    if (TIER != 3) {
+      sg = h2f(s_sc[(4 * j + i) * bh_scale_row(G) + grp]);
+      su = h2f(s_sc[(4 * j + i) * bh_scale_row(G) + G + grp]);
     }
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const half8v ag = GroupA<TIER>::step(A.g, s), au = GroupA<TIER>::step(A.u, s);
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const half8v bx = *reinterpret_cast<const half8v*>(s_xw + (16 * t + col) * kBXRow +
-                                                            bh_xcol<TIER>(j, s));
-        tg[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ag, bx, tg[t], 0, 0, 0);
-        tu[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(au, bx, tu[t], 0, 0, 0);
-      }
+    for (int t = 0; t < NT; ++t) {
+      acc_g[t][i] = fmaf(sg, tg[t][i], acc_g[t][i]);
+      acc_u[t][i] = fmaf(su, tu[t][i], acc_u[t][i]);
     }
-    // rows 4j + i of the result: scale each by its neuron's group scale
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float sg = 1.0f, su = 1.0f;
-      if (TIER != 3) {
-        sg = h2f(s_sc[(4 * j + i) * bh_scale_row(G) + grp]);
-        su = h2f(s_sc[(4 * j + i) * bh_scale_row(G) + G + grp]);
-      }
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        acc_g[t][i] = fmaf(sg, tg[t][i], acc_g[t][i]);
-        acc_u[t][i] = fmaf(su, tu[t][i], acc_u[t][i]);
-      }
-    }
+  }
+}
+
+// NT: 16-column tiles of the batch (1 for B <= 16, 2 for B <= 32); NXQ: x
+// loads per lane and group (4 NXQ >= B). s_xw: this wave's x rows (16 NT of
+// kBXRow halves; rows from 4 NXQ on are zero from the start). s_sc: the
+// tile's gate and up group scales, [16][bh_scale_row(G)] halves. The wave's
+// groups are w, w + 8, ...; the loads of the next one go out before the
+// current one's arithmetic (past the last group the prefetch re-reads the
+// current one, which keeps every load unconditional).
+template <int TIER, int NT, int NXQ>
+__device__ __forceinline__ void bh_tier(int lane, int w, int d, int G, int B, const uint16_t* x,
+                                        const uint8_t* rec, uint16_t* s_xw, const uint16_t* s_sc,
+                                        float4v (&acc_g)[NT], float4v (&acc_u)[NT]) {
+  int grp = w;
+  if (grp >= G) return;  // wave-uniform
+  BhLoads<TIER, NXQ> L0, L1;
+  L0.issue(x, rec, d, B, grp, lane);
+  for (;;) {
+    const int g1 = grp + kBHWaves;
+    L1.issue(x, rec, d, B, g1 < G ? g1 : grp, lane);
+    L0.stage(s_xw, B, lane);
+    bh_compute<TIER, NT>(L0.A, s_xw, s_sc, G, grp, lane, acc_g, acc_u);
+    if (g1 >= G) break;
+    const int g2 = g1 + kBHWaves;
+    L0.issue(x, rec, d, B, g2 < G ? g2 : g1, lane);
+    L1.stage(s_xw, B, lane);
+    bh_compute<TIER, NT>(L1.A, s_xw, s_sc, G, g1, lane, acc_g, acc_u);
+    if (g2 >= G) break;
+    grp = g2;
   }
 }
 
@@ -230,7 +268,7 @@ __host__ __device__ constexpr int bh_lds_words() {
 }
 static_assert(kBHWaves * 2 * 16 * 16 * 4 <= kBHWaves * 16 * kBXRow * 2, "partials fit over the x rows");
 
-template <int NT>
+template <int NT, int NXQ>
 __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     const uint16_t* __restrict__ x, int d, int B, const int32_t* __restrict__ counts,
     const int32_t* __restrict__ work_slot, const uint32_t* __restrict__ work_mask,
@@ -277,6 +315,9 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
           *reinterpret_cast<const uint4*>(slots + (int64_t)sr * slot_bytes + sbase + 16 * c);
     }
   }
+  // rows of the wave's x copy that the group loads never write stay zero
+  for (int e = lane; e < (16 * NT - 4 * NXQ) * (kBXRow / 8); e += 64)
+    reinterpret_cast<uint4*>(s_xw + 4 * NXQ * kBXRow)[e] = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
   float4v acc_g[NT], acc_u[NT];
 #pragma unroll
@@ -285,11 +326,11 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
     acc_u[t] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
   }
   if (tier == 3)
-    bh_tier<3, NT>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
+    bh_tier<3, NT, NXQ>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
   else if (tier == 2)
-    bh_tier<2, NT>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
+    bh_tier<2, NT, NXQ>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
   else
-    bh_tier<1, NT>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
+    bh_tier<1, NT, NXQ>(lane, w, d, G, B, x, rec, s_xw, s_sc, acc_g, acc_u);
   if (threadIdx.x < 16) s_mask[threadIdx.x] = my_slot < n_slots ? my_mask : 0u;
   __syncthreads();  // every wave is done with its x rows: the partials take their bytes
   // partials of the waves -> LDS: [w][gate/up][row][col]
@@ -669,12 +710,15 @@ hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const ui
   float* hB = reinterpret_cast<float*>(L->ab);  // [batch][cap]
   // tiles of 8 (FP16) and 16 items: at most ceil(cap/8) + 2 for any split into tiers
   const int tiles = (cap + 7) / 8 + 2;
-  if (batch <= 16) {
-    hipLaunchKernelGGL(ffn_bh_kernel<1>, dim3(tiles), dim3(kBHThreads), 0, stream, x, d, batch,
-                       counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
+  if (batch <= 8) {
+    hipLaunchKernelGGL((ffn_bh_kernel<1, 2>), dim3(tiles), dim3(kBHThreads), 0, stream, x, d,
+                       batch, counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
+  } else if (batch <= 16) {
+    hipLaunchKernelGGL((ffn_bh_kernel<1, 4>), dim3(tiles), dim3(kBHThreads), 0, stream, x, d,
+                       batch, counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
   } else {
-    hipLaunchKernelGGL(ffn_bh_kernel<2>, dim3(tiles), dim3(kBHThreads), 0, stream, x, d, batch,
-                       counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
+    hipLaunchKernelGGL((ffn_bh_kernel<2, 8>), dim3(tiles), dim3(kBHThreads), 0, stream, x, d,
+                       batch, counts, work_slot, work_mask, L->slots, sb, cap, n_slots, hB);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
