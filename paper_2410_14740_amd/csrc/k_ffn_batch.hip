@@ -354,7 +354,7 @@ __global__ __launch_bounds__(kBHThreads) void ffn_bh_kernel(
       u += s_part[((q * 2 + 1) * 16 + r) * NC + b];
     }
     // zero where row b did not select neuron r (or its slot is invalid)
-    hB[(int64_t)b * cap + item0 + r] = (s_mask[r] >> b) & 1u ? silu_mul(a, u) : 0.0f;
+    hB[(int64_t)b * ((cap + 3) & ~3) + item0 + r] = (s_mask[r] >> b) & 1u ? silu_mul(a, u) : 0.0f;
   }
 }
 
@@ -496,12 +496,14 @@ __device__ __forceinline__ uint32_t dm_offset(uint32_t v) { return v ^ 0x8888888
 
 // One wave's share of a run: neurons [first, first + 16 S) of the run's
 // items, group grp; acc[t][e] gets the lane's D rows 16 t + 4 j + i of MFMA e.
+// s_hw: the wave's LDS for its h values, 16 NT rows of 16 S floats.
+typedef float float4u __attribute__((ext_vector_type(4), aligned(4)));
 template <int TIER, int NT>
 __device__ __forceinline__ void dm_wave(int first, int hi, int grp, int d, int G, int B, int cap,
                                         const int32_t* __restrict__ work_slot,
                                         const float* __restrict__ hB,
                                         const uint8_t* __restrict__ slots, int64_t slot_bytes,
-                                        int n_slots, float4v (&acc)[NT][8]) {
+                                        int n_slots, float* s_hw, float4v (&acc)[NT][8]) {
   constexpr int S = dm_steps<TIER>();
   typedef typename DmWord<TIER>::T Word;
   const int lane = threadIdx.x & 63, x = lane & 15, j = lane >> 4;
@@ -528,16 +530,19 @@ __device__ __forceinline__ void dm_wave(int first, int hi, int grp, int d, int G
     for (int m = 0; m < 4; ++m)
       sl[st][m] = (u[m] & mj0) | (u[4 + m] & mj1) | (u[8 + m] & mj2) | (u[12 + m] & mj3);
   }
-  float a[S][NT][4];
+  // h of the wave's 16 S items for every batch row (rows cap rounded up to
+  // 4 apart): 16-byte loads of 4 consecutive items, which run along a row,
+  // staged through LDS; chunk e = 64 q + lane is row e / (4 S), items 4 (e %
+  // (4 S)) .. + 4. Rows past the batch and items past the run are masked below.
+  constexpr int CPR = 4 * S;  // 16-byte chunks per batch row
+  const int hs = (cap + 3) & ~3;
+  float4u hv[S * NT];
 #pragma unroll
-  for (int st = 0; st < S; ++st)
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const int idx = min(first + 16 * st + 4 * j + m, hi - 1);
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-        a[st][t][m] = hB[(int64_t)min(16 * t + x, B - 1) * cap + idx];
-    }
+  for (int q = 0; q < S * NT; ++q) {
+    const int e = 64 * q + lane, row = e / CPR, c = e - row * CPR;
+    hv[q] = *reinterpret_cast<const float4u*>(hB + (int64_t)min(row, B - 1) * hs +
+                                               min(first + 4 * c, hi - 1));
+  }
   // phase 2: per neuron its group scale and its codes (the zero slot past the run)
   half2v sc[S][2];  // two fp16 scales per register
   Word cw[S][4];
@@ -551,6 +556,20 @@ __device__ __forceinline__ void dm_wave(int first, int hi, int grp, int d, int G
       cw[st][m] = *reinterpret_cast<const Word*>(rec + doff);
     }
   __builtin_amdgcn_sched_barrier(0);  // keep every load issued before the first use
+#pragma unroll
+  for (int q = 0; q < S * NT; ++q) {
+    const int e = 64 * q + lane, row = e / CPR, c = e - row * CPR;
+    *reinterpret_cast<float4v*>(s_hw + row * 16 * S + 4 * c) = hv[q];
+  }
+  float a[S][NT][4];
+#pragma unroll
+  for (int st = 0; st < S; ++st)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float4v v = *reinterpret_cast<const float4v*>(s_hw + (16 * t + x) * 16 * S + 16 * st + 4 * j);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) a[st][t][m] = v[m];
+    }
   // h of rows past the batch and of items past the run is 0
 #pragma unroll
   for (int st = 0; st < S; ++st)
@@ -623,6 +642,7 @@ __global__ __launch_bounds__(kDMThreads) void ffn_bdm_kernel(
   // waves 4..7 add theirs to them, so that every LDS word has one writer at a
   // time (LDS float atomics are slow)
   __shared__ float s_y[kDMRegions][16 * NT][kRow];
+  static_assert(kDMWaves * 16 * dm_steps<1>() <= kDMRegions * kRow, "h staging fits in s_y");
   const int G = d >> 7;
   int grp = blockIdx.x % G;
   // Groups 2i and 2i + 1 of a run go to workgroup ids 8 apart: one XCD (ids
@@ -645,15 +665,19 @@ __global__ __launch_bounds__(kDMThreads) void ffn_bdm_kernel(
   for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[t][e] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+  // the waves' h staging (16 NT rows of at most 16 dm_steps<1>() floats
+  // each) lives in s_y until the partial results take it
+  float* s_hw = &s_y[0][0][0] + w * 16 * NT * 16 * dm_steps<1>();
   if (tier == 3)
     dm_wave<3, NT>(lo + w * 16 * dm_steps<3>(), hi, grp, d, G, B, cap, work_slot, hB, slots,
-                   slot_bytes, n_slots, acc);
+                   slot_bytes, n_slots, s_hw, acc);
   else if (tier == 2)
     dm_wave<2, NT>(lo + w * 16 * dm_steps<2>(), hi, grp, d, G, B, cap, work_slot, hB, slots,
-                   slot_bytes, n_slots, acc);
+                   slot_bytes, n_slots, s_hw, acc);
   else
     dm_wave<1, NT>(lo + w * 16 * dm_steps<1>(), hi, grp, d, G, B, cap, work_slot, hB, slots,
-                   slot_bytes, n_slots, acc);
+                   slot_bytes, n_slots, s_hw, acc);
+  __syncthreads();  // every wave's h staging is read
   const int lane = threadIdx.x & 63, x = lane & 15, j = lane >> 4;
 #pragma unroll
   for (int pass = 0; pass < 2; ++pass) {
@@ -707,7 +731,7 @@ hipError_t launch_ffn_batch(m2c_layer* L, const uint16_t* x, int batch, const ui
   const int n_slots = L->desc.cache_slots + L->S;
   const int cap = L->cap;
   if (cap <= 0) return hipSuccess;
-  float* hB = reinterpret_cast<float*>(L->ab);  // [batch][cap]
+  float* hB = reinterpret_cast<float*>(L->ab);  // [batch][cap rounded up to 4]
   // tiles of 8 (FP16) and 16 items: at most ceil(cap/8) + 2 for any split into tiers
   const int tiles = (cap + 7) / 8 + 2;
   if (batch <= 8) {
