@@ -124,9 +124,10 @@ def build_stack(wl, n_layers, steps_total, weight_sets, torch, m2c, W, flags=0, 
     order) and stage every layer's decode inputs on the device."""
     k, n16, n8 = wl.counts()
     C = wl.cache_slots()
-    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, flags=flags,
+    B = wl.batch
+    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, max_batch=B, flags=flags,
                          tier_slots=tier_slots)
-    x_dev = torch.empty((n_layers, steps_total, wl.d_model), dtype=torch.float16, device="cuda")
+    x_dev = torch.empty((n_layers, steps_total, B, wl.d_model), dtype=torch.float16, device="cuda")
     layers, first = [], None
 
     def draw(l):
@@ -140,7 +141,7 @@ def build_stack(wl, n_layers, steps_total, weight_sets, torch, m2c, W, flags=0, 
         for l, fu in enumerate(futs):
             ld = fu.result()
             futs[l] = None
-            x_dev[l].copy_(torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16))
+            x_dev[l].copy_(torch.from_numpy(ld.x[:, :B].view(np.uint16)).view(torch.float16))
             owner = None
             if weight_sets > 0 and l >= weight_sets:
                 owner = layers[l % weight_sets]
@@ -174,16 +175,20 @@ def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy, tier_slots=None):
     leg inside."""
     k, n16, n8 = wl.counts()
     C = wl.cache_slots()
-    cap = min(wl.d_ff, k)
+    B = wl.batch
+    cap = min(wl.d_ff, B * k)
     n_cores = len(os.sched_getaffinity(0))
     oracle.set_threads(n_cores)
+
+    def tier_maps(t):  # [B][d_ff] (rows of step t)
+        return np.stack([oracle.select_tiers(oracle.predict(ld.pred_a, ld.pred_b, ld.bias,
+                                                            ld.x[t, b])[1], k, n16, n8)[0]
+                         for b in range(B)])
+
     # records for the neurons the sample can touch (found by a first pass)
     steps_avail = ld.x.shape[0]
-    tiers_by_step = []
-    for t in range(steps_avail):
-        _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
-        tiers_by_step.append(oracle.select_tiers(s, k, n16, n8)[0])
-    used = np.nonzero(np.any(np.stack(tiers_by_step) > 0, axis=0))[0]
+    tiers_by_step = [tier_maps(t) for t in range(steps_avail)]
+    used = np.nonzero(np.any(np.concatenate(tiers_by_step) > 0, axis=0))[0]
     row = np.full(wl.d_ff, -1, np.int64)
     row[used] = np.arange(used.size)
     recs = {q: oracle.build_records(ld.w_gate[used], ld.w_up[used],
@@ -199,11 +204,11 @@ def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy, tier_slots=None):
         t_start = time.perf_counter()
         done = 0
         for t in range(steps_avail):
-            _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
-            tm, _ = oracle.select_tiers(s, k, n16, n8)
-            plan = cache.plan(tm, t)
+            tm = tier_maps(t)
+            plan = cache.plan(tm if B > 1 else tm[0], t)
             ids = row[plan["req_ids"]].astype(np.int32)
-            oracle.sparse_ffn(ld.x[t], ids, plan["req_tier"], recs)
+            oracle.sparse_ffn(ld.x[t], ids, plan["req_tier"], recs,
+                              plan["req_mask"] if B > 1 else None)
             done += 1
             if time.perf_counter() - t_start > budget:
                 break
@@ -213,15 +218,16 @@ def cpu_baseline(wl, ld, n_layers, budget_s, oracle, policy, tier_slots=None):
     per1, done1, _ = leg(1, budget_s / 2)
     perN, doneN, used_threads = leg(n_cores, budget_s / 2)
     oracle.set_threads(1)
-    return {"value": 1.0 / (perN * n_layers), "unit": "tokens/s", "cores": used_threads,
+    rows = f" of {B} rows" if B > 1 else ""
+    return {"value": B / (perN * n_layers), "unit": "tokens/s", "cores": used_threads,
             "kind": "oracle",
-            "sample": f"layer 0 of the {wl.name} stack, {doneN} consecutive decode steps of "
+            "sample": f"layer 0 of the {wl.name} stack, {doneN} consecutive decode steps{rows} of "
                       f"predict + select + LRU plan + fp64 sparse FFN on {used_threads} threads "
                       f"(OpenMP over independent sums); {perN * 1e3:.1f} ms per layer-step, "
                       f"scaled to {n_layers} layers",
             "ms_per_layer_step": perN * 1e3,
             "cpu_model": _cpu_model(), "sched_getaffinity": n_cores,
-            "one_thread": {"value": 1.0 / (per1 * n_layers), "unit": "tokens/s", "cores": 1,
+            "one_thread": {"value": B / (per1 * n_layers), "unit": "tokens/s", "cores": 1,
                            "ms_per_layer_step": per1 * 1e3, "steps": done1}}
 
 
@@ -316,29 +322,31 @@ def ffn_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
     (their active records exceed the 256 MB Infinity Cache for the 70B shape,
     so the data comes from HBM), back to back on one stream. Returns the HBM
     roofline of the FFN call (algorithmic bytes: every active record at its
-    tier, x and y)."""
+    tier, x and y; with a batch, the union of the rows' active records at
+    the union tier, averaged over the layers)."""
     k, n16, n8 = wl.counts()
     n4 = k - n16 - n8
     C = wl.cache_slots()
-    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, flags=flags)
+    B = wl.batch
+    desc = m2c.make_desc(wl.d_model, wl.d_ff, wl.pred_rank, k, C, max_batch=B, flags=flags)
     steps = 4
     layers = []
     for l in range(n_layers):
         ld = W.workload_layer(wl, l, steps=steps, draw_weights=(l == 0))
         layers.append((m2c.Layer(desc, ld, weights_of=layers[0][0] if l else None),
-                       torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16).cuda()))
+                       torch.from_numpy(ld.x[:, :B].view(np.uint16)).view(torch.float16).cuda()))
     d, d_ff = wl.d_model, wl.d_ff
-    tiers = torch.empty((1, d_ff), dtype=torch.uint8, device="cuda")
-    y = torch.zeros((1, d), dtype=torch.float32, device="cuda")
+    tiers = torch.empty((B, d_ff), dtype=torch.uint8, device="cuda")
+    y = torch.zeros((B, d), dtype=torch.float32, device="cuda")
     s = torch.cuda.current_stream()
     for t in range(steps):
         for L, x in layers:
-            L.predict_rank(x[t], 1, k, n16, n8, None, tiers, stream=s)
-            L.cache_plan(tiers, 1, t, stream=s)
+            L.predict_rank(x[t], B, k, n16, n8, None, tiers, stream=s)
+            L.cache_plan(tiers, B, t, stream=s)
             L.cache_fill(stream=s)
-            L.sparse_ffn(x[t], 1, y, stream=s)
+            L.sparse_ffn(x[t], B, y, stream=s)
     torch.cuda.synchronize()
-    calls = [(lambda L=L, x=x: L.sparse_ffn(x[steps - 1], 1, y, stream=s))
+    calls = [(lambda L=L, x=x: L.sparse_ffn(x[steps - 1], B, y, stream=s))
              for _ in range(reps) for L, x in layers]
     t0 = time.perf_counter()
     for fn in calls[:n_layers]:
@@ -347,7 +355,12 @@ def ffn_isolated(wl, n_layers, reps, torch, m2c, W, flags=0):
     per_call = (time.perf_counter() - t0) / n_layers
     ms, covered = timed_back_to_back(torch, s, calls, per_call * len(calls) * 10 + 0.05)
     rb = layers[0][0].info.record_bytes
-    nbytes = n16 * rb[3] + n8 * rb[2] + n4 * rb[1] + 2 * d + 4 * d
+    if B == 1:
+        nbytes = n16 * rb[3] + n8 * rb[2] + n4 * rb[1] + 2 * d + 4 * d
+    else:
+        per = [L.read_plan()["counts"] for L, _ in layers]
+        nbytes = int(round(sum(c[m2c.CNT_REQ_FP16] * rb[3] + c[m2c.CNT_REQ_INT8] * rb[2] +
+                               c[m2c.CNT_REQ_INT4] * rb[1] for c in per) / len(per))) + B * 6 * d
     avg = ms * 1e-3
     for L, _ in layers:
         L.close()
@@ -585,12 +598,13 @@ def run_stack(wl, n_layers, steps, warmup, weight_sets, flags, overlap_steps, st
     layers, x_dev, ld0 = build_stack(wl, n_layers, steps_total + overlap_steps, weight_sets, torch,
                                      m2c, W, flags=flags, tier_slots=tier_slots)
     log(f"setup {time.perf_counter() - t_setup:.1f} s")
-    d, d_ff = wl.d_model, wl.d_ff
-    tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
-    # m2c_sparse_ffn adds into y (a residual stream): one zeroed row per
+    d, d_ff, B = wl.d_model, wl.d_ff, wl.batch
+    tiers = torch.empty((n_layers, B, d_ff), dtype=torch.uint8, device="cuda")
+    # m2c_sparse_ffn adds into y (a residual stream): zeroed rows per
     # layer-step, so every output is the plain FFN of its token
-    y = torch.zeros((steps_total + overlap_steps, n_layers, d), dtype=torch.float32, device="cuda")
-    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=2)
+    y = torch.zeros((steps_total + overlap_steps, n_layers, B, d), dtype=torch.float32,
+                    device="cuda")
+    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=2, batch=B)
     timing = []
     ev_hooks = _StageEvents(torch, timing, None) if stage_events else None
 
@@ -639,7 +653,7 @@ def run_stack(wl, n_layers, steps, warmup, weight_sets, flags, overlap_steps, st
         L.close()
     return {
         "wall": wall, "n_layer_steps": n_ls, "ld0": ld0, "info": info,
-        "tokens_per_s": steps / wall, "us_per_layer_step": wall / n_ls * 1e6,
+        "tokens_per_s": steps * B / wall, "us_per_layer_step": wall / n_ls * 1e6,
         "pipeline": {
             "stage_events": bool(stage_events),
             "ffn_us_avg": float(ffn_ms.mean()) * 1e3 if ffn_ms is not None else None,
@@ -889,7 +903,9 @@ def main():
         8 if wl.name == "llama2-70b" else 0)
     flags = ffn_flags | (m2c.FLAG_DOMINANT_HITS if args.policy == "dominance" else 0)
     tier_slots = None
-    if args.arena == "pools":
+    if wl.batch > 1:
+        log(f"batch {wl.batch}: one arena (the per-tier arena serves batch 1)")
+    elif args.arena == "pools":
         tier_slots = m2c.pool_slots_for_budget(wl.d_model, {3: n16, 2: n8, 1: n4},
                                                wl.cache_slots() * 6 * wl.d_model)
         log(f"per-tier arena: {tier_slots} resident slots (FP16, INT8, INT4 pools)")
@@ -938,13 +954,16 @@ def main():
             os.path.join(ROOT, "profiles", f"sparse_ffn_{name}_layer.md"))
 
     ffn_kind = ("three kernels (up, down, ordered reduce), deterministic" if args.deterministic_ffn
+                else "batched: gate/up and down on the matrix cores" if wl.batch > 1
                 else "one launch (h tasks, then down tasks that wait on the h words)")
     d, d_ff = wl.d_model, wl.d_ff
 
     def roof(g, name, layers_cycled):
         return {"bound": "hbm", "achieved": g["achieved_GBps"], "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": g["achieved_GBps"] / PEAK_HBM_GBPS,
-                "traffic": traffic(name), "kernel": "m2c_sparse_ffn (ffn_fused_kernel)",
+                "traffic": traffic(name) if W.WORKLOADS[name].batch == 1 else None,
+                "kernel": ("m2c_sparse_ffn (ffn_bh_kernel + ffn_bdm_kernel)"
+                           if W.WORKLOADS[name].batch > 1 else "m2c_sparse_ffn (ffn_fused_kernel)"),
                 "workload": f"{name} layer shape, {layers_cycled} layers cycled",
                 "bytes_per_launch": g["bytes_per_launch"], "us_per_launch": g["us_avg"]}
 
@@ -964,7 +983,7 @@ def main():
         "config": {
             "workload": wl.name, "layers": n_layers, "d_model": d, "d_ff": d_ff,
             "pred_rank": wl.pred_rank, "k": k, "tiers_fp16_int8_int4": [n16, n8, n4],
-            "cache_slots": wl.cache_slots(), "batch": 1,
+            "cache_slots": wl.cache_slots(), "batch": wl.batch,
             "decode_steps": args.warmup + args.steps,
             "weights": "fp16 records with int8/int4 copies (group 128, fp16 scales), "
                        "pinned host store",

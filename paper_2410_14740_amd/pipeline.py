@@ -30,15 +30,18 @@ class StackSchedule:
     """Enqueues decode steps of `layers` (m2c.Layer objects) on three streams.
 
     k, n16, n8: top-k and tier counts for every layer. tiers: a uint8 device
-    tensor [n_layers][d_ff] for the tier maps. lag: how many layer-steps
-    behind the FFN the aux stream may run (1 or 2; at most the layer count).
+    tensor [n_layers][d_ff] (batch 1) or [n_layers][batch][d_ff] for the tier
+    maps. lag: how many layer-steps behind the FFN the aux stream may run (1
+    or 2; at most the layer count). batch: decode rows per step (each layer
+    created with max_batch >= batch); x_of / y_of then give [batch][d] rows.
     """
 
-    def __init__(self, torch, layers, k, n16, n8, tiers, lag=2, streams=None):
+    def __init__(self, torch, layers, k, n16, n8, tiers, lag=2, streams=None, batch=1):
         self.torch = torch
         self.layers = layers
         self.k, self.n16, self.n8 = k, n16, n8
         self.tiers = tiers
+        self.batch = batch
         n = len(layers)
         self.lag = max(1, min(lag, n))
         if streams is None:
@@ -50,9 +53,9 @@ class StackSchedule:
         self.enqueued = 0  # layer-steps enqueued so far
 
     def step(self, t, x_of, y_of, hooks=None, plan_of=None):
-        """Enqueue decode step t of every layer. x_of(l) -> fp16 device row
-        [d] (the token's input of layer l), y_of(l) -> fp32 device row [d]
-        that the FFN adds into. plan_of(l) -> plan buffer, or None for the
+        """Enqueue decode step t of every layer. x_of(l) -> fp16 device rows
+        [batch][d] (the tokens' inputs of layer l), y_of(l) -> fp32 device rows
+        [batch][d] that the FFN adds into. plan_of(l) -> plan buffer, or None for the
         layer's own. hooks: an object whose optional methods
         before_predict / after_plan / before_fill / after_fill / before_ffn /
         after_ffn (l, t, stream) run at those points (timing events, held
@@ -73,8 +76,9 @@ class StackSchedule:
             x = x_of(l)
             plan = None if plan_of is None else plan_of(l)
             hook("before_predict", l, self.aux)
-            L.predict_rank(x, 1, self.k, self.n16, self.n8, None, self.tiers[l], stream=self.aux)
-            L.cache_plan(self.tiers[l], 1, t, stream=self.aux, plan=plan)
+            B = self.batch
+            L.predict_rank(x, B, self.k, self.n16, self.n8, None, self.tiers[l], stream=self.aux)
+            L.cache_plan(self.tiers[l], B, t, stream=self.aux, plan=plan)
             hook("after_plan", l, self.aux)
             self.ev_plan[l].record(self.aux)
             self.copy.wait_event(self.ev_plan[l])
@@ -84,7 +88,7 @@ class StackSchedule:
             self.ev_fill[l].record(self.copy)
             self.main.wait_event(self.ev_fill[l])
             hook("before_ffn", l, self.main)
-            L.sparse_ffn(x, 1, y_of(l), stream=self.main, plan=plan)
+            L.sparse_ffn(x, B, y_of(l), stream=self.main, plan=plan)
             hook("after_ffn", l, self.main)
             self.ev_ffn[l].record(self.main)
             self.enqueued += 1

@@ -77,35 +77,39 @@ def _check_plan(L, raw, o, where):
 POOLS = {3: 20, 2: 80, 1: 120}  # below each tier's demand (35 / 140 / 175)
 
 
-@pytest.mark.parametrize("n_layers,lag,hold,poison,flags", [
-    (4, 2, False, False, 0),
-    (4, 2, True, True, 0),
-    (2, 1, True, True, 0),
-    (3, 2, True, True, m2c.FLAG_DOMINANT_HITS),
-    (3, 2, True, True, m2c.FLAG_TIER_POOLS),
-    (3, 2, True, True, m2c.FLAG_TIER_POOLS | m2c.FLAG_DOMINANT_HITS),
+@pytest.mark.parametrize("n_layers,lag,hold,poison,flags,batch", [
+    (4, 2, False, False, 0, 1),
+    (4, 2, True, True, 0, 1),
+    (2, 1, True, True, 0, 1),
+    (3, 2, True, True, m2c.FLAG_DOMINANT_HITS, 1),
+    (3, 2, True, True, m2c.FLAG_TIER_POOLS, 1),
+    (3, 2, True, True, m2c.FLAG_TIER_POOLS | m2c.FLAG_DOMINANT_HITS, 1),
+    (3, 2, True, True, 0, 4),
+    (3, 2, True, True, m2c.FLAG_DOMINANT_HITS, 4),
 ])
-def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
+def test_three_stream_schedule(n_layers, lag, hold, poison, flags, batch):
     d, d_ff, r, steps = 512, 1400, 32, 12
     k = 350
     n16, n8 = k // 10, (k // 2) - k // 10
     C = 250  # below k: evictions and bypasses through staging slots every step
     pools = bool(flags & m2c.FLAG_TIER_POOLS)
     desc = (m2c.make_desc(d, d_ff, r, k, 0, flags=flags & ~m2c.FLAG_TIER_POOLS, tier_slots=POOLS)
-            if pools else m2c.make_desc(d, d_ff, r, k, C, flags=flags))
+            if pools else m2c.make_desc(d, d_ff, r, k, C, max_batch=batch, flags=flags))
     policy = oracle.POLICY_DOMINANCE if flags & m2c.FLAG_DOMINANT_HITS else oracle.POLICY_EXACT
-    lds = [W.make_layer(900 + n_layers, l, d, d_ff, r, steps, rhos=(0.8,)) for l in range(n_layers)]
+    rhos = (0.8, 0.5, 0.9, 0.7)[:batch]
+    lds = [W.make_layer(900 + n_layers, l, d, d_ff, r, steps, rhos=rhos) for l in range(n_layers)]
     layers = [m2c.Layer(desc, ld) for ld in lds]
-    x = torch.stack([torch.from_numpy(ld.x[:, 0].view(np.uint16)).view(torch.float16)
-                     for ld in lds]).cuda()  # [layer][step][d]
-    y = torch.zeros((steps, n_layers, d), dtype=torch.float32, device="cuda")
-    tiers = torch.empty((n_layers, d_ff), dtype=torch.uint8, device="cuda")
+    x = torch.stack([torch.from_numpy(ld.x[:, :batch].view(np.uint16)).view(torch.float16)
+                     for ld in lds]).cuda()  # [layer][step][row][d]
+    y = torch.zeros((steps, n_layers, batch, d), dtype=torch.float32, device="cuda")
+    tiers = torch.empty((n_layers, batch, d_ff), dtype=torch.uint8, device="cuda")
     archive = torch.empty((steps, n_layers, layers[0].info.plan_bytes), dtype=torch.uint8,
                           device="cuda")
-    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=lag)
-    hooks = _Hooks(layers, archive, hold, poison, seed=n_layers * 10 + lag)
+    sched = pipeline.StackSchedule(torch, layers, k, n16, n8, tiers, lag=lag, batch=batch)
+    hooks = _Hooks(layers, archive, hold, poison, seed=n_layers * 10 + lag + batch)
     torch.cuda.synchronize()
-    say(f"pipeline layers={n_layers} lag={lag} hold={hold} poison={poison} flags={flags}: enqueue")
+    say(f"pipeline layers={n_layers} lag={lag} hold={hold} poison={poison} flags={flags} "
+        f"batch={batch}: enqueue")
     for t in range(steps):
         sched.step(t, lambda l: x[l, t], lambda l: y[t, l], hooks=hooks)
     torch.cuda.synchronize()
@@ -121,15 +125,18 @@ def test_three_stream_schedule(n_layers, lag, hold, poison, flags):
             cache = oracle.LRUCache(d_ff, C, L.info.staging_slots, policy)
         tot = np.zeros(16, np.int64)
         for t in range(steps):
-            _, s = oracle.predict(ld.pred_a, ld.pred_b, ld.bias, ld.x[t, 0])
-            tm, _ = oracle.select_tiers(s, k, n16, n8)
-            o = cache.plan(tm, t)
+            tm = np.stack([oracle.select_tiers(oracle.predict(ld.pred_a, ld.pred_b, ld.bias,
+                                                              ld.x[t, b])[1], k, n16, n8)[0]
+                           for b in range(batch)])
+            o = cache.plan(tm if batch > 1 else tm[0], t)
             tot += o["counts"]
             _check_plan(L, arch[t, l], o, f"layer {l} step {t}")
-            y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"])[0]
-            err = r8_errors(yg[t, l], y_ref).max()
-            worst = max(worst, err)
-            assert err <= FFN_TOL, f"layer {l} step {t}: FFN error {err:.3e}"
+            y_ref = oracle_ffn(ld, ld.x[t], o["req_ids"], o["req_tier"],
+                               o["req_mask"] if batch > 1 else None)
+            for b in range(batch):
+                err = r8_errors(yg[t, l, b], y_ref[b]).max()
+                worst = max(worst, err)
+                assert err <= FFN_TOL, f"layer {l} step {t} row {b}: FFN error {err:.3e}"
         if pools:
             for tr in (1, 2, 3):
                 so, key, last = m2c.m2c_debug_read_pool_tables(L.handle, tr, d_ff, POOLS[tr])
