@@ -319,23 +319,25 @@ __device__ void scan_entries2(unsigned long long* s_a, unsigned long long* s_b, 
     tmp[kPWaves + 1 + wave] = ib;
   }
   __syncthreads();
-  if (tid < 2) {  // thread 0 the first array's wave totals, thread 1 the second's
-    unsigned long long* w = tmp + tid * (kPWaves + 1);
-    unsigned long long run = 0;
-    for (int q = 0; q < kPWaves; ++q) {
-      const unsigned long long t = w[q];
-      w[q] = run;
-      run += t;
+  // every wave scans the wave totals itself (lane q: wave q's totals)
+  unsigned long long wa = lane < kPWaves ? tmp[lane] : 0ull;
+  unsigned long long wb = lane < kPWaves ? tmp[kPWaves + 1 + lane] : 0ull;
+#pragma unroll
+  for (int off = 1; off < kPWaves; off <<= 1) {
+    const unsigned long long oa = __shfl_up(wa, off), ob = __shfl_up(wb, off);
+    if (lane >= off) {
+      wa += oa;
+      wb += ob;
     }
-    w[kPWaves] = run;
   }
-  __syncthreads();
+  const unsigned long long ba = wave > 0 ? __shfl(wa, wave - 1) : 0ull;
+  const unsigned long long bb = wave > 0 ? __shfl(wb, wave - 1) : 0ull;
   if (tid < n) {
-    s_a[tid] = tmp[wave] + ia - va;
-    s_b[tid] = tmp[kPWaves + 1 + wave] + ib - vb;
+    s_a[tid] = ba + ia - va;
+    s_b[tid] = bb + ib - vb;
   }
-  *ta = tmp[kPWaves];
-  *tb = tmp[2 * kPWaves + 1];
+  *ta = __shfl(wa, kPWaves - 1);
+  *tb = __shfl(wb, kPWaves - 1);
   __syncthreads();
 }
 

@@ -179,9 +179,12 @@ __device__ __forceinline__ uint32_t score_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Block-wide exclusive prefix sum over one value per thread. `tmp` holds at
-// least blockDim.x / 64 + 1 entries of shared memory. Returns the exclusive
-// prefix; *total gets the block sum. Contains __syncthreads().
+// Block-wide exclusive prefix sum over one value per thread (at most 1024
+// threads). `tmp` holds at least blockDim.x / 64 entries of shared memory.
+// Returns the exclusive prefix; *total gets the block sum. Each wave scans
+// its lanes, then (after one barrier) the wave totals itself, lane q holding
+// wave q's total, so no single thread walks the totals. Contains
+// __syncthreads() (the second lets the caller reuse `tmp`).
 template <typename T>
 __device__ T block_exclusive_scan(T v, T* tmp, T* total) {
   const int lane = threadIdx.x & 63;
@@ -195,20 +198,16 @@ __device__ T block_exclusive_scan(T v, T* tmp, T* total) {
   }
   if (lane == 63) tmp[wave] = incl;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    T run = 0;
-    for (int w = 0; w < nwaves; ++w) {
-      T t = tmp[w];
-      tmp[w] = run;
-      run += t;
-    }
-    tmp[nwaves] = run;
+  T wt = lane < nwaves ? tmp[lane] : T(0);
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) {
+    T o = __shfl_up(wt, off);
+    if (lane >= off) wt += o;
   }
+  const T before = wave > 0 ? __shfl(wt, wave - 1) : T(0);
+  *total = __shfl(wt, nwaves - 1);
   __syncthreads();
-  T res = tmp[wave] + incl - v;
-  *total = tmp[nwaves];
-  __syncthreads();
-  return res;
+  return before + incl - v;
 }
 
 }  // namespace m2c
