@@ -12,17 +12,19 @@
 //   ffn_bh_kernel   a workgroup takes a tile of 16 neurons of one tier (8 for
 //                   FP16, padded with the zero slot); its 8
 //                   waves split d by quantization group (group g to wave
-//                   g % 8). For each group a wave issues
-//                   v_mfma_f32_16x16x16f16 over the 128 elements: A = the 16
-//                   neurons' codes (INT8 / INT4 unpacked to exact fp16),
-//                   B = x of 16 batch rows (rows past the batch read zeros).
-//                   The order of k inside a group is permuted the same way on
-//                   both operands, so that lane group j holds 32 consecutive
-//                   elements -- one 16-byte INT4 load, two INT8, four FP16.
-//                   Each group's product is scaled by its fp16 scales in fp32
-//                   and added up, so the dequantization stays exact. The
-//                   waves' partials meet in LDS; h_{b,i} = silu(a) * u, zero
-//                   where row b did not select neuron i.
+//                   g % 8). For each group a wave issues four
+//                   v_mfma_f32_16x16x32_f16 steps per row kind over the 128
+//                   elements: A = the 16 neurons' codes (INT8 / INT4 unpacked
+//                   to exact fp16), B = x of 16 batch rows (rows past the
+//                   batch are zeros), read from the wave's LDS copy of the
+//                   group's x rows. Which columns a lane takes in a step is
+//                   chosen per tier so that every 16-byte record load of a
+//                   wave covers 64 contiguous bytes of each row; both
+//                   operands follow the same order. Each group's product is
+//                   scaled by its fp16 scales in fp32 and added up, so the
+//                   dequantization stays exact. The waves' partials meet in
+//                   LDS; h_{b,i} = silu(a) * u, zero where row b did not
+//                   select neuron i.
 //   ffn_bdm_kernel  the down projection, also on the matrix cores, by
 //                   quantization group and single-tier run (below).
 #include "ffn_device.h"
