@@ -107,6 +107,19 @@ def test_tier_pools_llama70b_layer_at_the_same_budget(dominance):
         f"hit rate {tot[1] / tot[0]:.3f}")
 
 
+@pytest.mark.parametrize("dominance", [False, True])
+def test_tier_pools_lists_longer_than_the_merge_staging(dominance):
+    """k = 5000: the merged required and fill lists are longer than the 4096
+    ids the merge kernel stages in LDS, so it searches the pools' lists in
+    global memory instead."""
+    ld = W.make_layer(19, 0, 256, 12000, 16, 4, rhos=(0.7,))
+    k, n16, n8 = 5000, 500, 2000
+    worst, tot = _run(ld, 4, k, n16, n8, {3: 800, 2: 1500, 1: 2000},
+                      f"long lists dom {dominance}", dominance)
+    assert tot[0] == 4 * k and tot[1] > 0
+    say(f"long merge lists dominance {dominance}: worst FFN error {worst:.2e}")
+
+
 def test_tier_pools_overflow_leaves_everything_unchanged():
     ld = W.make_layer(17, 0, 256, 300, 16, 2)
     L = m2c.Layer(m2c.make_desc(256, 300, 16, 20, 0, tier_slots={3: 5, 2: 5, 1: 5}), ld)
