@@ -411,7 +411,8 @@ struct PlanLds {
   int hit, refill, empty, all, f[4], der[2];
 };
 
-template <bool ONE_ROW>
+// POOL: a per-tier pool's plan (pool_tier > 0, no dominance inside a pool).
+template <bool ONE_ROW, bool POOL>
 __device__ __forceinline__ void plan_fast_body(
     const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step, int dom,
     const DeviceState& st, const PlanPtrs& P, int pool_tier, int32_t* __restrict__ abort_word,
@@ -468,16 +469,28 @@ __device__ __forceinline__ void plan_fast_body(
       if (valid) s_info[i] = req ? (uint8_t)(t[g] | ((hit ? 1 : res ? 2 : 0) << 2) | (old[g] << 4)) : 0;
       if (res) s_sl[i] = (uint16_t)sl[g];
       if (res) atomicOr(&s_touch[sl[g] >> 5], 1u << (sl[g] & 31));
-      const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
-                               b2 = __ballot(req && !hit), b3 = __ballot(req && t[g] == 3),
-                               b4 = __ballot(req && t[g] == 2), b5 = __ballot(req && t[g] == 1),
-                               bh = __ballot(hit), br = __ballot(res && !hit);
-      if (lane == 0 && j < NJ) {
-        s_ca[j * kPWaves + wave] = pk3(popc(b0), popc(b1), popc(b2));
-        s_cb[j * kPWaves + wave] = pk3(popc(b3), popc(b4), popc(b5));
+      if constexpr (POOL) {
+        // one tier, resident = hit: fills are the NEW neurons, every count
+        // follows from two ballots
+        const int n0 = popc(__ballot(req)), n1 = popc(__ballot(req && !res));
+        if (lane == 0 && j < NJ) {
+          s_ca[j * kPWaves + wave] = pk3(n0, n1, n1);
+          s_cb[j * kPWaves + wave] = pk3(pool_tier == 3 ? n0 : 0, pool_tier == 2 ? n0 : 0,
+                                         pool_tier == 1 ? n0 : 0);
+        }
+        c_hit += n0 - n1;
+      } else {
+        const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
+                                 b2 = __ballot(req && !hit), b3 = __ballot(req && t[g] == 3),
+                                 b4 = __ballot(req && t[g] == 2), b5 = __ballot(req && t[g] == 1),
+                                 bh = __ballot(hit), br = __ballot(res && !hit);
+        if (lane == 0 && j < NJ) {
+          s_ca[j * kPWaves + wave] = pk3(popc(b0), popc(b1), popc(b2));
+          s_cb[j * kPWaves + wave] = pk3(popc(b3), popc(b4), popc(b5));
+        }
+        c_hit += popc(bh);
+        c_ref += popc(br);
       }
-      c_hit += popc(bh);
-      c_ref += popc(br);
     }
   }
   if (lane == 0) {
@@ -519,15 +532,27 @@ __device__ __forceinline__ void plan_fast_body(
       const int info = valid ? s_info[i] : 0;
       const int t = info & 3, code = (info >> 2) & 3;
       const bool req = t > 0, res = code != 0, hit = code == 1;
-      const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
-                               b2 = __ballot(req && !hit), b3 = __ballot(req && t == 3),
-                               b4 = __ballot(req && t == 2), b5 = __ballot(req && t == 1);
-      if (!req) continue;
-      const unsigned long long pa = s_ca[j * kPWaves + wave], pb = s_cb[j * kPWaves + wave];
-      const int pos = fd3(pa, 0) + popc(b0 & lt);
-      const int wp = t == 3 ? fd3(pb, 0) + popc(b3 & lt)
-                     : t == 2 ? N3 + fd3(pb, 1) + popc(b4 & lt)
-                              : N3 + N2 + fd3(pb, 2) + popc(b5 & lt);
+      int pos, wp, inew, ifill;
+      if constexpr (POOL) {  // one tier: the work order is the required order
+        const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res);
+        if (!req) continue;
+        const unsigned long long pa = s_ca[j * kPWaves + wave];
+        pos = wp = fd3(pa, 0) + popc(b0 & lt);
+        inew = fd3(pa, 1) + popc(b1 & lt);
+        ifill = fd3(pa, 2) + popc(b1 & lt);
+      } else {
+        const unsigned long long b0 = __ballot(req), b1 = __ballot(req && !res),
+                                 b2 = __ballot(req && !hit), b3 = __ballot(req && t == 3),
+                                 b4 = __ballot(req && t == 2), b5 = __ballot(req && t == 1);
+        if (!req) continue;
+        const unsigned long long pa = s_ca[j * kPWaves + wave], pb = s_cb[j * kPWaves + wave];
+        pos = fd3(pa, 0) + popc(b0 & lt);
+        wp = t == 3 ? fd3(pb, 0) + popc(b3 & lt)
+             : t == 2 ? N3 + fd3(pb, 1) + popc(b4 & lt)
+                      : N3 + N2 + fd3(pb, 2) + popc(b5 & lt);
+        inew = fd3(pa, 1) + popc(b1 & lt);
+        ifill = fd3(pa, 2) + popc(b2 & lt);
+      }
       P.req_ids[pos] = i;
       P.req_tier[pos] = (uint8_t)t;
       P.req_mask[pos] = m[g];
@@ -541,10 +566,10 @@ __device__ __forceinline__ void plan_fast_body(
         from = info >> 4;
         if (!hit) st.slot_tier[sl] = (uint8_t)t;
       } else {
-        st.new_pos[fd3(pa, 1) + popc(b1 & lt)] = pos;
+        st.new_pos[inew] = pos;
       }
       if (!hit) {
-        const int fr = fd3(pa, 2) + popc(b2 & lt);
+        const int fr = ifill;
         st.fill_pos[pos] = fr;
         P.fill_ids[fr] = i;
         P.fill_tier[fr] = (uint8_t)t;
@@ -708,9 +733,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_fast_kernel(
     DeviceState st, PlanPtrs P, int32_t* __restrict__ abort_word) {
   __shared__ PlanLds sm;
   if (B == 1)
-    plan_fast_body<true>(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word, sm);
+    plan_fast_body<true, false>(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word, sm);
   else
-    plan_fast_body<false>(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word, sm);
+    plan_fast_body<false, false>(tier_map, B, d_ff, C, cap, step, dom, st, P, 0, abort_word, sm);
 }
 
 // Per-tier arena: workgroup q plans pool 3 - q (FP16, INT8, INT4) into its
@@ -727,11 +752,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_pools_kernel(
   const int q = blockIdx.x;
   __shared__ PlanLds sm;
   if (B == 1)
-    plan_fast_body<true>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q], 3 - q,
-                         abort_word, sm);
+    plan_fast_body<true, true>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q],
+                               3 - q, abort_word, sm);
   else
-    plan_fast_body<false>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q],
-                          3 - q, abort_word, sm);
+    plan_fast_body<false, true>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q],
+                                3 - q, abort_word, sm);
 }
 
 // Per-tier arena with dominance hits: the pool that serves each neuron this
