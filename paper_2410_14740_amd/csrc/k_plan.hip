@@ -408,15 +408,20 @@ struct PlanLds {
   uint32_t cu[kPJ * kPWaves];               // slot compactions per (chunk, wave)
   unsigned long long scan64[2 * (kPWaves + 1)];
   uint32_t scan32[kPWaves + 1];
+  int pre[kPJ + 1];  // pool plans: offsets of the pool's per-chunk lists
   int hit, refill, empty, all, f[4], der[2];
 };
 
-// POOL: a per-tier pool's plan (pool_tier > 0, no dominance inside a pool).
+// POOL: a per-tier pool's plan (pool_tier > 0, no dominance inside a pool),
+// over the pool's required neurons as pool_compact_kernel listed them: plist
+// (chunk j's ids from j * kPlanThreads, ascending) and pcount ([3][NJ], every
+// pool's, for the capacity check); tier_map and B are not read.
 template <bool ONE_ROW, bool POOL>
 __device__ __forceinline__ void plan_fast_body(
     const uint8_t* __restrict__ tier_map, int B, int d_ff, int C, int cap, int step, int dom,
     const DeviceState& st, const PlanPtrs& P, int pool_tier, int32_t* __restrict__ abort_word,
-    PlanLds& sm) {
+    PlanLds& sm, const int32_t* __restrict__ plist = nullptr,
+    const int32_t* __restrict__ pcount = nullptr) {
   uint8_t* s_info = sm.info;
   uint16_t* s_sl = sm.sl;
   uint32_t* s_touch = sm.touch;
@@ -436,6 +441,111 @@ __device__ __forceinline__ void plan_fast_body(
   }
   for (int w = tid; w < (C + 31) / 32; w += kPlanThreads) s_touch[w] = 0;
   __syncthreads();
+  int NREQ, NNEW, NF, N3, N2, N1;
+  if constexpr (POOL) {
+    // ---------------- A (pool): the pool's required list is the
+    // concatenation of its chunk lists; entry e is required neuron e
+    const int q = 3 - pool_tier;
+    int* s_pre = sm.pre;
+    if (wave == 0) {  // chunk offsets (NJ <= 32) and the total over every pool
+      int own = lane < NJ ? pcount[q * NJ + lane] : 0;
+      int all = lane < NJ ? pcount[lane] + pcount[NJ + lane] + pcount[2 * NJ + lane] : 0;
+#pragma unroll
+      for (int off = 1; off < 32; off <<= 1) {
+        const int o = __shfl_up(own, off), a = __shfl_up(all, off);
+        if (lane >= off) {
+          own += o;
+          all += a;
+        }
+      }
+      if (lane < NJ) s_pre[lane + 1] = own;
+      if (lane == 0) s_pre[0] = 0;
+      if (lane == 31) sh_all = all;
+    }
+    __syncthreads();
+    const int R = s_pre[NJ], NALL = sh_all;
+    if (NALL > cap) {  // workgroup-uniform: an empty plan, the cache untouched
+      if (tid == 0) {
+        for (int c = 0; c < M2C_NCOUNTS; ++c) P.counts[c] = 0;
+        P.counts[M2C_NCOUNTS - 1] = NALL;
+        if (pool_tier == 3) {
+          atomicOr(st.status, M2C_STATUS_PLAN_OVERFLOW);
+          *abort_word = 1;
+        }
+      }
+      return;
+    }
+    if (pool_tier == 3 && tid == 0) *abort_word = 0;
+    // entry e of the list: chunk j with s_pre[j] <= e < s_pre[j + 1]
+    auto entry = [&](int e) {
+      int lo = 0, hi = NJ;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (s_pre[mid] <= e) lo = mid;
+        else hi = mid;
+      }
+      return plist[lo * kPlanThreads + (e - s_pre[lo])];
+    };
+    const int NE = (R + kPlanThreads - 1) / kPlanThreads;  // rounds of entries (<= kPJ)
+    constexpr int kPR = 4;  // rounds whose loads are in flight together
+    // pass 1: the NEW neurons (not resident) per (round, wave); resident
+    // neurons touch their slots
+    for (int r0 = 0; r0 < NE; r0 += kPR) {
+      int id[kPR], sl[kPR];
+#pragma unroll
+      for (int u = 0; u < kPR; ++u) id[u] = entry(min(tid + kPlanThreads * (r0 + u), max(R - 1, 0)));
+#pragma unroll
+      for (int u = 0; u < kPR; ++u) sl[u] = st.slot_of[id[u]];
+#pragma unroll
+      for (int u = 0; u < kPR; ++u) {
+        const int r = r0 + u;
+        const bool in = r < NE && tid + kPlanThreads * r < R;
+        if (in && sl[u] >= 0) atomicOr(&s_touch[sl[u] >> 5], 1u << (sl[u] & 31));
+        const unsigned long long b = __ballot(in && sl[u] < 0);
+        if (lane == 0 && r < NE) s_cu[r * kPWaves + wave] = (uint32_t)popc(b);
+      }
+    }
+    __syncthreads();
+    const int nnew = (int)scan_entries<uint32_t>(s_cu, NE * kPWaves, scan32);
+    // pass 2: required, NEW and fill lists (the fills are the NEW neurons)
+    for (int r0 = 0; r0 < NE; r0 += kPR) {
+      int id[kPR], sl[kPR];
+#pragma unroll
+      for (int u = 0; u < kPR; ++u) id[u] = entry(min(tid + kPlanThreads * (r0 + u), max(R - 1, 0)));
+#pragma unroll
+      for (int u = 0; u < kPR; ++u) sl[u] = st.slot_of[id[u]];
+#pragma unroll
+      for (int u = 0; u < kPR; ++u) {
+        const int r = r0 + u, e = tid + kPlanThreads * r;
+        const bool in = r < NE && e < R, nw = in && sl[u] < 0;
+        const unsigned long long b = __ballot(nw);
+        if (!in) continue;
+        P.req_ids[e] = id[u];
+        P.req_tier[e] = (uint8_t)pool_tier;
+        P.req_mask[e] = 1u;
+        st.work_pos[e] = e;
+        if (!nw) {
+          P.req_slot[e] = sl[u];
+          P.req_hit[e] = 1;
+          st.slot_last[sl[u]] = step;
+          st.fill_pos[e] = -1;
+        } else {
+          const int inew = (int)s_cu[r * kPWaves + wave] + popc(b & lt);
+          st.new_pos[inew] = e;
+          st.fill_pos[e] = inew;
+          P.fill_ids[inew] = id[u];
+          P.fill_tier[inew] = (uint8_t)pool_tier;
+          P.fill_from[inew] = 0;
+        }
+      }
+    }
+    NREQ = R;
+    NNEW = NF = nnew;
+    N3 = pool_tier == 3 ? R : 0;
+    N2 = pool_tier == 2 ? R : 0;
+    N1 = pool_tier == 1 ? R : 0;
+    if (tid == 0) sh_hit = R - nnew;
+  } else {
   // ---------------- A1: classify and count (reads only)
   // every load of a group is issued before the first value is used; the
   // wave's counts stay in registers until the end of the sweep
@@ -501,8 +611,12 @@ __device__ __forceinline__ void plan_fast_body(
   __syncthreads();
   unsigned long long totA, totB;
   scan_entries2(s_ca, s_cb, NJ * kPWaves, scan64, &totA, &totB);
-  const int NREQ = fd3(totA, 0), NNEW = fd3(totA, 1), NF = fd3(totA, 2);
-  const int N3 = fd3(totB, 0), N2 = fd3(totB, 1), N1 = fd3(totB, 2);
+  NREQ = fd3(totA, 0);
+  NNEW = fd3(totA, 1);
+  NF = fd3(totA, 2);
+  N3 = fd3(totB, 0);
+  N2 = fd3(totB, 1);
+  N1 = fd3(totB, 2);
   const int NALL = pool_tier ? sh_all : NREQ;  // sh_all is final after the scans' barriers
   if (NALL > cap) {  // workgroup-uniform: an empty plan, the cache untouched
     if (tid == 0) {
@@ -580,6 +694,7 @@ __device__ __forceinline__ void plan_fast_body(
       }
     }
   }
+  }  // A1, A2 (the touched-slot marks were made before the scans' barriers)
   // ---------------- C: victims = untouched slots in LRU order
   const int cur = *st.lru_cur;
   const int32_t* lru_in = st.lru + (int64_t)cur * C;
@@ -747,38 +862,67 @@ struct PoolJobs {
 };
 
 __global__ __launch_bounds__(kPlanThreads) void plan_pools_kernel(
-    const uint8_t* __restrict__ tier_map, int B, int d_ff, int cap, int step, PoolJobs jobs,
-    int32_t* __restrict__ abort_word) {
+    const int32_t* __restrict__ lists, const int32_t* __restrict__ counts, int d_ff, int cap,
+    int step, PoolJobs jobs, int32_t* __restrict__ abort_word) {
   const int q = blockIdx.x;
   __shared__ PlanLds sm;
-  if (B == 1)
-    plan_fast_body<true, true>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q],
-                               3 - q, abort_word, sm);
-  else
-    plan_fast_body<false, true>(tier_map, B, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q],
-                                3 - q, abort_word, sm);
+  plan_fast_body<true, true>(nullptr, 1, d_ff, jobs.C[q], cap, step, 0, jobs.st[q], jobs.P[q],
+                             3 - q, abort_word, sm, lists + (int64_t)q * d_ff, counts);
 }
 
-// Per-tier arena with dominance hits: the pool that serves each neuron this
-// step. A neuron required at tier t (its highest tier over the batch rows)
+// Per-tier arena: the pool that serves each neuron this step, and each
+// pool's required neurons as lists per chunk of kPlanThreads neurons (one
+// workgroup per chunk; ascending id inside a chunk, so the chunk lists in
+// order are the pool's required list). A neuron's step tier is its highest
+// over the batch rows. With dominance hits (dom), a neuron required at tier t
 // that is not resident in pool t but is resident in a pool of higher
 // precision goes to the lowest such pool, as a hit at that pool's tier; any
 // other neuron keeps its tier. Residency is read before any pool plans the
-// step. slot_of: the pools' tables [3][d_ff], FP16 first.
-__global__ __launch_bounds__(256) void pool_resolve_kernel(const uint8_t* __restrict__ tier_map,
-                                                           int B, int d_ff,
-                                                           const int32_t* __restrict__ slot_of,
-                                                           uint8_t* __restrict__ out) {
-  for (int n = blockIdx.x * blockDim.x + threadIdx.x; n < d_ff; n += gridDim.x * blockDim.x) {
-    // every load at once (one memory round trip; this kernel runs beside the
-    // fills, whose host reads make each round trip long)
-    const bool r3 = slot_of[n] >= 0, r2 = slot_of[(int64_t)d_ff + n] >= 0,
-               r1 = slot_of[2 * (int64_t)d_ff + n] >= 0;
-    int t = 0;
-    for (int b = 0; b < B; ++b) t = max(t, (int)tier_map[(int64_t)b * d_ff + n]);
+// step. slot_of: the pools' tables [3][d_ff], FP16 first; lists [3][d_ff]
+// (chunk j's from j * kPlanThreads), counts [3][gridDim.x].
+__global__ __launch_bounds__(kPlanThreads) void pool_compact_kernel(
+    const uint8_t* __restrict__ tier_map, int B, int d_ff, int dom,
+    const int32_t* __restrict__ slot_of, int32_t* __restrict__ lists,
+    int32_t* __restrict__ counts) {
+  __shared__ uint32_t s_wc[3][kPWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = blockIdx.x * kPlanThreads + tid;
+  const int nc = min(n, d_ff - 1);
+  // every load at once (one memory round trip; this kernel runs beside the
+  // fills, whose host reads make each round trip long)
+  bool r3 = false, r2 = false, r1 = false;
+  if (dom) {
+    r3 = slot_of[nc] >= 0;
+    r2 = slot_of[(int64_t)d_ff + nc] >= 0;
+    r1 = slot_of[2 * (int64_t)d_ff + nc] >= 0;
+  }
+  int t = 0;
+  for (int b = 0; b < B; ++b) t = max(t, (int)tier_map[(int64_t)b * d_ff + nc]);
+  t = min(t, 3);
+  if (dom) {
     const bool own = t == 3 ? r3 : t == 2 ? r2 : t == 1 ? r1 : true;
     if (!own) t = (t < 2 && r2) ? 2 : r3 ? 3 : t;
-    out[n] = (uint8_t)t;
+  }
+  if (n >= d_ff) t = 0;
+  unsigned long long mine = 0ull;
+#pragma unroll
+  for (int p = 3; p >= 1; --p) {
+    const unsigned long long b = __ballot(t == p);
+    if (t == p) mine = b;
+    if (lane == 0) s_wc[3 - p][wave] = (uint32_t)popc(b);
+  }
+  __syncthreads();
+  if (t > 0) {
+    const int q = 3 - t;
+    int pre = 0;
+    for (int w = 0; w < wave; ++w) pre += (int)s_wc[q][w];
+    lists[(int64_t)q * d_ff + (int64_t)blockIdx.x * kPlanThreads + pre +
+          popc(mine & ((1ull << lane) - 1ull))] = n;
+  }
+  if (tid < 3) {
+    int c = 0;
+    for (int w = 0; w < kPWaves; ++w) c += (int)s_wc[tid][w];
+    counts[tid * (int)gridDim.x + blockIdx.x] = c;
   }
 }
 
@@ -1011,21 +1155,13 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
     pp.p[q] = {Pq.counts, Pq.req_ids, Pq.req_hit, Pq.req_slot, Pq.req_mask, Pq.fill_ids,
                Pq.fill_slot, Pq.evicted_ids};
   }
-  const uint8_t* pool_map = tier_map;
-  int pool_batch = batch;
-  if (dom) {
-    const int d_ff = L->desc.d_ff;
-    int blocks = (d_ff + 255) / 256;
-    blocks = blocks > 128 ? 128 : blocks;
-    hipLaunchKernelGGL(pool_resolve_kernel, dim3(blocks), dim3(256), 0, stream, tier_map, batch,
-                       d_ff, L->st.slot_of, L->pool_res);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    pool_map = L->pool_res;
-    pool_batch = 1;
-  }
-  hipLaunchKernelGGL(plan_pools_kernel, dim3(3), dim3(kPlanThreads), 0, stream, pool_map,
-                     pool_batch, L->desc.d_ff, L->cap, step, jobs, L->plan_abort);
+  const int NJ = (L->desc.d_ff + kPlanThreads - 1) / kPlanThreads;  // <= kPJ (checked at create)
+  hipLaunchKernelGGL(pool_compact_kernel, dim3(NJ), dim3(kPlanThreads), 0, stream, tier_map, batch,
+                     L->desc.d_ff, dom, L->st.slot_of, L->pool_lists, L->pool_counts);
+  hipError_t e0 = hipGetLastError();
+  if (e0 != hipSuccess) return e0;
+  hipLaunchKernelGGL(plan_pools_kernel, dim3(3), dim3(kPlanThreads), 0, stream, L->pool_lists,
+                     L->pool_counts, L->desc.d_ff, L->cap, step, jobs, L->plan_abort);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   int blocks = (L->cap + kMergeThreads - 1) / kMergeThreads;

@@ -243,7 +243,8 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   void* p_slot_last; void* p_lru; void* p_lru_cur; void* p_new_pos; void* p_work_pos;
   void* p_vslot; void* p_vold; void* p_fill_pos; void* p_prev_tier; void* p_have; void* p_stats;
   void* p_status;
-  void* p_gen; void* p_hw; void* p_pool_plan; void* p_abort; void* p_pool_res;
+  void* p_gen; void* p_hw; void* p_pool_plan; void* p_abort; void* p_pool_lists;
+  void* p_pool_counts;
   Piece pieces[] = {
       // C resident + S staging slots, then one slot that stays zero: padding
       // lanes of the FFN kernels read it instead of branching around loads
@@ -275,7 +276,8 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
       {&p_hw, cap * 8},
       {&p_pool_plan, L->pools ? 3 * L->plan_core_bytes : 0},
       {&p_abort, 4},
-      {&p_pool_res, L->pools ? dff : 0},
+      {&p_pool_lists, L->pools ? 3 * dff * 4 : 0},
+      {&p_pool_counts, L->pools ? 3 * 32 * 4 : 0},
   };
   int64_t total = 0;
   int64_t offs[sizeof(pieces) / sizeof(pieces[0])];
@@ -316,7 +318,8 @@ m2c_status alloc_device(m2c_layer* L, bool with_bias) {
   L->st.ffn_hw = (unsigned long long*)p_hw;
   L->pool_plan = (uint8_t*)p_pool_plan;
   L->plan_abort = (int32_t*)p_abort;
-  L->pool_res = (uint8_t*)p_pool_res;
+  L->pool_lists = (int32_t*)p_pool_lists;
+  L->pool_counts = (int32_t*)p_pool_counts;
   L->info.device_bytes = total;
   HIPOK(hipMemset(L->slots + L->map.zero, 0, L->info.slot_bytes), "clear the zero slot");
   HIPOK(hipMemset(L->plan_abort, 0, 4), "clear the plan abort word");

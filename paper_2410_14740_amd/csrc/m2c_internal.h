@@ -103,7 +103,11 @@ struct m2c_layer {
   m2c::SlotMap map;               // slot id -> byte offset, by tier
   int64_t arena_bytes = 0;        // pools + zero slot
   uint8_t* pool_plan = nullptr;   // [3][plan_core_bytes] the pools' own plans
-  uint8_t* pool_res = nullptr;    // [d_ff] serving pool's tier per neuron (pools with dominance hits)
+  // per-tier arena: each pool's required neurons of a step, per chunk of
+  // 1024 neurons in ascending id ([3][d_ff], FP16 first; chunk j from j * 1024),
+  // and their counts ([3][32])
+  int32_t* pool_lists = nullptr;
+  int32_t* pool_counts = nullptr;
   int64_t plan_core_bytes = 0;    // a plan without the one-launch FFN's task table
   int32_t* plan_abort = nullptr;  // [1] set when a step's required set overflowed
 };
