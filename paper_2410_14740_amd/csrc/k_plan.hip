@@ -17,6 +17,14 @@
 //      (tier-major FP16, INT8, INT4; ascending id inside a tier).
 // Ranks in id / position order come from block scans over contiguous
 // per-thread ranges.
+//
+// Three launches build this plan: plan_kernel (any d_ff, the steps above
+// over per-thread ranges), plan_fast_kernel (d_ff <= 32768, the same steps
+// as coalesced sweeps with LDS-resident per-neuron state) and, for the
+// per-tier arena, pool_compact_kernel (which pool serves each neuron; each
+// pool's required ids, per chunk) -> plan_pools_kernel (one workgroup per
+// pool, the fast plan over that pool's list) -> plan_merge_kernel (the
+// three pools' plans merged by id into the caller's plan).
 #include "m2c_internal.h"
 
 namespace m2c {
