@@ -688,11 +688,14 @@ __device__ __forceinline__ void dn_task(const FTaskArgs& a, const int (&idt)[kFL
   }
 }
 
-// at most 96 VGPRs: five workgroups per CU
-template <int K>
+// Register budget of at least five workgroups per CU (96 VGPRs). At d = 8192
+// the code takes 76, so six are resident, which the LDS (21.8 KB per
+// workgroup) also allows; a budget of seven (72 VGPRs) spills in the INT4 h
+// path and made that call 15% slower. At d = 4096 it takes 96 (five).
 #ifndef M2C_FFN_WAVES_PER_EU
 #define M2C_FFN_WAVES_PER_EU 5
 #endif
+template <int K>
 __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(M2C_FFN_WAVES_PER_EU))) void ffn_fused_kernel(
     const uint16_t* __restrict__ x, const int32_t* __restrict__ tasks,
     const int32_t* __restrict__ task_ids, unsigned long long* __restrict__ gen,
