@@ -690,8 +690,9 @@ __device__ __forceinline__ void dn_task(const FTaskArgs& a, const int (&idt)[kFL
 
 // Register budget of at least five workgroups per CU (96 VGPRs). At d = 8192
 // the code takes 76, so six are resident, which the LDS (21.8 KB per
-// workgroup) also allows; a budget of seven (72 VGPRs) spills in the INT4 h
-// path and made that call 15% slower. At d = 4096 it takes 96 (five).
+// workgroup) also allows. Six is the measured optimum there: seven (INT4
+// gate / up chunks computed in pairs, 67 VGPRs, no spills) took 14.6 us
+// against 14.36, five 15.5. At d = 4096 the code takes 96 (five).
 #ifndef M2C_FFN_WAVES_PER_EU
 #define M2C_FFN_WAVES_PER_EU 5
 #endif
