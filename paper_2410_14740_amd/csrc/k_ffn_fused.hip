@@ -696,7 +696,10 @@ __device__ __forceinline__ void dn_task(const FTaskArgs& a, const int (&idt)[kFL
 #ifndef M2C_FFN_WAVES_PER_EU
 #define M2C_FFN_WAVES_PER_EU 5
 #endif
-template <int K>
+// EXACT: d = 1024 K (constant offsets in the h tasks), a kernel of its own so
+// that the register count of the general-d paths (96 at K = 4, for INT4)
+// does not set its occupancy.
+template <int K, bool EXACT>
 __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(M2C_FFN_WAVES_PER_EU))) void ffn_fused_kernel(
     const uint16_t* __restrict__ x, const int32_t* __restrict__ tasks,
     const int32_t* __restrict__ task_ids, unsigned long long* __restrict__ gen,
@@ -747,7 +750,7 @@ __global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(M2C_FFN_WAV
   a.slice = hd.w;
   const uint32_t epoch = (uint32_t)e0 + 1u;
   if (kind == 1) {
-    if (K >= 2 && d == 1024 * K) {
+    if constexpr (EXACT) {
       if (tier == 1)
         h_task<K, 1, true>(a, idt, x, xlds, sh, hw, epoch, withhold, tid);
       else if (tier == 2)
@@ -779,9 +782,14 @@ hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* tasks, f
   const int d = L->desc.d_model;
   const size_t lds = fused_lds_bytes(d);
   const int32_t* task_ids = tasks + task_ids_offset(L->ffn_grid) / 4;
-  hipLaunchKernelGGL(ffn_fused_kernel<K>, dim3(L->ffn_grid), dim3(kFT), lds, stream, x, tasks,
-                     task_ids, L->st.ffn_gen, L->slots, d, L->st.ffn_hw, L->st.status, y,
-                     L->ffn_withhold);
+  if (K >= 2 && d == 1024 * K)
+    hipLaunchKernelGGL((ffn_fused_kernel<K, K >= 2>), dim3(L->ffn_grid), dim3(kFT), lds, stream,
+                       x, tasks, task_ids, L->st.ffn_gen, L->slots, d, L->st.ffn_hw, L->st.status,
+                       y, L->ffn_withhold);
+  else
+    hipLaunchKernelGGL((ffn_fused_kernel<K, false>), dim3(L->ffn_grid), dim3(kFT), lds, stream, x,
+                       tasks, task_ids, L->st.ffn_gen, L->slots, d, L->st.ffn_hw, L->st.status, y,
+                       L->ffn_withhold);
   return hipGetLastError();
 }
 
