@@ -697,10 +697,13 @@ __device__ __forceinline__ void dn_task(const FTaskArgs& a, const int (&idt)[kFL
 #define M2C_FFN_WAVES_PER_EU 5
 #endif
 // EXACT: d = 1024 K (constant offsets in the h tasks), a kernel of its own so
-// that the register count of the general-d paths (96 at K = 4, for INT4)
-// does not set its occupancy.
+// that the register count of the general-d paths does not set its occupancy.
+// General d at K = 4 gets a budget of four workgroups per CU: its INT4 h path
+// needs 100 VGPRs, and at 96 the compiler spills scale values as they load,
+// each spill waiting for every load in flight.
 template <int K, bool EXACT>
-__global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(M2C_FFN_WAVES_PER_EU))) void ffn_fused_kernel(
+__global__ __launch_bounds__(kFT) __attribute__((amdgpu_waves_per_eu(
+    K == 4 && !EXACT ? 4 : M2C_FFN_WAVES_PER_EU))) void ffn_fused_kernel(
     const uint16_t* __restrict__ x, const int32_t* __restrict__ tasks,
     const int32_t* __restrict__ task_ids, unsigned long long* __restrict__ gen,
     const uint8_t* __restrict__ slots, int d, unsigned long long* __restrict__ hw,

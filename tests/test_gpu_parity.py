@@ -540,7 +540,8 @@ def test_ffn_wait_give_up_is_reported():
     L.close()
 
 
-@pytest.mark.parametrize("d,d_ff", [(1024, 2752), (4096, 3000), (8192, 3000)])
+@pytest.mark.parametrize("d,d_ff", [(1024, 2752), (1536, 2000), (2048, 2000), (3072, 2000),
+                                    (4096, 3000), (5120, 2000), (8192, 3000)])
 def test_ffn_modes_accumulate_and_determinism(d, d_ff):
     """Both FFN paths add into y; the deterministic path repeats bit for bit
     and the fused path agrees with it to fp32 rounding. (Each of the fused
@@ -548,7 +549,9 @@ def test_ffn_modes_accumulate_and_determinism(d, d_ff):
     holds, so the cross-mode check starts from y = 0; a column's sum is one
     fp32 partial per down task that covers it, and their number follows the
     task geometry, so the cross-mode bound is a quarter of the oracle
-    tolerance rather than a fixed multiple of one rounding.)"""
+    tolerance rather than a fixed multiple of one rounding.) The widths cover
+    every fused kernel instance: K = 1, 2, 4 and 8 sixteen-byte loads per
+    lane and unit, each with d = 1024 K (K > 1) and with another d."""
     ld = W.make_layer(61, 0, d, d_ff, 64, 1)
     k = d_ff // 5
     n16, n8 = _counts(k, (1, 10), (2, 5))
