@@ -4,7 +4,7 @@
 //   y += sum_i silu(<g_i, x>) * <u_i, x> * d_i
 //
 // The work is a list of equal-sized tasks, one per workgroup (8 sixteen-byte
-// loads per lane of a 512-thread workgroup, all issued at once):
+// loads per lane of a 256-thread workgroup, all issued at once):
 //
 //   h tasks     gate/up dot products of a few neurons of one tier ("units" of
 //               d bytes, one or more per wave), h_i = silu(a_i) * b_i, each
@@ -22,8 +22,8 @@
 // nothing, so every producer runs. The hardware dispatcher replaces each
 // finished workgroup at once, so the down loads stream behind the gate/up
 // loads without a second launch. The poll is bounded anyway: past the limit
-// it sets the layer's status word and takes h = 0. At most 80 VGPRs keep
-// three workgroups on a CU, so enough loads are in flight and the
+// it sets the layer's status word and takes h = 0. Six workgroups share a CU
+// at d = 8192 (76 VGPRs), so enough loads are in flight and the
 // dequantization of one workgroup overlaps the loads of the others.
 //
 // Call tag: the grid has a fixed size per layer (the most tasks a plan of
