@@ -48,129 +48,11 @@
 // Padding lanes and invalid slots read slot n_slots, which is all zeros, so
 // no load sits under a per-lane branch; every task kind issues the same
 // number of loads, so the compiler's wait counts do not depend on the kind.
-#include "ffn_device.h"
+#include "ffn_tasks.h"
 
 namespace m2c {
 
 namespace {
-
-#ifndef M2C_FFN_THREADS
-#define M2C_FFN_THREADS 256
-#endif
-constexpr int kFT = M2C_FFN_THREADS;     // threads per workgroup
-constexpr int kFWaves = kFT / 64;
-constexpr int kFL = 8;                   // 16-byte data loads per lane and task
-constexpr int kFSW = 512;                // down tasks: output columns per slice
-constexpr int kFLPN = kFSW / 32;         // lanes per neuron row of a slice
-constexpr int kFNPR = kFT / kFLPN;       // neurons per round of a down task
-constexpr int kFMaxItems = kFL * kFNPR;  // most work items of one task (INT4 down)
-// Rounds of kFNPR neurons per down task by tier (INT4, INT8, FP16): one
-// load per lane and round for INT4, two for INT8, four for FP16.
-constexpr int kDnRounds1 = kFL, kDnRounds2 = kFL / 2, kDnRounds3 = kFL / 4;
-constexpr int kFSpin = 1 << 16;          // polls of one h word before giving up
-constexpr float kTwo24 = 16777216.0f;
-static_assert(kFMaxItems <= kFT, "one slot id / h word per thread");
-// The task table in a plan: task count and zero slot (16 bytes), one 32-byte
-// header per workgroup, then kTaskIds slot ids per workgroup from a 256-byte
-// boundary.
-constexpr int kTaskIds = kFL * kFNPR;
-inline int64_t task_ids_offset(int grid) { return (16 + 32 * (int64_t)grid + 255) / 256 * 256; }
-static_assert(kFLPN == 16, "the fold pairs lanes 16 and 32 apart");
-static_assert(kFSW % kFT == 0, "the cross-wave fold gives each thread whole columns of the slice");
-
-struct FMap {
-  int n3, n2, n1;  // work items by tier
-  int w1, w2, w3;  // h tasks by tier (INT4, INT8, FP16)
-  int n_slices;
-  int e[6];        // ends of the six task regions in launch order
-};
-
-struct FTask {
-  int kind;  // 0 none, 1 h, 2 down
-  int tier;
-  int lo, hi;
-  int slice;
-};
-
-// K: 16-byte loads per lane and unit (a unit is d bytes of a neuron's gate and
-// up rows); a wave takes kFL / K units of an h task.
-// Launch order of the six task regions: (kind, tier) per region.
-constexpr int kOrderKind[6] = {1, 1, 1, 2, 2, 2};
-constexpr int kOrderTier[6] = {1, 2, 3, 1, 2, 3};
-
-template <int K>
-__device__ __forceinline__ FMap make_map(const int32_t* counts, int cap, int d) {
-  constexpr int U = kFWaves * (kFL / K);  // units per h task
-  FMap m;
-  work_counts(counts, cap, m.n3, m.n2, m.n1);
-  m.w1 = (m.n1 + U - 1) / U;
-  m.w2 = (m.n2 + U / 2 - 1) / (U / 2);
-  m.w3 = (m.n3 + U / 4 - 1) / (U / 4);
-  m.n_slices = (d + kFSW - 1) / kFSW;
-  const int u1 = (m.n1 + kDnRounds1 * kFNPR - 1) / (kDnRounds1 * kFNPR);
-  const int u2 = (m.n2 + kDnRounds2 * kFNPR - 1) / (kDnRounds2 * kFNPR);
-  const int u3 = (m.n3 + kDnRounds3 * kFNPR - 1) / (kDnRounds3 * kFNPR);
-  int end = 0;
-#pragma unroll
-  for (int r = 0; r < 6; ++r) {
-    const int tr = kOrderTier[r];
-    end += kOrderKind[r] == 1 ? (tr == 1 ? m.w1 : tr == 2 ? m.w2 : m.w3)
-                              : (tr == 1 ? u1 : tr == 2 ? u2 : u3) * m.n_slices;
-    m.e[r] = end;
-  }
-  return m;
-}
-
-// Task t in launch order. Work items are tier-major in the plan: FP16, INT8,
-// INT4.
-template <int K>
-__device__ __forceinline__ FTask decode(const FMap& m, int t) {
-  constexpr int U = kFWaves * (kFL / K);
-  FTask k;
-  k.kind = 0;
-  k.tier = 1;
-  k.lo = k.hi = 0;
-  k.slice = 0;
-  // region by comparisons (no indexed array: it would live in scratch memory)
-  int kind = 0, tier = 1, start = 0;
-#pragma unroll
-  for (int r = 5; r >= 0; --r) {
-    const int lo_r = r ? m.e[r - 1] : 0;
-    if (t >= lo_r && t < m.e[r]) {
-      kind = kOrderKind[r];
-      tier = kOrderTier[r];
-      start = lo_r;
-    }
-  }
-  if (kind == 0) return k;
-  const int q = t - start;
-  k.tier = tier;
-  // by value (a select between fields would index a stack copy of the map)
-  const int i1 = tier == 1, i2 = tier == 2, i3 = tier == 3;
-  const int base = i1 * (m.n3 + m.n2) + i2 * m.n3;
-  const int n = i1 * m.n1 + i2 * m.n2 + i3 * m.n3;
-  if (kind == 1) {
-    k.kind = 1;
-    const int per = tier == 1 ? U : tier == 2 ? U / 2 : U / 4;
-    k.lo = base + per * q;
-    k.hi = base + min(per * (q + 1), n);
-  } else {
-    k.kind = 2;
-    const int per = (tier == 1 ? kDnRounds1 : tier == 2 ? kDnRounds2 : kDnRounds3) * kFNPR;
-    // Runs in blocks of 8, slice-major within a block: workgroup b runs on
-    // XCD b % 8, so all slices of a run (which read the same scale lines of
-    // the run's records) land on one XCD and its L2.
-    const int nr = (n + per - 1) / per;
-    const int blk = q / (8 * m.n_slices);
-    const int within = q - blk * 8 * m.n_slices;
-    const int nb = min(8, nr - 8 * blk);
-    k.slice = within / nb;
-    const int run = 8 * blk + (within - k.slice * nb);
-    k.lo = base + per * run;
-    k.hi = base + min(per * (run + 1), n);
-  }
-  return k;
-}
 
 // Record data is read once per call: non-temporal loads keep it from
 // evicting what is reused (slot ids, x, h words, scales, the kernel's code).
@@ -796,48 +678,18 @@ hipError_t launch_fused(m2c_layer* L, const uint16_t* x, const int32_t* tasks, f
   return hipGetLastError();
 }
 
-// The task table, one wave per task: the 32-byte header {kind | tier << 8,
-// first work item, items, slice, then the tier pool's byte offset, first slot
-// id, slot count, record stride} and the slot ids in the order the FFN's
-// waves read them (a down task's items in work order; an h task's units at
-// entry (uw / 4) kFNPR + 4 w + uw % 4 for unit w UW + uw). The table starts
-// with the task count and the zero slot's byte offset.
+// The task table of a plan (the single cache unit's plan; the per-tier
+// arena's is written with the merge, from the pools' plans).
 template <int K>
 __global__ __launch_bounds__(256) void ffn_tasks_kernel(const int32_t* __restrict__ counts,
                                                         const int32_t* __restrict__ work_slot,
                                                         int cap, int d, int grid, SlotMap map,
                                                         int32_t* __restrict__ tasks,
                                                         int32_t* __restrict__ task_ids) {
-  constexpr int UW = kFL / K;
   const FMap m = make_map<K>(counts, cap, d);
-  const int n_tasks = m.e[5] < grid ? m.e[5] : grid;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    tasks[0] = n_tasks;
-    tasks[1] = (int32_t)map.zero;
-  }
-  const int lane = threadIdx.x & 63;
-  const int nw = (int)(gridDim.x * blockDim.x) >> 6;
-  for (int t = (int)(blockIdx.x * blockDim.x + threadIdx.x) >> 6; t < n_tasks; t += nw) {
-    const FTask k = decode<K>(m, t);
-    const int n = k.hi - k.lo;
-    if (lane == 0) {
-      const int tr = k.tier;
-      int4* h = reinterpret_cast<int4*>(tasks + 4) + 2 * t;
-      h[0] = make_int4(k.kind | (tr << 8), k.lo, n, k.slice);
-      h[1] = make_int4((int)map.base[tr], map.first[tr], map.count[tr], (int)map.stride[tr]);
-    }
-    int32_t* out = task_ids + (int64_t)t * kTaskIds;
-    if (k.kind == 2) {
-      for (int e = lane; e < n; e += 64) out[e] = work_slot[k.lo + e];
-    } else if (k.kind == 1) {
-      const int upi = k.tier == 3 ? 4 : k.tier == 2 ? 2 : 1;
-      const int item = lane / upi;  // unit lane of the task
-      if (lane < kFWaves * UW && item < n) {
-        const int w = lane / UW, uw = lane % UW;
-        out[(uw >> 2) * kFNPR + 4 * w + (uw & 3)] = work_slot[k.lo + item];
-      }
-    }
-  }
+  write_task_table<K>(m, grid, map, tasks, task_ids,
+                      (int)(blockIdx.x * blockDim.x + threadIdx.x) >> 6,
+                      (int)(gridDim.x * blockDim.x) >> 6, [&](int e) { return work_slot[e]; });
 }
 
 template <int K>
@@ -854,12 +706,12 @@ hipError_t launch_tasks(m2c_layer* L, uint8_t* plan, hipStream_t stream) {
   return hipGetLastError();
 }
 
-int loads_per_unit(int d) {
+}  // namespace
+
+int ffn_loads_per_unit(int d) {
   const int kneed = (d + 1023) / 1024;
   return kneed <= 1 ? 1 : kneed <= 2 ? 2 : kneed <= 4 ? 4 : 8;
 }
-
-}  // namespace
 
 bool ffn_fused_supported(const m2c_layer* L) {
   return L->desc.d_model <= 8192 && L->arena_bytes < ((int64_t)1 << 32);
@@ -870,7 +722,7 @@ int ffn_fused_grid(int d, int cap, int num_cus) {
   if (cap <= 0) return 0;
   // h tasks: at most cap / (FP16 neurons per task) + 1 per tier; down tasks:
   // per slice at most cap / (FP16 neurons per run) + 1 per tier
-  const int U = kFWaves * (kFL / loads_per_unit(d));
+  const int U = kFWaves * (kFL / ffn_loads_per_unit(d));
   const int64_t most = (int64_t)cap / (U / 4) + 3 +
                        (int64_t)((d + kFSW - 1) / kFSW) * (cap / (kDnRounds3 * kFNPR) + 3);
   return (int)most;
@@ -880,7 +732,7 @@ hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan
                             hipStream_t stream) {
   if (L->cap <= 0 || L->ffn_grid <= 0) return hipSuccess;
   const int32_t* tasks = reinterpret_cast<const int32_t*>(plan + L->layout.ffn_tasks);
-  switch (loads_per_unit(L->desc.d_model)) {
+  switch (ffn_loads_per_unit(L->desc.d_model)) {
     case 1: return launch_fused<1>(L, x, tasks, y, stream);
     case 2: return launch_fused<2>(L, x, tasks, y, stream);
     case 4: return launch_fused<4>(L, x, tasks, y, stream);
@@ -898,7 +750,7 @@ int64_t ffn_task_table_bytes(int grid) {
 
 hipError_t launch_ffn_tasks(m2c_layer* L, uint8_t* plan, hipStream_t stream) {
   if (!ffn_tasks_used(L) || L->ffn_grid <= 0) return hipSuccess;
-  switch (loads_per_unit(L->desc.d_model)) {
+  switch (ffn_loads_per_unit(L->desc.d_model)) {
     case 1: return launch_tasks<1>(L, plan, stream);
     case 2: return launch_tasks<2>(L, plan, stream);
     case 4: return launch_tasks<4>(L, plan, stream);

@@ -26,6 +26,7 @@
 // pool, the fast plan over that pool's list) -> plan_merge_kernel (the
 // three pools' plans merged by id into the caller's plan).
 #include "m2c_internal.h"
+#include "ffn_tasks.h"
 
 namespace m2c {
 
@@ -1017,11 +1018,49 @@ __device__ __forceinline__ void stage_ids(int32_t* __restrict__ dst, const int32
   }
 }
 
+// The batch-1 FFN's task table, written beside the merge (workgroups from
+// merge_blocks on), from the pools' plans: work item e of the merged plan is
+// entry e of the pools' required lists in tier order.
+struct TaskTable {
+  int32_t* tasks;
+  int32_t* task_ids;
+  int d, grid, cap;
+};
+
+template <int K>
+__device__ __forceinline__ void pool_task_table(const PoolPlans& pp, const SlotMap& map,
+                                                const TaskTable& tt, bool ab, int block,
+                                                int blocks) {
+  int n3 = ab ? 0 : pp.p[0].counts[M2C_CNT_REQ];
+  int n2 = ab ? 0 : pp.p[1].counts[M2C_CNT_REQ];
+  int n1 = ab ? 0 : pp.p[2].counts[M2C_CNT_REQ];
+  n3 = n3 < 0 ? 0 : n3 > tt.cap ? tt.cap : n3;
+  n2 = n2 < 0 ? 0 : n2 > tt.cap - n3 ? tt.cap - n3 : n2;
+  n1 = n1 < 0 ? 0 : n1 > tt.cap - n3 - n2 ? tt.cap - n3 - n2 : n1;
+  const FMap m = make_map_n<K>(n3, n2, n1, tt.d);
+  const int f3 = map.first[3], f2 = map.first[2], f1 = map.first[1];
+  write_task_table<K>(m, tt.grid, map, tt.tasks, tt.task_ids,
+                      (int)(block * blockDim.x + threadIdx.x) >> 6,
+                      (int)(blocks * blockDim.x) >> 6, [&](int e) {
+                        return e < n3        ? pp.p[0].req_slot[e] + f3
+                               : e < n3 + n2 ? pp.p[1].req_slot[e - n3] + f2
+                                             : pp.p[2].req_slot[e - n3 - n2] + f1;
+                      });
+}
+
+// Workgroups [0, merge_blocks): the merge; the rest (if any): the task table.
+template <int K>
 __global__ __launch_bounds__(kMergeThreads) void plan_merge_kernel(PoolPlans pp, PlanPtrs out,
                                                                     SlotMap map,
-                                                                    const int32_t* __restrict__ abort_word) {
+                                                                    const int32_t* __restrict__ abort_word,
+                                                                    int merge_blocks, TaskTable tt) {
   __shared__ int32_t s_req[kMergeIds], s_fill[kMergeIds];
   const bool ab = *abort_word != 0;
+  if ((int)blockIdx.x >= merge_blocks) {
+    pool_task_table<K>(pp, map, tt, ab, (int)blockIdx.x - merge_blocks,
+                       (int)gridDim.x - merge_blocks);
+    return;
+  }
   int nr[3], nf[3], ne[3];
 #pragma unroll
   for (int q = 0; q < 3; ++q) {
@@ -1029,7 +1068,7 @@ __global__ __launch_bounds__(kMergeThreads) void plan_merge_kernel(PoolPlans pp,
     nf[q] = ab ? 0 : pp.p[q].counts[M2C_CNT_FILL];
     ne[q] = ab ? 0 : pp.p[q].counts[M2C_CNT_EVICT];
   }
-  const int tid = blockIdx.x * blockDim.x + threadIdx.x, nth = gridDim.x * blockDim.x;
+  const int tid = blockIdx.x * blockDim.x + threadIdx.x, nth = merge_blocks * blockDim.x;
   if (tid < M2C_NCOUNTS) {
     int v = 0;
     if (ab)
@@ -1174,10 +1213,25 @@ hipError_t launch_plan(m2c_layer* L, const uint8_t* tier_map, int batch, int ste
   if (e != hipSuccess) return e;
   int blocks = (L->cap + kMergeThreads - 1) / kMergeThreads;
   blocks = blocks < 1 ? 1 : blocks > 64 ? 64 : blocks;
-  hipLaunchKernelGGL(plan_merge_kernel, dim3(blocks), dim3(kMergeThreads), 0, stream, pp, P, L->map,
-                     L->plan_abort);
-  e = hipGetLastError();
-  return e == hipSuccess ? launch_ffn_tasks(L, plan, stream) : e;
+  // the FFN's task table in the same launch, from the pools' plans (one wave
+  // per task, as in the single unit's table kernel)
+  TaskTable tt{};
+  int tblocks = 0;
+  if (ffn_tasks_used(L) && L->ffn_grid > 0) {
+    int32_t* tasks = reinterpret_cast<int32_t*>(plan + L->layout.ffn_tasks);
+    tt = {tasks, tasks + task_ids_offset(L->ffn_grid) / 4, L->desc.d_model, L->ffn_grid,
+          L->cap};
+    tblocks = (L->ffn_grid + 3) / 4;
+    tblocks = tblocks < 1 ? 1 : tblocks > 256 ? 256 : tblocks;
+  }
+  const dim3 g(blocks + tblocks), b(kMergeThreads);
+  switch (ffn_loads_per_unit(L->desc.d_model)) {
+    case 1: hipLaunchKernelGGL(plan_merge_kernel<1>, g, b, 0, stream, pp, P, L->map, L->plan_abort, blocks, tt); break;
+    case 2: hipLaunchKernelGGL(plan_merge_kernel<2>, g, b, 0, stream, pp, P, L->map, L->plan_abort, blocks, tt); break;
+    case 4: hipLaunchKernelGGL(plan_merge_kernel<4>, g, b, 0, stream, pp, P, L->map, L->plan_abort, blocks, tt); break;
+    default: hipLaunchKernelGGL(plan_merge_kernel<8>, g, b, 0, stream, pp, P, L->map, L->plan_abort, blocks, tt); break;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_reset(m2c_layer* L, hipStream_t stream) {

@@ -166,6 +166,7 @@ int ffn_fused_grid(int d_model, int cap, int num_cus);  // workgroups (and gen c
 // one (batch-1 FFN calls use that kernel), its bytes for a grid, and the
 // kernel that writes it from the plan's counts and work order.
 bool ffn_tasks_used(const m2c_layer* L);
+int ffn_loads_per_unit(int d);  // K of the one-launch FFN: 16-byte loads per lane and unit
 int64_t ffn_task_table_bytes(int grid);
 hipError_t launch_ffn_tasks(m2c_layer* L, uint8_t* plan, hipStream_t stream);
 hipError_t launch_ffn_fused(m2c_layer* L, const uint16_t* x, const uint8_t* plan, float* y,

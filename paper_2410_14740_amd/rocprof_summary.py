@@ -32,7 +32,7 @@ import re
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-FFN_SOURCES = ("csrc/k_ffn_fused.hip", "csrc/ffn_device.h")
+FFN_SOURCES = ("csrc/k_ffn_fused.hip", "csrc/ffn_tasks.h", "csrc/ffn_device.h")
 FFN_KERNELS = ("ffn_fused_kernel",)
 
 
