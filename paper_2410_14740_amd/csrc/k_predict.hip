@@ -74,7 +74,8 @@ __global__ __launch_bounds__(256) void pred_z_kernel(const uint16_t* __restrict_
   }
   for (int off = L >> 1; off >= 1; off >>= 1) {
 #pragma unroll
-    for (int b = 0; b < kPredBatch; ++b) acc[b] = acc[b] + __shfl_xor(acc[b], off);
+    for (int b = 0; b < kPredBatch; ++b)
+      if (b < nb) acc[b] = acc[b] + __shfl_xor(acc[b], off);  // rows of the pass only
   }
   if (valid && sl == 0) {
 #pragma unroll
@@ -121,7 +122,8 @@ __global__ __launch_bounds__(256) void pred_s_kernel(const uint16_t* __restrict_
     }
     for (int off = L >> 1; off >= 1; off >>= 1) {
 #pragma unroll
-      for (int b = 0; b < kPredBatch; ++b) acc[b] = acc[b] + __shfl_xor(acc[b], off);
+      for (int b = 0; b < kPredBatch; ++b)
+        if (b < nb) acc[b] = acc[b] + __shfl_xor(acc[b], off);  // rows of the pass only
     }
     if (valid && sl == 0) {
 #pragma unroll
