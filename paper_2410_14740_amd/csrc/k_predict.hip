@@ -84,39 +84,53 @@ __global__ __launch_bounds__(256) void pred_z_kernel(const uint16_t* __restrict_
   }
 }
 
-// s[b][i] = dot(B[i], z[b]) (+ bias[i]); z of the pass staged in LDS.
+// s[b][i] = dot(B[i], z[b]) (+ bias[i]); z of the pass staged in LDS. A
+// wave takes RB row groups (64 / L rows each) in one pass: their rows' loads
+// go out before z is staged, so the two share one memory round trip. A row
+// has at most 2 L chunks (r <= 1024): a lane's chunks are sl and, when it
+// exists, sl + L, in that order (the canonical order of its partial).
+template <int kPredRB>
 __global__ __launch_bounds__(256) void pred_s_kernel(const uint16_t* __restrict__ Bm,
                                                      const float* __restrict__ z,
                                                      const float* __restrict__ bias, int d_ff,
                                                      int r, int nb, int L, int64_t s_stride,
                                                      float* __restrict__ s) {
   extern __shared__ float zs[];  // [nb][r]
-  for (int t = threadIdx.x; t < nb * r; t += blockDim.x) zs[t] = z[t];
-  __syncthreads();
   const int lane = threadIdx.x & 63;
   const int rpw = 64 / L;
   const int sl = lane & (L - 1);
   const int gw = __builtin_amdgcn_readfirstlane((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
-  const int nw = (gridDim.x * blockDim.x) >> 6;
   const int chunks = r >> 3;
-  for (int base = gw * rpw; base < d_ff; base += nw * rpw) {
-    const int i = base + lane / L;
-    const bool valid = i < d_ff;
+  const bool two = sl + L < chunks;
+  uint4 bv[kPredRB][2];
+  int row[kPredRB];
+#pragma unroll
+  for (int rb = 0; rb < kPredRB; ++rb) {
+    row[rb] = (gw * kPredRB + rb) * rpw + lane / L;
+    const uint4* brow =
+        reinterpret_cast<const uint4*>(Bm + (int64_t)min(row[rb], d_ff - 1) * r);
+    bv[rb][0] = brow[sl];
+    bv[rb][1] = brow[two ? sl + L : sl];
+  }
+  for (int t = threadIdx.x; t < nb * r; t += blockDim.x) zs[t] = z[t];
+  __syncthreads();
+#pragma unroll
+  for (int rb = 0; rb < kPredRB; ++rb) {
     float acc[kPredBatch];
 #pragma unroll
     for (int b = 0; b < kPredBatch; ++b) acc[b] = 0.0f;
-    if (valid) {
-      const uint4* brow = reinterpret_cast<const uint4*>(Bm + (int64_t)i * r);
-      for (int c = sl; c < chunks; c += L) {
-        float bf[8];
-        unpack8(brow[c], bf);
 #pragma unroll
-        for (int b = 0; b < kPredBatch; ++b) {
-          if (b < nb) {
-            const float* zb = zs + b * r + 8 * c;
+    for (int h = 0; h < 2; ++h) {
+      if (h == 1 && !two) break;
+      const int c = sl + h * L;
+      float bf[8];
+      unpack8(bv[rb][h], bf);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[b] = __builtin_fmaf(bf[e], zb[e], acc[b]);
-          }
+      for (int b = 0; b < kPredBatch; ++b) {
+        if (b < nb) {
+          const float* zb = zs + b * r + 8 * c;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[b] = __builtin_fmaf(bf[e], zb[e], acc[b]);
         }
       }
     }
@@ -125,7 +139,8 @@ __global__ __launch_bounds__(256) void pred_s_kernel(const uint16_t* __restrict_
       for (int b = 0; b < kPredBatch; ++b)
         if (b < nb) acc[b] = acc[b] + __shfl_xor(acc[b], off);  // rows of the pass only
     }
-    if (valid && sl == 0) {
+    const int i = row[rb];
+    if (i < d_ff && sl == 0) {
 #pragma unroll
       for (int b = 0; b < kPredBatch; ++b) {
         if (b < nb) {
@@ -176,13 +191,22 @@ hipError_t launch_predict(const m2c_layer* L, const uint16_t* x, int batch, floa
       launch_z<32>(bz, lz, stream, L->pred_a, xb, d, r, nb, Lz, zb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    // one row group per wave: every wave makes a single pass
+    // RB row groups per wave, every wave makes a single pass; two when the
+    // grid would otherwise hold many more workgroups than the chip (70B:
+    // 54.5 -> 52.0 us per predict call; 7B, with fewer rows, is faster with one)
     const int rows_s = 64 / Ls;
-    const int waves_s = (d_ff + rows_s - 1) / rows_s;
+    const int groups = (d_ff + rows_s - 1) / rows_s;
+    const int rb = groups >= 16384 ? 2 : 1;
+    const int waves_s = (groups + rb - 1) / rb;
     const int blocks = (waves_s + 3) / 4;
-    hipLaunchKernelGGL(pred_s_kernel, dim3(blocks), dim3(256), (size_t)nb * r * sizeof(float),
-                       stream, L->pred_b, zb, L->bias, d_ff, r, nb, Ls, (int64_t)d_ff,
-                       scores + (int64_t)b0 * d_ff);
+    if (rb == 2)
+      hipLaunchKernelGGL(pred_s_kernel<2>, dim3(blocks), dim3(256), (size_t)nb * r * sizeof(float),
+                         stream, L->pred_b, zb, L->bias, d_ff, r, nb, Ls, (int64_t)d_ff,
+                         scores + (int64_t)b0 * d_ff);
+    else
+      hipLaunchKernelGGL(pred_s_kernel<1>, dim3(blocks), dim3(256), (size_t)nb * r * sizeof(float),
+                         stream, L->pred_b, zb, L->bias, d_ff, r, nb, Ls, (int64_t)d_ff,
+                         scores + (int64_t)b0 * d_ff);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
