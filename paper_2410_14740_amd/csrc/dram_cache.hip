@@ -9,9 +9,10 @@
 // fast the loads go: for the acquired layer l the window W(l) = l .. l + a
 // (mod L) is made resident in order (l first, the consumer waits for it);
 // a missing layer takes the lowest empty slot, else the slot whose layer is
-// outside W(l), loaded, not held by a consumer, and used furthest in the
-// future in the cyclic layer order, the largest (layer - l) mod L. A
-// look-ahead load with no slot to give up is skipped.
+// outside W(l), not held by a consumer, and used furthest in the future in
+// the cyclic layer order, the largest (layer - l) mod L (if its own load is
+// still running, the acquire waits for it). A look-ahead load with no slot
+// to give up is skipped.
 //
 // A slot's bytes may still be read by GPU fills already enqueued; the
 // consumer attaches a HIP event when it releases the slot, and the loader
@@ -153,42 +154,50 @@ void loader_main(m2c_dram* D) {
 
 // Makes layer m resident or queued for the window of layer l (lock held).
 // Returns false if the layer could not be placed.
-bool ensure(m2c_dram* D, int l, int m) {
+// A victim that is still loading is waited for (lk is the cache's lock), not
+// passed over, so that the choice does not depend on how fast loads go.
+bool ensure(m2c_dram* D, std::unique_lock<std::mutex>& lk, int l, int m) {
   const int L = D->desc.n_layers, a = D->desc.lookahead;
-  if (D->where[m] != -1) return true;
-  int pick = -1;
-  for (int q = 0; q < (int)D->slots.size(); ++q)
-    if (D->slots[q].layer < 0) {
-      pick = q;
-      break;
-    }
-  int old = -1;
-  if (pick < 0) {
-    int best = -1;
-    for (int q = 0; q < (int)D->slots.size(); ++q) {
-      const m2c_dram::Slot& s = D->slots[q];
-      if (!s.ready || s.pins > 0) continue;
-      const int dist = ((s.layer - l) % L + L) % L;
-      if (dist <= a) continue;  // inside the window
-      if (dist > best) {
-        best = dist;
+  for (;;) {
+    if (D->where[m] != -1) return true;
+    int pick = -1;
+    for (int q = 0; q < (int)D->slots.size(); ++q)
+      if (D->slots[q].layer < 0) {
         pick = q;
+        break;
       }
+    int old = -1;
+    if (pick < 0) {
+      int best = -1;
+      for (int q = 0; q < (int)D->slots.size(); ++q) {
+        const m2c_dram::Slot& s = D->slots[q];
+        if (s.pins > 0) continue;
+        const int dist = ((s.layer - l) % L + L) % L;
+        if (dist <= a) continue;  // inside the window
+        if (dist > best) {
+          best = dist;
+          pick = q;
+        }
+      }
+      if (pick < 0) return false;
+      if (!D->slots[pick].ready) {  // its load ends on its own (ready is set even on error)
+        D->cv.wait(lk);
+        continue;
+      }
+      old = D->slots[pick].layer;
+      D->where[old] = -1;
+      D->st.evictions++;
     }
-    if (pick < 0) return false;
-    old = D->slots[pick].layer;
-    D->where[old] = -1;
-    D->st.evictions++;
+    m2c_dram::Slot& s = D->slots[pick];
+    s.layer = m;
+    s.ready = false;
+    D->where[m] = pick;
+    D->queue.push_back({pick, m});
+    D->log_loaded.push_back(m);
+    D->log_evicted.push_back(old);
+    D->cv.notify_all();
+    return true;
   }
-  m2c_dram::Slot& s = D->slots[pick];
-  s.layer = m;
-  s.ready = false;
-  D->where[m] = pick;
-  D->queue.push_back({pick, m});
-  D->log_loaded.push_back(m);
-  D->log_evicted.push_back(old);
-  D->cv.notify_all();
-  return true;
 }
 
 }  // namespace
@@ -209,8 +218,8 @@ m2c_status dram_acquire(m2c_dram* D, int layer, const uint8_t** data, int* slot)
   const auto t0 = std::chrono::steady_clock::now();
   for (;;) {
     // the layer in use first, then the look-ahead in order
-    const bool placed = ensure(D, layer, layer);
-    for (int j = 1; j <= D->desc.lookahead; ++j) ensure(D, layer, (layer + j) % L);
+    const bool placed = ensure(D, lk, layer, layer);
+    for (int j = 1; j <= D->desc.lookahead; ++j) ensure(D, lk, layer, (layer + j) % L);
     if (placed) break;
     D->cv.wait(lk);  // every slot is held: wait for a release
   }
